@@ -1,0 +1,284 @@
+"""Seeded synthetic inputs and the workload table for SpecTrain stage steps.
+
+This module is shared by the CPU oracle and the HIP path. It holds no step of
+the method: only the description of each workload (shapes, learning rate,
+momentum, pipeline position), the flat parameter layout both sides agree on,
+and seeded random draws of initial weights, stage inputs, upstream gradients
+and labels.
+
+Inputs stand in for the paper's datasets (CIFAR-10 images, IMDb reviews;
+Section 4.1), which are not used: every array here is drawn from a seeded
+normal or uniform generator with the shape of the corresponding workload.
+
+bf16 workloads receive their floating inputs already rounded once to bf16
+(round-to-nearest-even) and stored as the float32 value of that bf16 number,
+so both sides see identical input bits.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Tuple
+
+import numpy as np
+
+KINDS = ("fc", "conv3x3", "bottleneck", "transformer", "reslstm")
+INIT_SEED = 1809
+DATA_SEED = 2839
+
+
+@dataclasses.dataclass(frozen=True)
+class StageSpec:
+    """One pipeline stage: what it computes and where it sits.
+
+    dims meaning per kind:
+      fc:          (in_features, out_features, hidden)   widths in, hidden*(L-1), out
+      conv3x3:     (C_in, C_out, H, W)                    L layers, first C_in->C_out
+      bottleneck:  (C, C_mid, H, W)                       L blocks
+      transformer: (d_model, heads, ffn, seq)             L encoder layers
+      reslstm:     (input, hidden, T, vocab)              L layers, vocab used by a CE head
+    """
+
+    kind: str
+    dtype: str              # "fp32" or "bf16": the compute dtype of operands
+    head: str               # "none" (dY supplied) or "ce" (labels supplied)
+    stage_index: int        # k, 0-based
+    num_stages: int         # N
+    batch: int
+    num_layers: int
+    dims: Tuple[int, ...]
+    lr: float
+    momentum: float
+
+    # ----- shapes -------------------------------------------------------
+    def fc_widths(self) -> List[int]:
+        fin, fout, hid = self.dims[0], self.dims[1], self.dims[2]
+        return [fin] + [hid] * (self.num_layers - 1) + [fout]
+
+    def input_shape(self) -> Tuple[int, ...]:
+        d = self.dims
+        if self.kind == "fc":
+            return (self.batch, d[0])
+        if self.kind == "conv3x3":
+            return (self.batch, d[2], d[3], d[0])          # NHWC
+        if self.kind == "bottleneck":
+            return (self.batch, d[2], d[3], d[0])          # NHWC
+        if self.kind == "transformer":
+            return (self.batch, d[3], d[0])                # [B, S, d]
+        if self.kind == "reslstm":
+            return (d[2], self.batch, d[0])                # time-major [T, B, I]
+        raise ValueError(self.kind)
+
+    def output_shape(self) -> Tuple[int, ...]:
+        """Shape of Y for a stage without a loss head (the tensor dY matches)."""
+        d = self.dims
+        if self.kind == "fc":
+            return (self.batch, d[1])
+        if self.kind == "conv3x3":
+            return (self.batch, d[2], d[3], d[1])
+        if self.kind == "bottleneck":
+            return (self.batch, d[2], d[3], d[0])
+        if self.kind == "transformer":
+            return (self.batch, d[3], d[0])
+        if self.kind == "reslstm":
+            return (d[2], self.batch, d[1])
+        raise ValueError(self.kind)
+
+    def label_shape(self) -> Tuple[int, ...]:
+        if self.kind == "fc":
+            return (self.batch,)
+        if self.kind == "reslstm":
+            return (self.dims[2], self.batch)
+        raise ValueError(f"{self.kind} has no loss head")
+
+    def num_classes(self) -> int:
+        if self.kind == "fc":
+            return self.dims[1]
+        if self.kind == "reslstm":
+            return self.dims[3]
+        raise ValueError(self.kind)
+
+    def grad_count(self) -> int:
+        """Samples (or tokens) the synthetic upstream gradient is averaged over."""
+        if self.kind == "transformer":
+            return self.batch * self.dims[3]
+        if self.kind == "reslstm":
+            return self.batch * self.dims[2]
+        return self.batch
+
+
+def param_layout(spec: StageSpec) -> List[Tuple[str, Tuple[int, ...], str]]:
+    """Ordered (name, shape, init) list: the flat parameter order of a stage.
+
+    init is "he" (normal, variance 2/fan_in with fan_in the product of all but
+    the first dimension), "zeros" or "ones". Linear weights are [out, in]
+    row-major, conv filters [C_out, kh, kw, C_in], LSTM gate blocks (i, f, g, o).
+    """
+    d, L = spec.dims, spec.num_layers
+    out: List[Tuple[str, Tuple[int, ...], str]] = []
+    if spec.kind == "fc":
+        w = spec.fc_widths()
+        for l in range(L):
+            out.append((f"fc{l}.weight", (w[l + 1], w[l]), "he"))
+            out.append((f"fc{l}.bias", (w[l + 1],), "zeros"))
+    elif spec.kind == "conv3x3":
+        cin, cout = d[0], d[1]
+        for l in range(L):
+            out.append((f"conv{l}.weight", (cout, 3, 3, cin if l == 0 else cout), "he"))
+    elif spec.kind == "bottleneck":
+        c, cm = d[0], d[1]
+        for l in range(L):
+            out.append((f"block{l}.conv1.weight", (cm, 1, 1, c), "he"))
+            out.append((f"block{l}.conv2.weight", (cm, 3, 3, cm), "he"))
+            out.append((f"block{l}.conv3.weight", (c, 1, 1, cm), "he"))
+    elif spec.kind == "transformer":
+        dm, ffn = d[0], d[2]
+        for l in range(L):
+            p = f"layer{l}."
+            out += [
+                (p + "attn.qkv.weight", (3 * dm, dm), "he"),
+                (p + "attn.qkv.bias", (3 * dm,), "zeros"),
+                (p + "attn.out.weight", (dm, dm), "he"),
+                (p + "attn.out.bias", (dm,), "zeros"),
+                (p + "ln1.weight", (dm,), "ones"),
+                (p + "ln1.bias", (dm,), "zeros"),
+                (p + "ffn1.weight", (ffn, dm), "he"),
+                (p + "ffn1.bias", (ffn,), "zeros"),
+                (p + "ffn2.weight", (dm, ffn), "he"),
+                (p + "ffn2.bias", (dm,), "zeros"),
+                (p + "ln2.weight", (dm,), "ones"),
+                (p + "ln2.bias", (dm,), "zeros"),
+            ]
+    elif spec.kind == "reslstm":
+        inp, hid, _, vocab = d
+        for l in range(L):
+            out.append((f"lstm{l}.weight_x", (4 * hid, inp if l == 0 else hid), "he"))
+            out.append((f"lstm{l}.weight_h", (4 * hid, hid), "he"))
+            out.append((f"lstm{l}.bias", (4 * hid,), "zeros"))
+        if spec.head == "ce":
+            out.append(("vocab.weight", (vocab, hid), "he"))
+            out.append(("vocab.bias", (vocab,), "zeros"))
+    else:
+        raise ValueError(spec.kind)
+    return out
+
+
+def num_params(spec: StageSpec) -> int:
+    return int(sum(int(np.prod(s)) for _, s, _ in param_layout(spec)))
+
+
+# ----------------------------------------------------------------------------
+# Workload table
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    stages: Tuple[StageSpec, ...]   # all simulated stages (one, or a whole pipeline)
+    steps: int = 20                 # mini-batches per trajectory (one update each)
+
+
+def _mlp3(batch=32, widths=(784, 256, 256, 10), lr=0.01, steps=20) -> Workload:
+    n = len(widths) - 1
+    stages = []
+    for k in range(n):
+        last = k == n - 1
+        stages.append(StageSpec("fc", "fp32", "ce" if last else "none", k, n, batch, 1,
+                                (widths[k], widths[k + 1], widths[k + 1]), lr, 0.9))
+    return Workload("mlp3", tuple(stages), steps)
+
+
+def _single(name, kind, dtype, head, k, N, batch, L, dims, lr, steps=20) -> Workload:
+    return Workload(name, (StageSpec(kind, dtype, head, k, N, batch, L, tuple(dims), lr, 0.9),), steps)
+
+
+# Full-size workloads: the five stage configurations of the benchmark.
+# Learning rates for the four paper models follow Section 4.1 (VGG16 2e-3,
+# ResNet-152 2e-2, Transformer 5e-5, Residual LSTM 5e-3); momentum 0.9 for all.
+WORKLOADS: Dict[str, Workload] = {
+    "mlp3": _mlp3(),
+    "vgg_conv": _single("vgg_conv", "conv3x3", "bf16", "none", 1, 4, 128, 4, (256, 512, 8, 8), 2e-3),
+    "resnet_bottleneck": _single("resnet_bottleneck", "bottleneck", "bf16", "none", 2, 4, 64, 8,
+                                 (1024, 256, 14, 14), 2e-2),
+    "transformer_enc": _single("transformer_enc", "transformer", "bf16", "none", 1, 4, 64, 3,
+                               (512, 8, 2048, 128), 5e-5),
+    "reslstm": _single("reslstm", "reslstm", "bf16", "ce", 3, 4, 64, 2, (1024, 1024, 35, 10000), 5e-3),
+}
+
+# Reduced workloads of the same structure for parity runs the oracle finishes
+# in seconds; sizes are chosen to cover several GEMM tiles plus ragged tails.
+SMALL_WORKLOADS: Dict[str, Workload] = {
+    "mlp3_small": _mlp3(batch=7, widths=(37, 50, 21, 10), lr=0.05),
+    "vgg_conv_small": _single("vgg_conv_small", "conv3x3", "bf16", "none", 1, 4, 3, 3, (24, 40, 7, 9), 1e-3),
+    "resnet_bottleneck_small": _single("resnet_bottleneck_small", "bottleneck", "bf16", "none", 2, 4, 2, 2,
+                                       (72, 24, 7, 5), 1e-3),
+    "transformer_enc_small": _single("transformer_enc_small", "transformer", "bf16", "none", 1, 4, 3, 2,
+                                     (64, 2, 136, 40), 2e-3),
+    "reslstm_small": _single("reslstm_small", "reslstm", "bf16", "ce", 3, 4, 5, 2, (48, 48, 6, 104), 5e-2),
+}
+
+ALL_WORKLOADS: Dict[str, Workload] = {**WORKLOADS, **SMALL_WORKLOADS}
+
+
+# ----------------------------------------------------------------------------
+# Seeded draws
+# ----------------------------------------------------------------------------
+
+def to_bf16_values(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (nearest, ties to even); return them as float32."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32)
+
+
+def bf16_bits(x32: np.ndarray) -> np.ndarray:
+    """Upper 16 bits of float32 values that are already bf16 numbers."""
+    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32)
+    if np.any(u & 0xFFFF):
+        raise ValueError("values are not bf16-representable")
+    return (u >> 16).astype(np.uint16)
+
+
+def _rng(*key: int) -> np.random.Generator:
+    return np.random.default_rng([int(k) for k in key])
+
+
+def initial_params(spec: StageSpec, seed: int = INIT_SEED) -> np.ndarray:
+    """Flat float32 initial parameters W0 in the order of param_layout."""
+    parts = []
+    for i, (_, shape, init) in enumerate(param_layout(spec)):
+        n = int(np.prod(shape))
+        if init == "he":
+            fan_in = int(np.prod(shape[1:]))
+            r = _rng(seed, spec.stage_index, i)
+            parts.append((r.standard_normal(n) * np.sqrt(2.0 / fan_in)).astype(np.float32))
+        elif init == "zeros":
+            parts.append(np.zeros(n, np.float32))
+        elif init == "ones":
+            parts.append(np.ones(n, np.float32))
+        else:
+            raise ValueError(init)
+    return np.concatenate(parts).astype(np.float32)
+
+
+def _input_scale(spec: StageSpec) -> float:
+    return 0.02 if spec.kind == "transformer" else 1.0
+
+
+def stage_input(spec: StageSpec, mb: int, seed: int = DATA_SEED) -> np.ndarray:
+    """X for mini-batch mb at this stage (float32; bf16 values for bf16 stages)."""
+    r = _rng(seed, spec.stage_index, mb, 0)
+    x = (r.standard_normal(spec.input_shape()) * _input_scale(spec)).astype(np.float32)
+    return to_bf16_values(x) if spec.dtype == "bf16" else x
+
+
+def upstream_grad(spec: StageSpec, mb: int, seed: int = DATA_SEED) -> np.ndarray:
+    """dL/dY for a stage without a loss head: N(0,1)/count, in the stage dtype."""
+    r = _rng(seed, spec.stage_index, mb, 1)
+    g = (r.standard_normal(spec.output_shape()) / spec.grad_count()).astype(np.float32)
+    return to_bf16_values(g) if spec.dtype == "bf16" else g
+
+
+def labels(spec: StageSpec, mb: int, seed: int = DATA_SEED) -> np.ndarray:
+    """Integer targets, uniform in [0, classes), for a stage with a CE head."""
+    r = _rng(seed, spec.stage_index, mb, 2)
+    return r.integers(0, spec.num_classes(), size=spec.label_shape(), dtype=np.int64).astype(np.int32)
