@@ -1,0 +1,170 @@
+/*
+ * spectrain.h - C ABI of one SpecTrain pipeline stage on an MI355X (gfx950).
+ *
+ * SpecTrain (Chen, Yang, Cheng: "Efficient and Robust Parallel DNN Training
+ * through Model Parallelism on Multi-GPU Platform") runs each pipeline stage's
+ * forward and backward pass against weights predicted for the moment the
+ * mini-batch completes its round trip (Section 3.2):
+ *
+ *   Eq. 1  v_t = gamma * v_{t-1} + (1 - gamma) * g_t          smoothed gradient
+ *          W_{t+1} = W_t - eta * v_t                          momentum update
+ *   Eq. 4  What_{t+s} = W_t - s * eta * v_{t-1}               s-step prediction
+ *   Eq. 5  s = floor(k/2) + N - k - 1                          forward pass, stage k of N
+ *   Eq. 6  s = floor(k/2)                                      backward pass
+ *
+ * A stage owns its master weights W, smoothed gradient v and gradient g (all
+ * float32, one flat arena each), two predicted-weight buffers in the compute
+ * dtype (slot 0 for the next forward, slot 1 for the next backward) and a ring
+ * of activation stashes, one per mini-batch in flight (at most N - k in the
+ * one-forward-one-backward order of Section 3.1).
+ *
+ * Conventions for every function below:
+ *  - The return value is a status code (SPECTRAIN_OK = 0). No function throws
+ *    or aborts; on failure spectrain_last_error() describes the cause.
+ *  - Device work is enqueued asynchronously on the HIP stream given to
+ *    spectrain_stage_create, in call order. Only the functions documented as
+ *    synchronising wait for it.
+ *  - "device pointer" arguments point to GPU memory owned by the caller; the
+ *    library never frees them. Host pointers are only read during the call.
+ *  - A stage handle may be used from one host thread at a time.
+ *
+ * Parameter order (the flat float32 array that crosses this boundary), per
+ * kind, repeated per layer l = 0 .. num_layers-1:
+ *   FC          weight [out, in] row-major, bias [out]
+ *   CONV3X3     filter [C_out, 3, 3, C_in]                  (no bias)
+ *   BOTTLENECK  conv1 [C_mid,1,1,C], conv2 [C_mid,3,3,C_mid], conv3 [C,1,1,C_mid]
+ *   TRANSFORMER qkv.weight [3d, d], qkv.bias [3d], out.weight [d, d], out.bias [d],
+ *               ln1.weight [d], ln1.bias [d], ffn1.weight [F, d], ffn1.bias [F],
+ *               ffn2.weight [d, F], ffn2.bias [d], ln2.weight [d], ln2.bias [d]
+ *   RESLSTM     weight_x [4H, I], weight_h [4H, H], bias [4H], gate blocks (i, f, g, o);
+ *               then, with a CE head, vocab.weight [V, H], vocab.bias [V]
+ *
+ * Activation layouts (compute dtype; bf16 is stored as raw 16-bit bf16):
+ *   FC [B, features]; CONV3X3 and BOTTLENECK NHWC [B, H, W, C];
+ *   TRANSFORMER [B, S, d]; RESLSTM time-major [T, B, H]; labels int32
+ *   [B] (FC) or [T, B] (RESLSTM) with values in [0, classes); a label outside
+ *   that range makes the reported loss NaN.
+ */
+#ifndef SPECTRAIN_H
+#define SPECTRAIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPECTRAIN_ABI_VERSION 1u
+
+/* Status codes. */
+enum {
+  SPECTRAIN_OK = 0,
+  SPECTRAIN_EINVAL = 1,     /* bad argument or descriptor */
+  SPECTRAIN_ENOMEM = 2,     /* device allocation failed */
+  SPECTRAIN_EHIP = 3,       /* a HIP runtime call failed; message carries its error string */
+  SPECTRAIN_ESTATE = 4,     /* call out of order for the stage's current state */
+  SPECTRAIN_ENONFINITE = 5  /* the last update produced a non-finite W or v */
+};
+
+typedef struct spectrain_stage* spectrain_stage_t;   /* opaque, owned by the library */
+
+typedef enum { SPECTRAIN_FP32 = 0, SPECTRAIN_BF16 = 1 } spectrain_dtype;
+
+typedef enum {
+  SPECTRAIN_KIND_FC = 0,           /* dims: in, out, hidden; widths in, hidden x (L-1), out */
+  SPECTRAIN_KIND_CONV3X3 = 1,      /* dims: C_in, C_out, H, W; 3x3 stride 1 pad 1, ReLU */
+  SPECTRAIN_KIND_BOTTLENECK = 2,   /* dims: C, C_mid, H, W; 1x1-3x3-1x1, identity skip, ReLU */
+  SPECTRAIN_KIND_TRANSFORMER = 3,  /* dims: d_model, heads, ffn, seq; post-LN encoder layer */
+  SPECTRAIN_KIND_RESLSTM = 4       /* dims: input, hidden, T, vocab; residual LSTM layers */
+} spectrain_kind;
+
+typedef enum {
+  SPECTRAIN_HEAD_NONE = 0,  /* the caller passes dL/dY to backward */
+  SPECTRAIN_HEAD_CE = 1     /* mean softmax cross-entropy over rows; caller passes int32 labels */
+} spectrain_head;
+
+typedef struct {
+  uint32_t abi_version;     /* SPECTRAIN_ABI_VERSION */
+  int32_t kind;             /* spectrain_kind */
+  int32_t dtype;            /* spectrain_dtype: operand/activation format; W, v, g are float32 */
+  int32_t head;             /* spectrain_head: CE allowed for FC and RESLSTM only */
+  int32_t stage_index;      /* k, 0-based, 0 <= k < num_stages */
+  int32_t num_stages;       /* N >= 1 */
+  int32_t batch;            /* mini-batch size B >= 1 */
+  int32_t num_layers;       /* L >= 1 (layers, blocks or LSTM layers) */
+  int32_t dims[8];          /* kind-specific, see spectrain_kind; unused entries 0 */
+  float lr;                 /* eta > 0 */
+  float momentum;           /* gamma, 0 < gamma <= 1 */
+} spectrain_stage_desc;
+
+/* Eq. 5 (is_forward != 0) or Eq. 6: version difference s for stage k of N.
+ * Returns s >= 0, or -1 when k < 0, k >= N or N < 1. */
+int32_t spectrain_version_difference(int32_t k, int32_t N, int32_t is_forward);
+
+/* Create a stage. W0_host: n_params float32 values in the parameter order
+ * above (n_params must equal the kind's count, else EINVAL). hip_stream: a
+ * hipStream_t (NULL = the null stream) on the current device; all of the
+ * stage's device work runs on it. v starts at 0, so both predicted slots start
+ * equal to W0 (Eq. 4 with v = 0). Device dims that the kernels need to be
+ * multiples of 8 (bf16 channel/feature counts) are checked here (EINVAL).
+ * Synchronises the stream before returning. */
+int spectrain_stage_create(const spectrain_stage_desc* desc, const float* W0_host, size_t n_params,
+                           void* hip_stream, spectrain_stage_t* out);
+
+/* Number of parameters of the stage (the length of the flat arrays). */
+int spectrain_stage_num_params(spectrain_stage_t st, size_t* n);
+
+/* Eq. 4 for one slot: What_slot = W - s * eta * v, rounded to the compute
+ * dtype. slot 0 feeds the next forward, slot 1 the next backward. EINVAL for
+ * s < 0 or a bad slot. */
+int spectrain_stage_predict(spectrain_stage_t st, int32_t s, int32_t slot);
+
+/* Forward pass of mini-batch mb_id against slot 0. x_dev: input activations.
+ * y_dev: output activations (HEAD_NONE; NULL with a CE head). labels_dev and
+ * loss_dev (one float32, the mean CE) are used with a CE head only. The stage
+ * keeps references to x_dev and y_dev until the matching backward returns:
+ * the caller must keep them alive and unmodified until then. ESTATE when
+ * N - k mini-batches are already in flight or mb_id is already in flight. */
+int spectrain_stage_forward(spectrain_stage_t st, int64_t mb_id, const void* x_dev, void* y_dev,
+                            const int32_t* labels_dev, float* loss_dev);
+
+/* Backward pass of mini-batch mb_id against slot 1 (dX) and the stashed
+ * activations (g). dy_dev: dL/dY (HEAD_NONE; ignored with a CE head).
+ * dx_dev: dL/dX output, or NULL to skip it (e.g. at k = 0). Overwrites g with
+ * this mini-batch's gradient and frees its stash slot. ESTATE when mb_id is
+ * not in flight or a previous gradient is still waiting for its update. */
+int spectrain_stage_backward(spectrain_stage_t st, int64_t mb_id, const void* dy_dev, void* dx_dev);
+
+/* One fused pass over the arenas: Eq. 1, W <- W - eta v, then Eq. 4 for both
+ * slots (slot 0 with s_next_fwd, slot 1 with s_next_bwd; a negative s leaves
+ * that slot unchanged). ESTATE unless a backward produced g since the last
+ * update. A non-finite W or v element raises a flag that makes the next call
+ * on the stage return ENONFINITE. */
+int spectrain_stage_update(spectrain_stage_t st, int32_t s_next_fwd, int32_t s_next_bwd);
+
+/* Copy W and v (float32, parameter order) to host buffers of n_params values.
+ * Either pointer may be NULL. Synchronises the stream. */
+int spectrain_stage_get_state(spectrain_stage_t st, float* W_host, float* v_host);
+
+/* Replace W and v (host float32, parameter order; v may be NULL for zero) and
+ * re-predict both slots with s = 0. ESTATE while any mini-batch is in flight.
+ * Synchronises the stream. */
+int spectrain_stage_set_state(spectrain_stage_t st, const float* W_host, const float* v_host);
+
+/* Copy a predicted slot (0 or 1), converted to float32, to the host.
+ * Synchronises the stream. */
+int spectrain_stage_get_predicted(spectrain_stage_t st, int32_t slot, float* What_host);
+
+/* Release every device buffer of the stage. Synchronises the stream.
+ * Passing NULL returns EINVAL. */
+int spectrain_stage_destroy(spectrain_stage_t st);
+
+/* Message of the last failed call on this host thread ("" if none). */
+const char* spectrain_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECTRAIN_H */

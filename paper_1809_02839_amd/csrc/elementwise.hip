@@ -1,0 +1,418 @@
+// Memory-bound kernels of the stage step: ReLU-gradient masks, deterministic
+// column sums (bias and layer-norm gradients), softmax cross-entropy,
+// layer norm, attention softmax forward/backward and the LSTM cell.
+// Every reduction runs in a fixed order, so results are bitwise reproducible.
+#include "kernels.hpp"
+
+namespace spx {
+namespace {
+
+constexpr int NT = 256;
+
+int blocks_for(long n, int per_thread) {
+  long b = (n + static_cast<long>(NT) * per_thread - 1) / (static_cast<long>(NT) * per_thread);
+  if (b < 1) b = 1;
+  if (b > 65535L * 4) b = 65535L * 4;
+  return static_cast<int>(b);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Block-wide reductions in a fixed order (256 threads = 4 waves).
+__device__ float block_sum(float v, float* sh) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  return (sh[0] + sh[1]) + (sh[2] + sh[3]);
+}
+__device__ float block_max(float v, float* sh) {
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(sh[0], sh[1]), fmaxf(sh[2], sh[3]));
+}
+
+// ---------------------------------------------------------------- masks ----
+__global__ void mask_bf16_kernel(const bf16_t* src, const bf16_t* mask, bf16_t* dst, long n) {
+  for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n; i += static_cast<long>(gridDim.x) * NT)
+    dst[i] = bf16_to_f32(mask[i]) > 0.0f ? src[i] : static_cast<bf16_t>(0);
+}
+__global__ void mask_f32_kernel(const float* src, const float* mask, float* dst, long n) {
+  for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n; i += static_cast<long>(gridDim.x) * NT)
+    dst[i] = mask[i] > 0.0f ? src[i] : 0.0f;
+}
+
+// --------------------------------------------------------- column sums ----
+// Pass 1: block (cb, rb) sums rows [rb*RCH, (rb+1)*RCH) of 64 columns.
+constexpr int RCH = 256;
+template <typename T>
+__global__ void colsum_partial_kernel(const T* X, long rows, int cols, long ld, float* partial) {
+  __shared__ float sh[4][64];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int col = blockIdx.x * 64 + tx;
+  const long r0 = static_cast<long>(blockIdx.y) * RCH;
+  float s = 0.0f;
+  if (col < cols) {
+    for (long r = r0 + ty; r < r0 + RCH && r < rows; r += 4) {
+      if constexpr (sizeof(T) == 2) s += bf16_to_f32(X[r * ld + col]);
+      else s += X[r * ld + col];
+    }
+  }
+  sh[ty][tx] = s;
+  __syncthreads();
+  if (ty == 0 && col < cols) partial[static_cast<long>(blockIdx.y) * cols + col] = (sh[0][tx] + sh[1][tx]) + (sh[2][tx] + sh[3][tx]);
+}
+__global__ void colsum_final_kernel(const float* partial, int nchunks, int cols, float* out, int accumulate) {
+  const int col = blockIdx.x * NT + threadIdx.x;
+  if (col >= cols) return;
+  float s = 0.0f;
+  for (int c = 0; c < nchunks; ++c) s += partial[static_cast<long>(c) * cols + col];
+  out[col] = accumulate ? out[col] + s : s;
+}
+
+// ---------------------------------------------------- cross-entropy ----
+template <int DT>
+__global__ __launch_bounds__(NT) void softmax_ce_kernel(const float* logits, const int32_t* labels, int R, int C,
+                                                        void* dlogits, float* row_loss) {
+  __shared__ float sh[4];
+  const int r = blockIdx.x;
+  const float* z = logits + static_cast<long>(r) * C;
+  float m = -INFINITY;
+  for (int c = threadIdx.x; c < C; c += NT) m = fmaxf(m, z[c]);
+  m = block_max(m, sh);
+  float s = 0.0f;
+  for (int c = threadIdx.x; c < C; c += NT) s += expf(z[c] - m);
+  s = block_sum(s, sh);
+  // a label outside [0, C) yields a NaN loss for its row and no target term
+  const int lab = labels[r];
+  const bool lab_ok = lab >= 0 && lab < C;
+  if (threadIdx.x == 0) row_loss[r] = lab_ok ? (m + logf(s)) - z[lab] : NAN;
+  const float inv_s = 1.0f / s, inv_r = 1.0f / static_cast<float>(R);
+  for (int c = threadIdx.x; c < C; c += NT) {
+    float p = expf(z[c] - m) * inv_s;
+    float d = ((c == lab) ? p - 1.0f : p) * inv_r;
+    if (DT == 1) static_cast<bf16_t*>(dlogits)[static_cast<long>(r) * C + c] = f32_to_bf16(d);
+    else static_cast<float*>(dlogits)[static_cast<long>(r) * C + c] = d;
+  }
+}
+__global__ __launch_bounds__(NT) void mean_kernel(const float* x, int n, float* out) {
+  __shared__ float sh[4];
+  float s = 0.0f;
+  for (int i = threadIdx.x; i < n; i += NT) s += x[i];
+  s = block_sum(s, sh);
+  if (threadIdx.x == 0) out[0] = s / static_cast<float>(n);
+}
+
+// ---------------------------------------------------------- layer norm ----
+// One wave per row; D is a multiple of 64 up to 64 * 32.
+constexpr int LN_MAXV = 32;
+__global__ __launch_bounds__(NT) void layernorm_fwd_kernel(const bf16_t* r, const bf16_t* gamma, const bf16_t* beta,
+                                                           int R, int D, float eps, bf16_t* y, float* mean,
+                                                           float* rstd) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= R) return;
+  const bf16_t* x = r + static_cast<long>(row) * D;
+  const int per = D / 64;
+  float v[LN_MAXV];
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < LN_MAXV; ++j)
+    if (j < per) {
+      v[j] = bf16_to_f32(x[j * 64 + lane]);
+      s += v[j];
+    }
+  const float mu = wave_sum(s) / static_cast<float>(D);
+  float q = 0.0f;
+#pragma unroll
+  for (int j = 0; j < LN_MAXV; ++j)
+    if (j < per) {
+      const float d = v[j] - mu;
+      q += d * d;
+    }
+  const float rs = rsqrtf(wave_sum(q) / static_cast<float>(D) + eps);
+#pragma unroll
+  for (int j = 0; j < LN_MAXV; ++j)
+    if (j < per) {
+      const int c = j * 64 + lane;
+      y[static_cast<long>(row) * D + c] = f32_to_bf16(bf16_to_f32(gamma[c]) * ((v[j] - mu) * rs) + bf16_to_f32(beta[c]));
+    }
+  if (lane == 0) {
+    mean[row] = mu;
+    rstd[row] = rs;
+  }
+}
+
+// Rows per block in the backward; partial dgamma/dbeta per block.
+constexpr int LNB_ROWS = 32;
+__global__ __launch_bounds__(NT) void layernorm_bwd_kernel(const bf16_t* dy, const bf16_t* r, const float* mean,
+                                                           const float* rstd, const bf16_t* gamma, int R, int D,
+                                                           bf16_t* dr, float* part_g, float* part_b) {
+  __shared__ float shg[4][64 * 8];
+  __shared__ float shb[4][64 * 8];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int per = D / 64;
+  float pg[LN_MAXV], pb[LN_MAXV];
+#pragma unroll
+  for (int j = 0; j < LN_MAXV; ++j) pg[j] = pb[j] = 0.0f;
+  for (int rr = w; rr < LNB_ROWS; rr += 4) {
+    const int row = blockIdx.x * LNB_ROWS + rr;
+    if (row >= R) break;
+    const long base = static_cast<long>(row) * D;
+    const float mu = mean[row], rs = rstd[row];
+    float xh[LN_MAXV], g[LN_MAXV];
+    float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+    for (int j = 0; j < LN_MAXV; ++j)
+      if (j < per) {
+        const int c = j * 64 + lane;
+        const float d = bf16_to_f32(dy[base + c]);
+        xh[j] = (bf16_to_f32(r[base + c]) - mu) * rs;
+        g[j] = d * bf16_to_f32(gamma[c]);
+        s1 += g[j];
+        s2 += g[j] * xh[j];
+        pg[j] += d * xh[j];
+        pb[j] += d;
+      }
+    const float m1 = wave_sum(s1) / static_cast<float>(D), m2 = wave_sum(s2) / static_cast<float>(D);
+#pragma unroll
+    for (int j = 0; j < LN_MAXV; ++j)
+      if (j < per) dr[base + j * 64 + lane] = f32_to_bf16(rs * (g[j] - m1 - xh[j] * m2));
+  }
+  // combine the four waves in a fixed order, 8 column groups of 64 at a time
+#pragma unroll
+  for (int j0 = 0; j0 < LN_MAXV; j0 += 8) {
+    if (j0 >= per) break;  // uniform across the block
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (j0 + j < per) {
+        shg[w][j * 64 + lane] = pg[j0 + j];
+        shb[w][j * 64 + lane] = pb[j0 + j];
+      }
+    __syncthreads();
+    for (int i = threadIdx.x; i < 8 * 64; i += NT) {
+      const int c = j0 * 64 + i;
+      if (c < D) {
+        part_g[static_cast<long>(blockIdx.x) * D + c] = (shg[0][i] + shg[1][i]) + (shg[2][i] + shg[3][i]);
+        part_b[static_cast<long>(blockIdx.x) * D + c] = (shb[0][i] + shb[1][i]) + (shb[2][i] + shb[3][i]);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------ softmax (rows) ----
+__global__ __launch_bounds__(NT) void softmax_rows_kernel(const float* S, int R, int C, float* P, bf16_t* Pb) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= R) return;
+  const float* s = S + static_cast<long>(row) * C;
+  float m = -INFINITY;
+  for (int c = lane; c < C; c += 64) m = fmaxf(m, s[c]);
+  m = wave_max(m);
+  float sum = 0.0f;
+  for (int c = lane; c < C; c += 64) sum += expf(s[c] - m);
+  sum = wave_sum(sum);
+  const float inv = 1.0f / sum;
+  for (int c = lane; c < C; c += 64) {
+    const float p = expf(s[c] - m) * inv;
+    P[static_cast<long>(row) * C + c] = p;
+    Pb[static_cast<long>(row) * C + c] = f32_to_bf16(p);
+  }
+}
+
+__global__ __launch_bounds__(NT) void softmax_bwd_kernel(const float* P, const float* dP, int R, int C, bf16_t* dS) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= R) return;
+  const long base = static_cast<long>(row) * C;
+  float dot = 0.0f;
+  for (int c = lane; c < C; c += 64) dot += P[base + c] * dP[base + c];
+  dot = wave_sum(dot);
+  for (int c = lane; c < C; c += 64) dS[base + c] = f32_to_bf16(P[base + c] * (dP[base + c] - dot));
+}
+
+// ------------------------------------------------------------ LSTM cell ----
+__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + expf(-x)); }
+
+__global__ void lstm_cell_fwd_kernel(const float* z, const float* c_prev, int B, int H, float* gates, float* c,
+                                     bf16_t* h) {
+  const long n = static_cast<long>(B) * H;
+  for (long t = static_cast<long>(blockIdx.x) * NT + threadIdx.x; t < n; t += static_cast<long>(gridDim.x) * NT) {
+    const int b = static_cast<int>(t / H), j = static_cast<int>(t - static_cast<long>(b) * H);
+    const long zb = static_cast<long>(b) * 4 * H;
+    const float i = sigm(z[zb + j]);
+    const float f = sigm(z[zb + H + j]);
+    const float g = tanhf(z[zb + 2 * H + j]);
+    const float o = sigm(z[zb + 3 * H + j]);
+    const float cp = c_prev ? c_prev[t] : 0.0f;
+    const float cn = fmaf(f, cp, i * g);
+    gates[zb + j] = i;
+    gates[zb + H + j] = f;
+    gates[zb + 2 * H + j] = g;
+    gates[zb + 3 * H + j] = o;
+    c[t] = cn;
+    h[t] = f32_to_bf16(o * tanhf(cn));
+  }
+}
+
+__global__ void lstm_cell_bwd_kernel(const bf16_t* dh_out, const float* dh_rec, const float* gates, const float* c,
+                                     const float* c_prev, int B, int H, float* dc, bf16_t* dz) {
+  const long n = static_cast<long>(B) * H;
+  for (long t = static_cast<long>(blockIdx.x) * NT + threadIdx.x; t < n; t += static_cast<long>(gridDim.x) * NT) {
+    const int b = static_cast<int>(t / H), j = static_cast<int>(t - static_cast<long>(b) * H);
+    const long zb = static_cast<long>(b) * 4 * H;
+    const float i = gates[zb + j], f = gates[zb + H + j], g = gates[zb + 2 * H + j], o = gates[zb + 3 * H + j];
+    const float dh = bf16_to_f32(dh_out[t]) + (dh_rec ? dh_rec[t] : 0.0f);
+    const float tc = tanhf(c[t]);
+    const float d_o = dh * tc;
+    const float dct = dc[t] + dh * o * (1.0f - tc * tc);
+    const float di = dct * g, dg = dct * i, df = dct * (c_prev ? c_prev[t] : 0.0f);
+    dc[t] = dct * f;
+    dz[zb + j] = f32_to_bf16(di * i * (1.0f - i));
+    dz[zb + H + j] = f32_to_bf16(df * f * (1.0f - f));
+    dz[zb + 2 * H + j] = f32_to_bf16(dg * (1.0f - g * g));
+    dz[zb + 3 * H + j] = f32_to_bf16(d_o * o * (1.0f - o));
+  }
+}
+
+// ---------------------------------------------------------------- misc ----
+__global__ void add_bf16_kernel(const bf16_t* a, const bf16_t* b, bf16_t* out, long n) {
+  for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n; i += static_cast<long>(gridDim.x) * NT)
+    out[i] = f32_to_bf16(bf16_to_f32(a[i]) + bf16_to_f32(b[i]));
+}
+__global__ void cast_f2b_kernel(const float* x, bf16_t* y, long n) {
+  for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n; i += static_cast<long>(gridDim.x) * NT)
+    y[i] = f32_to_bf16(x[i]);
+}
+__global__ void cast_b2f_kernel(const bf16_t* x, float* y, long n) {
+  for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n; i += static_cast<long>(gridDim.x) * NT)
+    y[i] = bf16_to_f32(x[i]);
+}
+__global__ void fill_kernel(float* x, float v, long n) {
+  for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n; i += static_cast<long>(gridDim.x) * NT)
+    x[i] = v;
+}
+
+}  // namespace
+
+hipError_t mask_relu_grad(const void* src, const void* mask, void* dst, long n, int dtype, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (dtype == 1)
+    hipLaunchKernelGGL(mask_bf16_kernel, dim3(blocks_for(n, 4)), dim3(NT), 0, s, static_cast<const bf16_t*>(src),
+                       static_cast<const bf16_t*>(mask), static_cast<bf16_t*>(dst), n);
+  else
+    hipLaunchKernelGGL(mask_f32_kernel, dim3(blocks_for(n, 4)), dim3(NT), 0, s, static_cast<const float*>(src),
+                       static_cast<const float*>(mask), static_cast<float*>(dst), n);
+  return hipGetLastError();
+}
+
+hipError_t column_sum(const void* X, int dtype, long rows, int cols, long ld, float* out, int accumulate,
+                      float* partial_ws, hipStream_t s) {
+  if (cols <= 0) return hipSuccess;
+  const int nchunks = rows > 0 ? static_cast<int>((rows + RCH - 1) / RCH) : 0;
+  if (nchunks > 0) {
+    dim3 grid((cols + 63) / 64, nchunks);
+    if (dtype == 1)
+      hipLaunchKernelGGL(colsum_partial_kernel<bf16_t>, grid, dim3(NT), 0, s, static_cast<const bf16_t*>(X), rows,
+                         cols, ld, partial_ws);
+    else
+      hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(NT), 0, s, static_cast<const float*>(X), rows,
+                         cols, ld, partial_ws);
+  }
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + NT - 1) / NT), dim3(NT), 0, s, partial_ws, nchunks, cols, out,
+                     accumulate);
+  return hipGetLastError();
+}
+
+hipError_t softmax_ce(const float* logits, const int32_t* labels, int R, int C, void* dlogits, int dtype, float* loss,
+                      float* row_loss_ws, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (dtype == 1)
+    hipLaunchKernelGGL(softmax_ce_kernel<1>, dim3(R), dim3(NT), 0, s, logits, labels, R, C, dlogits, row_loss_ws);
+  else
+    hipLaunchKernelGGL(softmax_ce_kernel<0>, dim3(R), dim3(NT), 0, s, logits, labels, R, C, dlogits, row_loss_ws);
+  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(NT), 0, s, row_loss_ws, R, loss);
+  return hipGetLastError();
+}
+
+hipError_t layernorm_fwd(const bf16_t* r, const bf16_t* gamma, const bf16_t* beta, int R, int D, float eps, bf16_t* y,
+                         float* mean, float* rstd, hipStream_t s) {
+  if (D % 64 || D > 64 * LN_MAXV) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(layernorm_fwd_kernel, dim3((R + 3) / 4), dim3(NT), 0, s, r, gamma, beta, R, D, eps, y, mean,
+                     rstd);
+  return hipGetLastError();
+}
+
+hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd, const bf16_t* gamma,
+                         int R, int D, bf16_t* dr, float* dgamma, float* dbeta, float* partial_ws, hipStream_t s) {
+  if (D % 64 || D > 64 * LN_MAXV) return hipErrorInvalidValue;
+  const int nb = (R + LNB_ROWS - 1) / LNB_ROWS;
+  float* pg = partial_ws;
+  float* pb = partial_ws + static_cast<long>(nb) * D;
+  hipLaunchKernelGGL(layernorm_bwd_kernel, dim3(nb), dim3(NT), 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + NT - 1) / NT), dim3(NT), 0, s, pg, nb, D, dgamma, 0);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + NT - 1) / NT), dim3(NT), 0, s, pb, nb, D, dbeta, 0);
+  return hipGetLastError();
+}
+
+hipError_t softmax_rows(const float* S, int R, int C, float* P, bf16_t* Pb, hipStream_t s) {
+  hipLaunchKernelGGL(softmax_rows_kernel, dim3((R + 3) / 4), dim3(NT), 0, s, S, R, C, P, Pb);
+  return hipGetLastError();
+}
+
+hipError_t softmax_bwd(const float* P, const float* dP, int R, int C, bf16_t* dS, hipStream_t s) {
+  hipLaunchKernelGGL(softmax_bwd_kernel, dim3((R + 3) / 4), dim3(NT), 0, s, P, dP, R, C, dS);
+  return hipGetLastError();
+}
+
+hipError_t lstm_cell_fwd(const float* z, const float* c_prev, int B, int H, float* gates, float* c, bf16_t* h,
+                         hipStream_t s) {
+  const long n = static_cast<long>(B) * H;
+  hipLaunchKernelGGL(lstm_cell_fwd_kernel, dim3(blocks_for(n, 1)), dim3(NT), 0, s, z, c_prev, B, H, gates, c, h);
+  return hipGetLastError();
+}
+
+hipError_t lstm_cell_bwd(const bf16_t* dh_out, const float* dh_rec, const float* gates, const float* c,
+                         const float* c_prev, int B, int H, float* dc, bf16_t* dz, hipStream_t s) {
+  const long n = static_cast<long>(B) * H;
+  hipLaunchKernelGGL(lstm_cell_bwd_kernel, dim3(blocks_for(n, 1)), dim3(NT), 0, s, dh_out, dh_rec, gates, c, c_prev,
+                     B, H, dc, dz);
+  return hipGetLastError();
+}
+
+hipError_t add_bf16(const bf16_t* a, const bf16_t* b, bf16_t* out, long n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(add_bf16_kernel, dim3(blocks_for(n, 4)), dim3(NT), 0, s, a, b, out, n);
+  return hipGetLastError();
+}
+hipError_t cast_f32_to_bf16(const float* x, bf16_t* y, long n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(cast_f2b_kernel, dim3(blocks_for(n, 4)), dim3(NT), 0, s, x, y, n);
+  return hipGetLastError();
+}
+hipError_t cast_bf16_to_f32(const bf16_t* x, float* y, long n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(cast_b2f_kernel, dim3(blocks_for(n, 4)), dim3(NT), 0, s, x, y, n);
+  return hipGetLastError();
+}
+hipError_t fill_f32(float* x, float v, long n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_kernel, dim3(blocks_for(n, 4)), dim3(NT), 0, s, x, v, n);
+  return hipGetLastError();
+}
+
+}  // namespace spx

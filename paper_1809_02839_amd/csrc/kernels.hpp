@@ -1,0 +1,110 @@
+// Kernel launchers of the SpecTrain stage library. Every launcher enqueues
+// on the given stream and returns hipSuccess or the launch error.
+#pragma once
+
+#include "common.hpp"
+
+namespace spx {
+
+// ---------------------------------------------------------------- GEMM ----
+// C[m, n] = sum_k A(m, k) * B(n, k), float32 accumulation, M x N x K, with an
+// optional batch over blockIdx.z. Operands are described by an access mode:
+//   K-modes deliver 8 consecutive k of one row (16-byte loads),
+//   R-modes deliver 8 consecutive rows of one k (16-byte loads, transposed on
+//   the way into LDS).
+enum OperandMode : int {
+  OP_K_PLAIN = 0,      // X[r * ld + k]
+  OP_K_CONV_FWD = 1,   // im2col of an NHWC map: k = tap * C + c, source pixel p + (kh-1, kw-1)
+  OP_K_CONV_DGRAD = 2, // im2col for the data gradient: k = tap * C + c, source pixel p - (kh-1, kw-1)
+  OP_R_PLAIN = 3,      // X[k * ld + r]
+  OP_R_CONV_WGRAD = 4, // rows r = tap * C + c, k = pixel: X[pixel + (kh-1, kw-1)][c]
+  OP_R_FILTER_T = 5,   // filter [C2][3][3][C] read as rows r = c, k = tap * C2 + c2
+};
+
+struct ConvGeom {
+  int B = 0, H = 0, W = 0;
+  int C = 0;    // channels of the gathered tensor (for FILTER_T: C_in, the row count)
+  int C2 = 0;   // FILTER_T only: C_out
+};
+
+struct Operand {
+  const void* ptr = nullptr;   // bf16 (or float32 for the float32 GEMM)
+  long ld = 0;
+  long bs1 = 0, bs2 = 0;       // batch strides (elements) for z / zdiv and z % zdiv
+  int mode = OP_K_PLAIN;
+  ConvGeom g;
+};
+
+struct Epilogue {
+  float* out_f32 = nullptr;        // value stored (or added, if accumulate) as float32
+  bf16_t* out_bf16 = nullptr;      // value rounded to bf16 and stored
+  long ldc = 0;
+  long bs1 = 0, bs2 = 0;           // batch strides of every [M, N] tensor below
+  const float* bias = nullptr;     // [N], added
+  const bf16_t* bias_bf16 = nullptr;  // [N], added (bf16 GEMM only)
+  const float* res_f32 = nullptr;  // [M, N] with ldc, added
+  const bf16_t* res_bf16 = nullptr;// [M, N] with ldc, added
+  const void* mask = nullptr;      // [M, N] with ldc: value zeroed where mask <= 0 (bf16 or f32 per GEMM dtype)
+  float alpha = 1.0f;              // scales the accumulator before everything else
+  int relu = 0;
+  int accumulate = 0;              // out_f32 += value
+};
+
+struct GemmDesc {
+  int M = 0, N = 0, K = 0;
+  int batch = 1, zdiv = 1;
+  Operand A, B;
+  Epilogue epi;
+};
+
+hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s);
+hipError_t gemm_f32(const GemmDesc& d, hipStream_t s);
+
+// ------------------------------------------------------- update/predict ----
+// Fused Eq. 1 + momentum update + Eq. 4 for two slots over n float32 values.
+// what_dtype: 0 float32, 1 bf16. s < 0 skips a slot. flag is set to 1 when a
+// non-finite W or v is produced.
+hipError_t fused_update(float* W, float* v, const float* g, void* what_f, void* what_b, int what_dtype,
+                        long n, float lr, float gamma, int s_f, int s_b, int* flag, hipStream_t s);
+hipError_t predict_slot(const float* W, const float* v, void* what, int what_dtype, long n, float lr, int s_pred,
+                        hipStream_t s);
+
+// ------------------------------------------------------------ elementwise ----
+// dst[i] = src[i] * (mask[i] > 0), bf16 (dtype 1) or float32 (dtype 0).
+hipError_t mask_relu_grad(const void* src, const void* mask, void* dst, long n, int dtype, hipStream_t s);
+// out[c] (=|+=) sum over rows r of X[r * ld + c], X bf16 or float32; deterministic.
+hipError_t column_sum(const void* X, int dtype, long rows, int cols, long ld, float* out, int accumulate,
+                      float* partial_ws, hipStream_t s);
+// Mean softmax cross-entropy over rows of float32 logits [R, C]; writes the
+// mean loss to loss (one float) and dlogits = (softmax - onehot) / R in dtype.
+hipError_t softmax_ce(const float* logits, const int32_t* labels, int R, int C, void* dlogits, int dtype,
+                      float* loss, float* row_loss_ws, hipStream_t s);
+// Layer norm over rows of bf16 r [R, D]: y = bf16(gamma * xhat + beta) with
+// bf16 gamma/beta; stats mean and rstd (float32) are written per row.
+hipError_t layernorm_fwd(const bf16_t* r, const bf16_t* gamma, const bf16_t* beta, int R, int D, float eps,
+                         bf16_t* y, float* mean, float* rstd, hipStream_t s);
+// Layer-norm backward for bf16 dy: dr = bf16(...); dgamma/dbeta (float32,
+// overwritten) reduced over rows deterministically.
+hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd,
+                         const bf16_t* gamma, int R, int D, bf16_t* dr, float* dgamma, float* dbeta,
+                         float* partial_ws, hipStream_t s);
+// Row softmax of float32 scores [R, C] -> P float32 and bf16(P).
+hipError_t softmax_rows(const float* S, int R, int C, float* P, bf16_t* Pb, hipStream_t s);
+// Softmax backward: dS = bf16(P * (dP - sum_j P dP)) per row.
+hipError_t softmax_bwd(const float* P, const float* dP, int R, int C, bf16_t* dS, hipStream_t s);
+// LSTM cell for one time step: z [B, 4H] float32 pre-activations (i, f, g, o)
+// -> gates (activated, float32), c_t, h_t = bf16(o * tanh(c_t)).
+hipError_t lstm_cell_fwd(const float* z, const float* c_prev, int B, int H, float* gates, float* c,
+                         bf16_t* h, hipStream_t s);
+// LSTM cell backward for one step: dh = dh_out + dh_rec; writes dz (bf16) and
+// carries dc (in/out, float32).
+hipError_t lstm_cell_bwd(const bf16_t* dh_out, const float* dh_rec, const float* gates, const float* c,
+                         const float* c_prev, int B, int H, float* dc, bf16_t* dz, hipStream_t s);
+// out = bf16(a + b) elementwise (bf16 inputs).
+hipError_t add_bf16(const bf16_t* a, const bf16_t* b, bf16_t* out, long n, hipStream_t s);
+// float32 <-> bf16 conversions.
+hipError_t cast_f32_to_bf16(const float* x, bf16_t* y, long n, hipStream_t s);
+hipError_t cast_bf16_to_f32(const bf16_t* x, float* y, long n, hipStream_t s);
+hipError_t fill_f32(float* x, float v, long n, hipStream_t s);
+
+}  // namespace spx

@@ -1,0 +1,940 @@
+// Stage engine: owns the float32 W / v / g arenas, the two predicted-weight
+// slots, the activation stash ring (one slot per mini-batch in flight) and a
+// workspace, and turns forward / backward / update calls into kernel launches
+// on the stage's stream. The per-kind sequences follow the layer definitions
+// of the five workload kinds (Section 4.1 of the paper: VGG-style 3x3
+// convolutions, ResNet bottlenecks, a post-LN Transformer encoder, a residual
+// LSTM, and fully-connected layers), with the forward pass reading predicted
+// slot 0 and the backward pass reading slot 1 (Section 3.2, Eq. 5 and Eq. 6).
+#include "stage.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+
+namespace spx {
+
+void hip_check(hipError_t e, const char* what) {
+  if (e != hipSuccess) throw StageError(SPECTRAIN_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// ------------------------------------------------------------ DeviceBlock ----
+size_t DeviceBlock::add(size_t bytes) {
+  size_t off = total_;
+  total_ += (bytes + 255) & ~static_cast<size_t>(255);
+  return off;
+}
+void DeviceBlock::allocate() {
+  if (total_ == 0) return;
+  void* p = nullptr;
+  hipError_t e = hipMalloc(&p, total_);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    throw StageError(SPECTRAIN_ENOMEM, "hipMalloc of " + std::to_string(total_) + " bytes failed: " +
+                                           hipGetErrorString(e));
+  }
+  base_ = static_cast<char*>(p);
+}
+void DeviceBlock::release() {
+  if (base_) (void)hipFree(base_);
+  base_ = nullptr;
+}
+
+namespace {
+
+constexpr long TENSOR_ALIGN = 64;   // elements: 256 B of float32, 128 B of bf16
+constexpr float LN_EPS = 1e-5f;
+
+Operand opK(const void* p, long ld) {
+  Operand o;
+  o.ptr = p;
+  o.ld = ld;
+  o.mode = OP_K_PLAIN;
+  return o;
+}
+Operand opR(const void* p, long ld) {
+  Operand o;
+  o.ptr = p;
+  o.ld = ld;
+  o.mode = OP_R_PLAIN;
+  return o;
+}
+Operand opConv(int mode, const void* p, int B, int H, int W, int C, int C2 = 0) {
+  Operand o;
+  o.ptr = p;
+  o.mode = mode;
+  o.g.B = B;
+  o.g.H = H;
+  o.g.W = W;
+  o.g.C = C;
+  o.g.C2 = C2;
+  return o;
+}
+GemmDesc gd(int M, int N, int K, const Operand& A, const Operand& B, long ldc) {
+  GemmDesc d;
+  d.M = M;
+  d.N = N;
+  d.K = K;
+  d.A = A;
+  d.B = B;
+  d.epi.ldc = ldc;
+  return d;
+}
+
+void fail(const std::string& m) { throw StageError(SPECTRAIN_EINVAL, m); }
+
+}  // namespace
+
+// ----------------------------------------------------------------- layout ----
+void Stage::build_layout() {
+  const int* dm = d_.dims;
+  const int L = d_.num_layers;
+  std::vector<long> sizes;
+  switch (d_.kind) {
+    case SPECTRAIN_KIND_FC: {
+      for (int l = 0; l < L; ++l) {
+        long fin = l == 0 ? dm[0] : dm[2];
+        long fout = l == L - 1 ? dm[1] : dm[2];
+        sizes.push_back(fout * fin);
+        sizes.push_back(fout);
+      }
+      break;
+    }
+    case SPECTRAIN_KIND_CONV3X3:
+      for (int l = 0; l < L; ++l) sizes.push_back(static_cast<long>(dm[1]) * 9 * (l == 0 ? dm[0] : dm[1]));
+      break;
+    case SPECTRAIN_KIND_BOTTLENECK:
+      for (int l = 0; l < L; ++l) {
+        sizes.push_back(static_cast<long>(dm[1]) * dm[0]);
+        sizes.push_back(static_cast<long>(dm[1]) * 9 * dm[1]);
+        sizes.push_back(static_cast<long>(dm[0]) * dm[1]);
+      }
+      break;
+    case SPECTRAIN_KIND_TRANSFORMER: {
+      const long d = dm[0], F = dm[2];
+      for (int l = 0; l < L; ++l) {
+        long s[12] = {3 * d * d, 3 * d, d * d, d, d, d, F * d, F, d * F, d, d, d};
+        sizes.insert(sizes.end(), s, s + 12);
+      }
+      break;
+    }
+    case SPECTRAIN_KIND_RESLSTM: {
+      const long I = dm[0], H = dm[1], V = dm[3];
+      for (int l = 0; l < L; ++l) {
+        sizes.push_back(4 * H * (l == 0 ? I : H));
+        sizes.push_back(4 * H * H);
+        sizes.push_back(4 * H);
+      }
+      if (d_.head == SPECTRAIN_HEAD_CE) {
+        sizes.push_back(V * H);
+        sizes.push_back(V);
+      }
+      break;
+    }
+    default:
+      fail("unknown stage kind");
+  }
+  long off = 0;
+  n_params_ = 0;
+  for (long n : sizes) {
+    tensors_.push_back({off, n});
+    off += (n + TENSOR_ALIGN - 1) / TENSOR_ALIGN * TENSOR_ALIGN;
+    n_params_ += n;
+  }
+  n_arena_ = off;
+}
+
+const void* Stage::wf(int i) const { return static_cast<const char*>(what_[0]) + tensors_[i].off * esz_; }
+const void* Stage::wb(int i) const { return static_cast<const char*>(what_[1]) + tensors_[i].off * esz_; }
+
+void Stage::gemm(const GemmDesc& d) {
+  hip_check(dt_ ? gemm_bf16(d, s_) : gemm_f32(d, s_), "gemm launch");
+}
+
+// Sizes of the stash slot buffers and workspace buffers of each kind.
+void Stage::plan_buffers() {
+  const int* dm = d_.dims;
+  const int L = d_.num_layers;
+  const long B = d_.batch;
+  std::vector<size_t> st, ws;   // byte sizes, indexed by buffer id
+  auto partial_floats = [](long rows, long cols) { return ((rows + 255) / 256) * cols; };
+  long partial = 0;
+  switch (d_.kind) {
+    case SPECTRAIN_KIND_FC: {
+      const long C = dm[1], hid = dm[2], maxw = std::max<long>(std::max<long>(dm[0], dm[1]), dm[2]);
+      for (int l = 1; l < L; ++l) st.push_back(B * hid * esz_);         // act l at id l-1
+      st.push_back(d_.head == SPECTRAIN_HEAD_CE ? B * C * esz_ : 0);     // dlogits at id L-1
+      ws = {static_cast<size_t>(B * C * 4), static_cast<size_t>(B * maxw * esz_),
+            static_cast<size_t>(B * maxw * esz_), static_cast<size_t>(B * 4)};
+      partial = partial_floats(B, maxw);
+      break;
+    }
+    case SPECTRAIN_KIND_CONV3X3: {
+      const long P = B * dm[2] * dm[3];
+      for (int l = 1; l < L; ++l) st.push_back(P * dm[1] * esz_);
+      const long cmax = std::max(dm[0], dm[1]);
+      ws = {static_cast<size_t>(P * cmax * esz_), static_cast<size_t>(P * cmax * esz_)};
+      break;
+    }
+    case SPECTRAIN_KIND_BOTTLENECK: {
+      const long P = B * dm[2] * dm[3], C = dm[0], Cm = dm[1];
+      for (int l = 0; l < L; ++l) {
+        st.push_back(P * Cm * esz_);
+        st.push_back(P * Cm * esz_);
+        st.push_back(l < L - 1 ? P * C * esz_ : 0);
+      }
+      ws = {static_cast<size_t>(P * C * esz_), static_cast<size_t>(P * C * esz_), static_cast<size_t>(P * Cm * esz_),
+            static_cast<size_t>(P * Cm * esz_)};
+      break;
+    }
+    case SPECTRAIN_KIND_TRANSFORMER: {
+      const long d = dm[0], H = dm[1], F = dm[2], S = dm[3], T = B * S, BHSS = B * H * S * S;
+      for (int l = 0; l < L; ++l) {
+        size_t s[13] = {static_cast<size_t>(T * 3 * d * 2), static_cast<size_t>(BHSS * 4),
+                        static_cast<size_t>(BHSS * 2),      static_cast<size_t>(T * d * 2),
+                        static_cast<size_t>(T * d * 2),     static_cast<size_t>(T * 4),
+                        static_cast<size_t>(T * 4),         static_cast<size_t>(T * d * 2),
+                        static_cast<size_t>(T * F * 2),     static_cast<size_t>(T * d * 2),
+                        static_cast<size_t>(T * 4),         static_cast<size_t>(T * 4),
+                        static_cast<size_t>(l < L - 1 ? T * d * 2 : 0)};
+        st.insert(st.end(), s, s + 13);
+      }
+      ws = {static_cast<size_t>(BHSS * 4), static_cast<size_t>(BHSS * 2), static_cast<size_t>(T * d * 2),
+            static_cast<size_t>(T * d * 2), static_cast<size_t>(T * d * 2), static_cast<size_t>(T * F * 2),
+            static_cast<size_t>(T * d * 2), static_cast<size_t>(T * d * 2), static_cast<size_t>(T * d * 2),
+            static_cast<size_t>(T * 3 * d * 2)};
+      partial = std::max(partial_floats(T, 3 * d), partial_floats(T, F));
+      partial = std::max(partial, 2 * ((T + 31) / 32) * d);
+      break;
+    }
+    case SPECTRAIN_KIND_RESLSTM: {
+      const long H = dm[1], T = dm[2], V = dm[3], TB = T * B;
+      const bool ce = d_.head == SPECTRAIN_HEAD_CE;
+      for (int l = 0; l < L; ++l) {
+        st.push_back(TB * 4 * H * 4);
+        st.push_back(TB * H * 4);
+        st.push_back(TB * H * 2);
+        st.push_back((l < L - 1 || ce) ? TB * H * 2 : 0);
+      }
+      st.push_back(ce ? TB * V * 2 : 0);
+      ws = {static_cast<size_t>(TB * 4 * H * 4), static_cast<size_t>(ce ? TB * V * 4 : 0),
+            static_cast<size_t>(TB * H * 2),     static_cast<size_t>(TB * H * 2),
+            static_cast<size_t>(TB * 4 * H * 2), static_cast<size_t>(B * H * 4),
+            static_cast<size_t>(B * H * 4),      static_cast<size_t>(TB * 4)};
+      partial = std::max(partial_floats(TB, 4 * H), ce ? partial_floats(TB, V) : 0);
+      break;
+    }
+  }
+  ws.push_back(static_cast<size_t>(std::max<long>(partial, 1) * 4));  // column-sum partials: last id
+  DeviceBlock probe;
+  for (size_t b : st) stash_off_.push_back(probe.add(std::max<size_t>(b, 1)));
+  for (size_t b : ws) ws_off_.push_back(ws_block_.add(std::max<size_t>(b, 1)));
+  const int nslots = d_.num_stages - d_.stage_index;
+  slots_.resize(nslots);
+  slot_blocks_.resize(nslots);
+  for (int i = 0; i < nslots; ++i) {
+    for (size_t b : st) slot_blocks_[i].add(std::max<size_t>(b, 1));
+    slot_blocks_[i].allocate();
+  }
+  ws_block_.allocate();
+}
+
+// ---------------------------------------------------------------- create ----
+Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hipStream_t s) : d_(d), s_(s) {
+  if (d.abi_version != SPECTRAIN_ABI_VERSION) fail("abi_version mismatch");
+  if (d.num_stages < 1 || d.stage_index < 0 || d.stage_index >= d.num_stages) fail("stage_index outside [0, N)");
+  if (d.batch < 1 || d.num_layers < 1) fail("batch and num_layers must be >= 1");
+  if (!(d.lr > 0.0f) || !std::isfinite(d.lr)) fail("lr must be a positive finite number");
+  if (!(d.momentum > 0.0f && d.momentum <= 1.0f)) fail("momentum must lie in (0, 1]");
+  if (d.dtype != SPECTRAIN_FP32 && d.dtype != SPECTRAIN_BF16) fail("unknown dtype");
+  if (d.head != SPECTRAIN_HEAD_NONE && d.head != SPECTRAIN_HEAD_CE) fail("unknown head");
+  if (d.head == SPECTRAIN_HEAD_CE && d.kind != SPECTRAIN_KIND_FC && d.kind != SPECTRAIN_KIND_RESLSTM)
+    fail("a CE head exists for FC and RESLSTM stages only");
+  dt_ = d.dtype == SPECTRAIN_BF16 ? 1 : 0;
+  esz_ = dt_ ? 2 : 4;
+  const int* dm = d.dims;
+  auto need = [&](int count) {
+    for (int i = 0; i < count; ++i)
+      if (dm[i] < 1) fail("dims[" + std::to_string(i) + "] must be >= 1");
+  };
+  auto mult8 = [&](long v, const char* what) {
+    if (v % 8) fail(std::string(what) + " must be a multiple of 8 for bf16 stages");
+  };
+  switch (d.kind) {
+    case SPECTRAIN_KIND_FC:
+      need(3);
+      if (dt_) {
+        mult8(dm[0], "in_features");
+        mult8(dm[1], "out_features");
+        mult8(dm[2], "hidden");
+      }
+      break;
+    case SPECTRAIN_KIND_CONV3X3:
+    case SPECTRAIN_KIND_BOTTLENECK:
+      need(4);
+      if (!dt_) fail("convolution stages run in bf16 only");
+      mult8(dm[0], "channels");
+      mult8(dm[1], "channels");
+      break;
+    case SPECTRAIN_KIND_TRANSFORMER:
+      need(4);
+      if (!dt_) fail("transformer stages run in bf16 only");
+      if (dm[0] % dm[1]) fail("d_model must be divisible by heads");
+      if (dm[0] % 64 || dm[0] > 2048) fail("d_model must be a multiple of 64 up to 2048");
+      mult8(dm[0] / dm[1], "head dimension");
+      mult8(dm[2], "ffn");
+      mult8(dm[3], "seq");
+      break;
+    case SPECTRAIN_KIND_RESLSTM:
+      need(3);
+      if (!dt_) fail("LSTM stages run in bf16 only");
+      if (dm[0] != dm[1]) fail("residual LSTM needs input == hidden");
+      mult8(dm[1], "hidden");
+      if (d.head == SPECTRAIN_HEAD_CE) {
+        need(4);
+        mult8(dm[3], "vocab");
+      }
+      break;
+    default:
+      fail("unknown stage kind");
+  }
+  build_layout();
+  if (n_params != n_params_) fail("n_params " + std::to_string(n_params) + " != " + std::to_string(n_params_));
+  if (!W0) fail("W0_host is NULL");
+
+  // arenas: W, v, g (float32), two predicted slots (operand dtype), all padded
+  size_t oW = arena_.add(n_arena_ * 4), ov = arena_.add(n_arena_ * 4), og = arena_.add(n_arena_ * 4);
+  size_t of = arena_.add(n_arena_ * esz_), ob = arena_.add(n_arena_ * esz_);
+  arena_.allocate();
+  W_ = arena_.at<float>(oW);
+  v_ = arena_.at<float>(ov);
+  g_ = arena_.at<float>(og);
+  what_[0] = arena_.at<void>(of);
+  what_[1] = arena_.at<void>(ob);
+  hip_check(hipHostMalloc(reinterpret_cast<void**>(&flag_host_), sizeof(int), hipHostMallocMapped), "hipHostMalloc");
+  *flag_host_ = 0;
+  hip_check(hipHostGetDevicePointer(reinterpret_cast<void**>(&flag_dev_), flag_host_, 0), "hipHostGetDevicePointer");
+  plan_buffers();
+
+  hip_check(fill_f32(v_, 0.0f, n_arena_, s_), "clear v");
+  hip_check(fill_f32(g_, 0.0f, n_arena_, s_), "clear g");
+  set_state(W0, nullptr);
+}
+
+Stage::~Stage() {
+  (void)hipStreamSynchronize(s_);
+  if (flag_host_) (void)hipHostFree(flag_host_);
+}
+
+void Stage::sync() { hip_check(hipStreamSynchronize(s_), "hipStreamSynchronize"); }
+
+// ------------------------------------------------------ state transfer ----
+void Stage::set_state(const float* W, const float* v) {
+  for (const Slot& sl : slots_)
+    if (sl.used) throw StageError(SPECTRAIN_ESTATE, "set_state with mini-batches in flight");
+  if (!W) fail("W_host is NULL");
+  std::vector<float> hw(n_arena_, 0.0f), hv(n_arena_, 0.0f);
+  long src = 0;
+  for (const TensorInfo& t : tensors_) {
+    std::memcpy(hw.data() + t.off, W + src, t.n * 4);
+    if (v) std::memcpy(hv.data() + t.off, v + src, t.n * 4);
+    src += t.n;
+  }
+  hip_check(hipMemcpyAsync(W_, hw.data(), n_arena_ * 4, hipMemcpyHostToDevice, s_), "copy W");
+  hip_check(hipMemcpyAsync(v_, hv.data(), n_arena_ * 4, hipMemcpyHostToDevice, s_), "copy v");
+  sync();
+  predict(0, 0);
+  predict(0, 1);
+  sync();
+  *flag_host_ = 0;
+  g_pending_ = false;
+}
+
+void Stage::get_state(float* W, float* v) {
+  sync();
+  std::vector<float> h(n_arena_);
+  for (int which = 0; which < 2; ++which) {
+    float* dst = which == 0 ? W : v;
+    if (!dst) continue;
+    hip_check(hipMemcpy(h.data(), which == 0 ? W_ : v_, n_arena_ * 4, hipMemcpyDeviceToHost), "copy state");
+    long o = 0;
+    for (const TensorInfo& t : tensors_) {
+      std::memcpy(dst + o, h.data() + t.off, t.n * 4);
+      o += t.n;
+    }
+  }
+}
+
+void Stage::get_predicted(int slot, float* out) {
+  if (slot < 0 || slot > 1) fail("slot must be 0 or 1");
+  if (!out) fail("What_host is NULL");
+  sync();
+  std::vector<char> h(n_arena_ * esz_);
+  hip_check(hipMemcpy(h.data(), what_[slot], n_arena_ * esz_, hipMemcpyDeviceToHost), "copy predicted");
+  long o = 0;
+  for (const TensorInfo& t : tensors_) {
+    for (long i = 0; i < t.n; ++i) {
+      if (dt_) {
+        uint32_t bits = static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(h.data())[t.off + i]) << 16;
+        std::memcpy(out + o + i, &bits, 4);
+      } else {
+        out[o + i] = reinterpret_cast<const float*>(h.data())[t.off + i];
+      }
+    }
+    o += t.n;
+  }
+}
+
+// --------------------------------------------------- predict and update ----
+void Stage::predict(int s, int slot) {
+  if (s < 0) fail("version difference must be >= 0");
+  if (slot < 0 || slot > 1) fail("slot must be 0 or 1");
+  hip_check(predict_slot(W_, v_, what_[slot], dt_, n_arena_, d_.lr, s, s_), "predict launch");
+}
+
+void Stage::update(int s_f, int s_b) {
+  if (!g_pending_) throw StageError(SPECTRAIN_ESTATE, "update without a gradient from a backward pass");
+  hip_check(fused_update(W_, v_, g_, what_[0], what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_dev_, s_),
+            "update launch");
+  g_pending_ = false;
+}
+
+// ------------------------------------------------------ forward/backward ----
+void Stage::forward(int64_t mb, const void* x, void* y, const int32_t* labels, float* loss) {
+  const bool ce = d_.head == SPECTRAIN_HEAD_CE;
+  if (!x) fail("x_dev is NULL");
+  if (ce && (!labels || !loss)) fail("a CE head needs labels_dev and loss_dev");
+  if (!ce && !y) fail("y_dev is NULL");
+  int free_slot = -1;
+  for (size_t i = 0; i < slots_.size(); ++i) {
+    if (slots_[i].used && slots_[i].mb == mb) throw StageError(SPECTRAIN_ESTATE, "mini-batch already in flight");
+    if (!slots_[i].used && free_slot < 0) free_slot = static_cast<int>(i);
+  }
+  if (free_slot < 0) throw StageError(SPECTRAIN_ESTATE, "N - k mini-batches already in flight");
+  switch (d_.kind) {
+    case SPECTRAIN_KIND_FC: fwd_fc(free_slot, x, y, labels, loss); break;
+    case SPECTRAIN_KIND_CONV3X3: fwd_conv(free_slot, x, y); break;
+    case SPECTRAIN_KIND_BOTTLENECK: fwd_bneck(free_slot, x, y); break;
+    case SPECTRAIN_KIND_TRANSFORMER: fwd_tfm(free_slot, x, y); break;
+    case SPECTRAIN_KIND_RESLSTM: fwd_lstm(free_slot, x, y, labels, loss); break;
+  }
+  slots_[free_slot] = Slot{true, mb, x, y};
+}
+
+void Stage::backward(int64_t mb, const void* dy, void* dx) {
+  int slot = -1;
+  for (size_t i = 0; i < slots_.size(); ++i)
+    if (slots_[i].used && slots_[i].mb == mb) slot = static_cast<int>(i);
+  if (slot < 0) throw StageError(SPECTRAIN_ESTATE, "backward of a mini-batch that is not in flight");
+  if (g_pending_) throw StageError(SPECTRAIN_ESTATE, "the previous gradient has not been applied by an update");
+  if (d_.head != SPECTRAIN_HEAD_CE && !dy) fail("dy_dev is NULL");
+  switch (d_.kind) {
+    case SPECTRAIN_KIND_FC: bwd_fc(slot, dy, dx); break;
+    case SPECTRAIN_KIND_CONV3X3: bwd_conv(slot, dy, dx); break;
+    case SPECTRAIN_KIND_BOTTLENECK: bwd_bneck(slot, dy, dx); break;
+    case SPECTRAIN_KIND_TRANSFORMER: bwd_tfm(slot, dy, dx); break;
+    case SPECTRAIN_KIND_RESLSTM: bwd_lstm(slot, dy, dx); break;
+  }
+  slots_[slot] = Slot{};
+  g_pending_ = true;
+}
+
+// ==================================================================== FC ====
+// y_l = relu(a_l W_l^T + b_l); the last layer of a CE stage produces logits.
+void Stage::fwd_fc(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
+  const int L = d_.num_layers, B = d_.batch;
+  const bool ce = d_.head == SPECTRAIN_HEAD_CE;
+  const void* a = x;
+  for (int l = 0; l < L; ++l) {
+    const int fin = l == 0 ? d_.dims[0] : d_.dims[2];
+    const int fout = l == L - 1 ? d_.dims[1] : d_.dims[2];
+    GemmDesc g = gd(B, fout, fin, opK(a, fin), opK(wf(2 * l), fin), fout);
+    if (dt_) g.epi.bias_bf16 = static_cast<const bf16_t*>(wf(2 * l + 1));
+    else g.epi.bias = static_cast<const float*>(wf(2 * l + 1));
+    void* out;
+    if (l == L - 1 && ce) {
+      out = ws<float>(0);
+      g.epi.out_f32 = static_cast<float*>(out);
+    } else {
+      out = l == L - 1 ? y : stash<char>(slot, l);
+      g.epi.relu = 1;
+      if (dt_) g.epi.out_bf16 = static_cast<bf16_t*>(out);
+      else g.epi.out_f32 = static_cast<float*>(out);
+    }
+    gemm(g);
+    a = out;
+  }
+  if (ce)
+    hip_check(softmax_ce(ws<float>(0), labels, B, d_.dims[1], stash<void>(slot, L - 1), dt_, loss, ws<float>(3), s_),
+              "softmax_ce");
+}
+
+void Stage::bwd_fc(int slot, const void* dy, void* dx) {
+  const int L = d_.num_layers, B = d_.batch;
+  const Slot& sl = slots_[slot];
+  auto act = [&](int l) -> const void* { return l == 0 ? sl.x : (l == L ? sl.y : stash<char>(slot, l - 1)); };
+  auto width = [&](int l) { return l == 0 ? d_.dims[0] : (l == L ? d_.dims[1] : d_.dims[2]); };
+  const void* dz;
+  if (d_.head == SPECTRAIN_HEAD_CE) {
+    dz = stash<void>(slot, L - 1);
+  } else {
+    hip_check(mask_relu_grad(dy, sl.y, ws<void>(1), static_cast<long>(B) * d_.dims[1], dt_, s_), "mask");
+    dz = ws<void>(1);
+  }
+  int pp = 2;
+  for (int l = L - 1; l >= 0; --l) {
+    const int fin = width(l), fout = width(l + 1);
+    GemmDesc gw = gd(fout, fin, B, opR(dz, fout), opR(act(l), fin), fin);
+    gw.epi.out_f32 = grad(2 * l);
+    gemm(gw);
+    hip_check(column_sum(dz, dt_, B, fout, fout, grad(2 * l + 1), 0, ws<float>(4), s_), "bias grad");
+    if (l == 0 && !dx) break;
+    void* out = l == 0 ? dx : ws<void>(pp);
+    GemmDesc gx = gd(B, fin, fout, opK(dz, fout), opR(wb(2 * l), fin), fin);
+    if (dt_) gx.epi.out_bf16 = static_cast<bf16_t*>(out);
+    else gx.epi.out_f32 = static_cast<float*>(out);
+    if (l > 0) gx.epi.mask = act(l);
+    gemm(gx);
+    dz = out;
+    pp = pp == 2 ? 1 : 2;
+  }
+}
+
+// ========================================================== CONV 3x3 ====
+void Stage::fwd_conv(int slot, const void* x, void* y) {
+  const int L = d_.num_layers, B = d_.batch, Cin = d_.dims[0], Cout = d_.dims[1], H = d_.dims[2], W = d_.dims[3];
+  const int P = B * H * W;
+  const void* a = x;
+  for (int l = 0; l < L; ++l) {
+    const int C = l == 0 ? Cin : Cout;
+    void* out = l == L - 1 ? y : stash<void>(slot, l);
+    GemmDesc g = gd(P, Cout, 9 * C, opConv(OP_K_CONV_FWD, a, B, H, W, C), opK(wf(l), 9 * C), Cout);
+    g.epi.relu = 1;
+    g.epi.out_bf16 = static_cast<bf16_t*>(out);
+    gemm(g);
+    a = out;
+  }
+}
+
+void Stage::bwd_conv(int slot, const void* dy, void* dx) {
+  const int L = d_.num_layers, B = d_.batch, Cin = d_.dims[0], Cout = d_.dims[1], H = d_.dims[2], W = d_.dims[3];
+  const int P = B * H * W;
+  const Slot& sl = slots_[slot];
+  auto act = [&](int l) -> const void* { return l == 0 ? sl.x : (l == L ? sl.y : stash<void>(slot, l - 1)); };
+  hip_check(mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * Cout, 1, s_), "mask");
+  const void* dz = ws<void>(0);
+  int pp = 1;
+  for (int l = L - 1; l >= 0; --l) {
+    const int C = l == 0 ? Cin : Cout;
+    GemmDesc gw = gd(Cout, 9 * C, P, opR(dz, Cout), opConv(OP_R_CONV_WGRAD, act(l), B, H, W, C), 9 * C);
+    gw.epi.out_f32 = grad(l);
+    gemm(gw);
+    if (l == 0 && !dx) break;
+    void* out = l == 0 ? dx : ws<void>(pp);
+    GemmDesc gx = gd(P, C, 9 * Cout, opConv(OP_K_CONV_DGRAD, dz, B, H, W, Cout),
+                     opConv(OP_R_FILTER_T, wb(l), B, H, W, C, Cout), C);
+    gx.epi.out_bf16 = static_cast<bf16_t*>(out);
+    if (l > 0) gx.epi.mask = act(l);
+    gemm(gx);
+    dz = out;
+    pp ^= 1;
+  }
+}
+
+// ======================================================== BOTTLENECK ====
+// y = relu(x + conv1x1_3(relu(conv3x3_2(relu(conv1x1_1(x)))))).
+void Stage::fwd_bneck(int slot, const void* x, void* y) {
+  const int L = d_.num_layers, B = d_.batch, C = d_.dims[0], Cm = d_.dims[1], H = d_.dims[2], W = d_.dims[3];
+  const int P = B * H * W;
+  const void* a = x;
+  for (int l = 0; l < L; ++l) {
+    bf16_t* t1 = stash<bf16_t>(slot, 3 * l);
+    bf16_t* t2 = stash<bf16_t>(slot, 3 * l + 1);
+    void* out = l == L - 1 ? y : stash<void>(slot, 3 * l + 2);
+    GemmDesc g1 = gd(P, Cm, C, opK(a, C), opK(wf(3 * l), C), Cm);
+    g1.epi.relu = 1;
+    g1.epi.out_bf16 = t1;
+    gemm(g1);
+    GemmDesc g2 = gd(P, Cm, 9 * Cm, opConv(OP_K_CONV_FWD, t1, B, H, W, Cm), opK(wf(3 * l + 1), 9 * Cm), Cm);
+    g2.epi.relu = 1;
+    g2.epi.out_bf16 = t2;
+    gemm(g2);
+    GemmDesc g3 = gd(P, C, Cm, opK(t2, Cm), opK(wf(3 * l + 2), Cm), C);
+    g3.epi.relu = 1;
+    g3.epi.res_bf16 = static_cast<const bf16_t*>(a);
+    g3.epi.out_bf16 = static_cast<bf16_t*>(out);
+    gemm(g3);
+    a = out;
+  }
+}
+
+void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
+  const int L = d_.num_layers, B = d_.batch, C = d_.dims[0], Cm = d_.dims[1], H = d_.dims[2], W = d_.dims[3];
+  const int P = B * H * W;
+  const Slot& sl = slots_[slot];
+  auto xin = [&](int l) -> const void* { return l == 0 ? sl.x : stash<void>(slot, 3 * (l - 1) + 2); };
+  // dr: gradient at the block's pre-ReLU output (after the output mask)
+  hip_check(mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * C, 1, s_), "mask");
+  int cur = 0;
+  bf16_t* dt2 = ws<bf16_t>(2);
+  bf16_t* dt1 = ws<bf16_t>(3);
+  for (int l = L - 1; l >= 0; --l) {
+    const bf16_t* dr = ws<bf16_t>(cur);
+    const bf16_t* t1 = stash<bf16_t>(slot, 3 * l);
+    const bf16_t* t2 = stash<bf16_t>(slot, 3 * l + 1);
+    GemmDesc g3 = gd(C, Cm, P, opR(dr, C), opR(t2, Cm), Cm);
+    g3.epi.out_f32 = grad(3 * l + 2);
+    gemm(g3);
+    GemmDesc d3 = gd(P, Cm, C, opK(dr, C), opR(wb(3 * l + 2), Cm), Cm);
+    d3.epi.out_bf16 = dt2;
+    d3.epi.mask = t2;
+    gemm(d3);
+    GemmDesc g2 = gd(Cm, 9 * Cm, P, opR(dt2, Cm), opConv(OP_R_CONV_WGRAD, t1, B, H, W, Cm), 9 * Cm);
+    g2.epi.out_f32 = grad(3 * l + 1);
+    gemm(g2);
+    GemmDesc d2 = gd(P, Cm, 9 * Cm, opConv(OP_K_CONV_DGRAD, dt2, B, H, W, Cm),
+                     opConv(OP_R_FILTER_T, wb(3 * l + 1), B, H, W, Cm, Cm), Cm);
+    d2.epi.out_bf16 = dt1;
+    d2.epi.mask = t1;
+    gemm(d2);
+    GemmDesc g1 = gd(Cm, C, P, opR(dt1, Cm), opR(xin(l), C), C);
+    g1.epi.out_f32 = grad(3 * l);
+    gemm(g1);
+    if (l == 0 && !dx) break;
+    void* out = l == 0 ? dx : ws<void>(cur ^ 1);
+    GemmDesc d1 = gd(P, C, Cm, opK(dt1, Cm), opR(wb(3 * l), C), C);
+    d1.epi.res_bf16 = dr;
+    d1.epi.out_bf16 = static_cast<bf16_t*>(out);
+    if (l > 0) d1.epi.mask = xin(l);
+    gemm(d1);
+    cur ^= 1;
+  }
+}
+
+// ======================================================= TRANSFORMER ====
+// Post-LN encoder layer; per layer stash ids 13*l + j:
+// 0 qkv, 1 P (f32), 2 P (bf16), 3 ctx, 4 r1, 5 mean1, 6 rstd1, 7 h, 8 f1,
+// 9 r2, 10 mean2, 11 rstd2, 12 layer output (l < L-1).
+void Stage::fwd_tfm(int slot, const void* x, void* y) {
+  const int L = d_.num_layers, B = d_.batch, d = d_.dims[0], Hh = d_.dims[1], F = d_.dims[2], S = d_.dims[3];
+  const int T = B * S, dh = d / Hh;
+  const float scale = 1.0f / std::sqrt(static_cast<float>(dh));
+  const void* a = x;
+  for (int l = 0; l < L; ++l) {
+    const int p = 12 * l, q = 13 * l;
+    bf16_t* qkv = stash<bf16_t>(slot, q);
+    float* P = stash<float>(slot, q + 1);
+    bf16_t* Pb = stash<bf16_t>(slot, q + 2);
+    bf16_t* ctx = stash<bf16_t>(slot, q + 3);
+    bf16_t* r1 = stash<bf16_t>(slot, q + 4);
+    bf16_t* h = stash<bf16_t>(slot, q + 7);
+    bf16_t* f1 = stash<bf16_t>(slot, q + 8);
+    bf16_t* r2 = stash<bf16_t>(slot, q + 9);
+    void* out = l == L - 1 ? y : stash<void>(slot, q + 12);
+
+    GemmDesc g = gd(T, 3 * d, d, opK(a, d), opK(wf(p), d), 3 * d);
+    g.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 1));
+    g.epi.out_bf16 = qkv;
+    gemm(g);
+    // scores[b, h] = Q K^T * scale
+    Operand qa = opK(qkv, 3 * d), kb = opK(qkv + d, 3 * d);
+    qa.bs1 = kb.bs1 = static_cast<long>(S) * 3 * d;
+    qa.bs2 = kb.bs2 = dh;
+    GemmDesc sc = gd(S, S, dh, qa, kb, S);
+    sc.batch = B * Hh;
+    sc.zdiv = Hh;
+    sc.epi.bs1 = static_cast<long>(Hh) * S * S;
+    sc.epi.bs2 = static_cast<long>(S) * S;
+    sc.epi.alpha = scale;
+    sc.epi.out_f32 = ws<float>(0);
+    gemm(sc);
+    hip_check(softmax_rows(ws<float>(0), B * Hh * S, S, P, Pb, s_), "softmax");
+    // ctx[b, :, h] = P V
+    Operand pa = opK(Pb, S), vb = opR(qkv + 2 * d, 3 * d);
+    pa.bs1 = static_cast<long>(Hh) * S * S;
+    pa.bs2 = static_cast<long>(S) * S;
+    vb.bs1 = static_cast<long>(S) * 3 * d;
+    vb.bs2 = dh;
+    GemmDesc pv = gd(S, dh, S, pa, vb, d);
+    pv.batch = B * Hh;
+    pv.zdiv = Hh;
+    pv.epi.bs1 = static_cast<long>(S) * d;
+    pv.epi.bs2 = dh;
+    pv.epi.out_bf16 = ctx;
+    gemm(pv);
+    GemmDesc go = gd(T, d, d, opK(ctx, d), opK(wf(p + 2), d), d);
+    go.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 3));
+    go.epi.res_bf16 = static_cast<const bf16_t*>(a);
+    go.epi.out_bf16 = r1;
+    gemm(go);
+    hip_check(layernorm_fwd(r1, static_cast<const bf16_t*>(wf(p + 4)), static_cast<const bf16_t*>(wf(p + 5)), T, d,
+                            LN_EPS, h, stash<float>(slot, q + 5), stash<float>(slot, q + 6), s_),
+              "layernorm");
+    GemmDesc g1 = gd(T, F, d, opK(h, d), opK(wf(p + 6), d), F);
+    g1.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 7));
+    g1.epi.relu = 1;
+    g1.epi.out_bf16 = f1;
+    gemm(g1);
+    GemmDesc g2 = gd(T, d, F, opK(f1, F), opK(wf(p + 8), F), d);
+    g2.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 9));
+    g2.epi.res_bf16 = h;
+    g2.epi.out_bf16 = r2;
+    gemm(g2);
+    hip_check(layernorm_fwd(r2, static_cast<const bf16_t*>(wf(p + 10)), static_cast<const bf16_t*>(wf(p + 11)), T, d,
+                            LN_EPS, static_cast<bf16_t*>(out), stash<float>(slot, q + 10), stash<float>(slot, q + 11),
+                            s_),
+              "layernorm");
+    a = out;
+  }
+}
+
+// workspace ids: 0 scores/dP (f32), 1 dS, 2/3 layer-output gradient ping-pong,
+// 4 dr2, 5 df1, 6 dh, 7 dr1, 8 dctx, 9 dqkv, 10 partials
+void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
+  const int L = d_.num_layers, B = d_.batch, d = d_.dims[0], Hh = d_.dims[1], F = d_.dims[2], S = d_.dims[3];
+  const int T = B * S, dh = d / Hh;
+  const float scale = 1.0f / std::sqrt(static_cast<float>(dh));
+  const Slot& sl = slots_[slot];
+  float* part = ws<float>(10);
+  const void* gy = dy;
+  int pp = 2;
+  for (int l = L - 1; l >= 0; --l) {
+    const int p = 12 * l, q = 13 * l;
+    const void* a = l == 0 ? sl.x : stash<void>(slot, 13 * (l - 1) + 12);
+    const bf16_t* qkv = stash<bf16_t>(slot, q);
+    const float* P = stash<float>(slot, q + 1);
+    const bf16_t* Pb = stash<bf16_t>(slot, q + 2);
+    const bf16_t* ctx = stash<bf16_t>(slot, q + 3);
+    const bf16_t* r1 = stash<bf16_t>(slot, q + 4);
+    const bf16_t* h = stash<bf16_t>(slot, q + 7);
+    const bf16_t* f1 = stash<bf16_t>(slot, q + 8);
+    const bf16_t* r2 = stash<bf16_t>(slot, q + 9);
+    bf16_t* dr2 = ws<bf16_t>(4);
+    bf16_t* df1 = ws<bf16_t>(5);
+    bf16_t* dhh = ws<bf16_t>(6);
+    bf16_t* dr1 = ws<bf16_t>(7);
+    bf16_t* dctx = ws<bf16_t>(8);
+    bf16_t* dqkv = ws<bf16_t>(9);
+
+    hip_check(layernorm_bwd(static_cast<const bf16_t*>(gy), r2, stash<float>(slot, q + 10), stash<float>(slot, q + 11),
+                            static_cast<const bf16_t*>(wb(p + 10)), T, d, dr2, grad(p + 10), grad(p + 11), part, s_),
+              "layernorm bwd");
+    GemmDesc w2 = gd(d, F, T, opR(dr2, d), opR(f1, F), F);
+    w2.epi.out_f32 = grad(p + 8);
+    gemm(w2);
+    hip_check(column_sum(dr2, 1, T, d, d, grad(p + 9), 0, part, s_), "bias grad");
+    GemmDesc x2 = gd(T, F, d, opK(dr2, d), opR(wb(p + 8), F), F);
+    x2.epi.mask = f1;
+    x2.epi.out_bf16 = df1;
+    gemm(x2);
+    GemmDesc w1 = gd(F, d, T, opR(df1, F), opR(h, d), d);
+    w1.epi.out_f32 = grad(p + 6);
+    gemm(w1);
+    hip_check(column_sum(df1, 1, T, F, F, grad(p + 7), 0, part, s_), "bias grad");
+    GemmDesc x1 = gd(T, d, F, opK(df1, F), opR(wb(p + 6), d), d);
+    x1.epi.res_bf16 = dr2;
+    x1.epi.out_bf16 = dhh;
+    gemm(x1);
+    hip_check(layernorm_bwd(dhh, r1, stash<float>(slot, q + 5), stash<float>(slot, q + 6),
+                            static_cast<const bf16_t*>(wb(p + 4)), T, d, dr1, grad(p + 4), grad(p + 5), part, s_),
+              "layernorm bwd");
+    GemmDesc wo = gd(d, d, T, opR(dr1, d), opR(ctx, d), d);
+    wo.epi.out_f32 = grad(p + 2);
+    gemm(wo);
+    hip_check(column_sum(dr1, 1, T, d, d, grad(p + 3), 0, part, s_), "bias grad");
+    GemmDesc xo = gd(T, d, d, opK(dr1, d), opR(wb(p + 2), d), d);
+    xo.epi.out_bf16 = dctx;
+    gemm(xo);
+
+    // attention backward, batched over (b, h)
+    const long sS = static_cast<long>(S) * S, sHSS = static_cast<long>(Hh) * S * S;
+    const long sQ = static_cast<long>(S) * 3 * d, sO = static_cast<long>(S) * d;
+    {  // dV = P^T dO
+      Operand A = opR(Pb, S), Bo = opR(dctx, d);
+      A.bs1 = sHSS;
+      A.bs2 = sS;
+      Bo.bs1 = sO;
+      Bo.bs2 = dh;
+      GemmDesc g = gd(S, dh, S, A, Bo, 3 * d);
+      g.batch = B * Hh;
+      g.zdiv = Hh;
+      g.epi.bs1 = sQ;
+      g.epi.bs2 = dh;
+      g.epi.out_bf16 = dqkv + 2 * d;
+      gemm(g);
+    }
+    {  // dP = dO V^T
+      Operand A = opK(dctx, d), Bv = opK(qkv + 2 * d, 3 * d);
+      A.bs1 = sO;
+      A.bs2 = dh;
+      Bv.bs1 = sQ;
+      Bv.bs2 = dh;
+      GemmDesc g = gd(S, S, dh, A, Bv, S);
+      g.batch = B * Hh;
+      g.zdiv = Hh;
+      g.epi.bs1 = sHSS;
+      g.epi.bs2 = sS;
+      g.epi.out_f32 = ws<float>(0);
+      gemm(g);
+    }
+    hip_check(softmax_bwd(P, ws<float>(0), B * Hh * S, S, ws<bf16_t>(1), s_), "softmax bwd");
+    {  // dQ = dS K * scale
+      Operand A = opK(ws<bf16_t>(1), S), Bk = opR(qkv + d, 3 * d);
+      A.bs1 = sHSS;
+      A.bs2 = sS;
+      Bk.bs1 = sQ;
+      Bk.bs2 = dh;
+      GemmDesc g = gd(S, dh, S, A, Bk, 3 * d);
+      g.batch = B * Hh;
+      g.zdiv = Hh;
+      g.epi.bs1 = sQ;
+      g.epi.bs2 = dh;
+      g.epi.alpha = scale;
+      g.epi.out_bf16 = dqkv;
+      gemm(g);
+    }
+    {  // dK = dS^T Q * scale
+      Operand A = opR(ws<bf16_t>(1), S), Bq = opR(qkv, 3 * d);
+      A.bs1 = sHSS;
+      A.bs2 = sS;
+      Bq.bs1 = sQ;
+      Bq.bs2 = dh;
+      GemmDesc g = gd(S, dh, S, A, Bq, 3 * d);
+      g.batch = B * Hh;
+      g.zdiv = Hh;
+      g.epi.bs1 = sQ;
+      g.epi.bs2 = dh;
+      g.epi.alpha = scale;
+      g.epi.out_bf16 = dqkv + d;
+      gemm(g);
+    }
+    GemmDesc wq = gd(3 * d, d, T, opR(dqkv, 3 * d), opR(a, d), d);
+    wq.epi.out_f32 = grad(p);
+    gemm(wq);
+    hip_check(column_sum(dqkv, 1, T, 3 * d, 3 * d, grad(p + 1), 0, part, s_), "bias grad");
+    if (l == 0 && !dx) break;
+    void* out = l == 0 ? dx : ws<void>(pp);
+    GemmDesc xq = gd(T, d, 3 * d, opK(dqkv, 3 * d), opR(wb(p), d), d);
+    xq.epi.res_bf16 = dr1;
+    xq.epi.out_bf16 = static_cast<bf16_t*>(out);
+    gemm(xq);
+    gy = out;
+    pp = pp == 2 ? 3 : 2;
+  }
+}
+
+// ===================================================== RESIDUAL LSTM ====
+// per layer stash ids 4*l + j: 0 gates (f32 [T,B,4H]), 1 c (f32), 2 h (bf16),
+// 3 layer output u_{l+1} (bf16); id 4L: dlogits (bf16) with a CE head.
+// workspace: 0 zx (f32), 1 logits (f32), 2/3 du ping-pong, 4 dz (bf16),
+// 5 dh_rec (f32), 6 dc (f32), 7 row losses, 8 partials.
+void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
+  const int L = d_.num_layers, B = d_.batch, I = d_.dims[0], H = d_.dims[1], T = d_.dims[2], V = d_.dims[3];
+  const bool ce = d_.head == SPECTRAIN_HEAD_CE;
+  const long TB = static_cast<long>(T) * B;
+  const void* u = x;
+  float* zx = ws<float>(0);
+  for (int l = 0; l < L; ++l) {
+    const int p = 3 * l, q = 4 * l;
+    const int in = l == 0 ? I : H;
+    float* gates = stash<float>(slot, q);
+    float* c = stash<float>(slot, q + 1);
+    bf16_t* hs = stash<bf16_t>(slot, q + 2);
+    void* out = (l == L - 1 && !ce) ? y : stash<void>(slot, q + 3);
+    GemmDesc gx = gd(static_cast<int>(TB), 4 * H, in, opK(u, in), opK(wf(p), in), 4 * H);
+    gx.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 2));
+    gx.epi.out_f32 = zx;
+    gemm(gx);
+    for (int t = 0; t < T; ++t) {
+      float* zt = zx + static_cast<long>(t) * B * 4 * H;
+      if (t > 0) {
+        GemmDesc gh = gd(B, 4 * H, H, opK(hs + static_cast<long>(t - 1) * B * H, H), opK(wf(p + 1), H), 4 * H);
+        gh.epi.res_f32 = zt;
+        gh.epi.out_f32 = zt;
+        gemm(gh);
+      }
+      hip_check(lstm_cell_fwd(zt, t > 0 ? c + static_cast<long>(t - 1) * B * H : nullptr, B, H,
+                              gates + static_cast<long>(t) * B * 4 * H, c + static_cast<long>(t) * B * H,
+                              hs + static_cast<long>(t) * B * H, s_),
+                "lstm cell");
+    }
+    hip_check(add_bf16(static_cast<const bf16_t*>(u), hs, static_cast<bf16_t*>(out), TB * H, s_), "residual");
+    u = out;
+  }
+  if (ce) {
+    GemmDesc gv = gd(static_cast<int>(TB), V, H, opK(u, H), opK(wf(3 * L), H), V);
+    gv.epi.bias_bf16 = static_cast<const bf16_t*>(wf(3 * L + 1));
+    gv.epi.out_f32 = ws<float>(1);
+    gemm(gv);
+    hip_check(softmax_ce(ws<float>(1), labels, static_cast<int>(TB), V, stash<void>(slot, 4 * L), 1, loss, ws<float>(7),
+                         s_),
+              "softmax_ce");
+  }
+}
+
+void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
+  const int L = d_.num_layers, B = d_.batch, I = d_.dims[0], H = d_.dims[1], T = d_.dims[2], V = d_.dims[3];
+  const bool ce = d_.head == SPECTRAIN_HEAD_CE;
+  const long TB = static_cast<long>(T) * B;
+  const Slot& sl = slots_[slot];
+  float* part = ws<float>(8);
+  const void* du = dy;
+  int pp = 2;
+  if (ce) {
+    const bf16_t* dl = stash<bf16_t>(slot, 4 * L);
+    const void* uL = stash<void>(slot, 4 * (L - 1) + 3);
+    GemmDesc gw = gd(V, H, static_cast<int>(TB), opR(dl, V), opR(uL, H), H);
+    gw.epi.out_f32 = grad(3 * L);
+    gemm(gw);
+    hip_check(column_sum(dl, 1, TB, V, V, grad(3 * L + 1), 0, part, s_), "bias grad");
+    GemmDesc gx = gd(static_cast<int>(TB), H, V, opK(dl, V), opR(wb(3 * L), H), H);
+    gx.epi.out_bf16 = ws<bf16_t>(pp);
+    gemm(gx);
+    du = ws<void>(pp);
+    pp = 3;
+  }
+  bf16_t* dz = ws<bf16_t>(4);
+  float* dh_rec = ws<float>(5);
+  float* dc = ws<float>(6);
+  for (int l = L - 1; l >= 0; --l) {
+    const int p = 3 * l, q = 4 * l;
+    const int in = l == 0 ? I : H;
+    const void* u = l == 0 ? sl.x : stash<void>(slot, 4 * (l - 1) + 3);
+    const float* gates = stash<float>(slot, q);
+    const float* c = stash<float>(slot, q + 1);
+    const bf16_t* hs = stash<bf16_t>(slot, q + 2);
+    hip_check(fill_f32(dc, 0.0f, static_cast<long>(B) * H, s_), "clear dc");
+    for (int t = T - 1; t >= 0; --t) {
+      const long o = static_cast<long>(t) * B;
+      hip_check(lstm_cell_bwd(static_cast<const bf16_t*>(du) + o * H, t < T - 1 ? dh_rec : nullptr, gates + o * 4 * H,
+                              c + o * H, t > 0 ? c + (o - B) * H : nullptr, B, H, dc, dz + o * 4 * H, s_),
+                "lstm cell bwd");
+      if (t > 0) {
+        GemmDesc gh = gd(B, H, 4 * H, opK(dz + o * 4 * H, 4 * H), opR(wb(p + 1), H), H);
+        gh.epi.out_f32 = dh_rec;
+        gemm(gh);
+      }
+    }
+    GemmDesc wx = gd(4 * H, in, static_cast<int>(TB), opR(dz, 4 * H), opR(u, in), in);
+    wx.epi.out_f32 = grad(p);
+    gemm(wx);
+    if (T > 1) {
+      GemmDesc wh = gd(4 * H, H, static_cast<int>(TB - B), opR(dz + static_cast<long>(B) * 4 * H, 4 * H), opR(hs, H), H);
+      wh.epi.out_f32 = grad(p + 1);
+      gemm(wh);
+    } else {
+      hip_check(fill_f32(grad(p + 1), 0.0f, 4L * H * H, s_), "clear grad");
+    }
+    hip_check(column_sum(dz, 1, TB, 4 * H, 4 * H, grad(p + 2), 0, part, s_), "bias grad");
+    if (l == 0 && !dx) break;
+    void* out = l == 0 ? dx : ws<void>(pp);
+    GemmDesc gxx = gd(static_cast<int>(TB), in, 4 * H, opK(dz, 4 * H), opR(wb(p), in), in);
+    gxx.epi.res_bf16 = static_cast<const bf16_t*>(du);
+    gxx.epi.out_bf16 = static_cast<bf16_t*>(out);
+    gemm(gxx);
+    du = out;
+    pp = pp == 2 ? 3 : 2;
+  }
+}
+
+}  // namespace spx

@@ -1,0 +1,121 @@
+// One SpecTrain pipeline stage on one GPU: parameter arenas, activation
+// stash ring and the per-kind forward/backward sequences of kernel launches.
+#pragma once
+
+#include <cstdint>
+#include <stdexcept>
+#include <string>
+#include <vector>
+
+#include "../../include/spectrain.h"
+#include "kernels.hpp"
+
+namespace spx {
+
+// Failure carrying an ABI status code; caught at the C boundary.
+struct StageError : std::runtime_error {
+  int code;
+  StageError(int c, const std::string& m) : std::runtime_error(m), code(c) {}
+};
+
+void hip_check(hipError_t e, const char* what);
+
+// A set of device sub-buffers carved from one hipMalloc, each 256-byte aligned.
+class DeviceBlock {
+ public:
+  DeviceBlock() = default;
+  DeviceBlock(const DeviceBlock&) = delete;
+  DeviceBlock& operator=(const DeviceBlock&) = delete;
+  DeviceBlock(DeviceBlock&& o) noexcept : base_(o.base_), total_(o.total_) { o.base_ = nullptr; o.total_ = 0; }
+  size_t add(size_t bytes);  // returns an offset; call before allocate()
+  void allocate();
+  void release();
+  template <typename T>
+  T* at(size_t off) const { return reinterpret_cast<T*>(base_ + off); }
+  size_t bytes() const { return total_; }
+  ~DeviceBlock() { release(); }
+
+ private:
+  char* base_ = nullptr;
+  size_t total_ = 0;
+};
+
+struct TensorInfo {
+  long off;   // element offset in the padded arenas
+  long n;     // element count
+};
+
+class Stage {
+ public:
+  Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hipStream_t s);
+  ~Stage();
+
+  size_t num_params() const { return n_params_; }
+  void predict(int s, int slot);
+  void forward(int64_t mb, const void* x, void* y, const int32_t* labels, float* loss);
+  void backward(int64_t mb, const void* dy, void* dx);
+  void update(int s_f, int s_b);
+  void get_state(float* W, float* v);
+  void set_state(const float* W, const float* v);
+  void get_predicted(int slot, float* out);
+  bool nonfinite() const { return *reinterpret_cast<volatile int*>(flag_host_) != 0; }
+  void sync();
+
+ private:
+  struct Slot {
+    bool used = false;
+    int64_t mb = -1;
+    const void* x = nullptr;
+    void* y = nullptr;
+  };
+
+  // ---- layout and buffers
+  void build_layout();
+  void plan_buffers();
+  long tensor_off(int i) const { return tensors_[i].off; }
+  const void* wf(int i) const;   // predicted slot 0 (forward) of tensor i
+  const void* wb(int i) const;   // predicted slot 1 (backward) of tensor i
+  float* grad(int i) const { return g_ + tensors_[i].off; }
+  template <typename T>
+  T* stash(int slot, int buf) const { return slot_blocks_[slot].at<T>(stash_off_[buf]); }
+  template <typename T>
+  T* ws(int buf) const { return ws_block_.at<T>(ws_off_[buf]); }
+  void gemm(const GemmDesc& d);
+
+  // ---- per kind
+  void fwd_fc(int slot, const void* x, void* y, const int32_t* labels, float* loss);
+  void bwd_fc(int slot, const void* dy, void* dx);
+  void fwd_conv(int slot, const void* x, void* y);
+  void bwd_conv(int slot, const void* dy, void* dx);
+  void fwd_bneck(int slot, const void* x, void* y);
+  void bwd_bneck(int slot, const void* dy, void* dx);
+  void fwd_tfm(int slot, const void* x, void* y);
+  void bwd_tfm(int slot, const void* dy, void* dx);
+  void fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, float* loss);
+  void bwd_lstm(int slot, const void* dy, void* dx);
+
+  spectrain_stage_desc d_;
+  hipStream_t s_;
+  int dt_;        // 1 = bf16 operands, 0 = float32
+  size_t esz_;    // operand element size
+  std::vector<TensorInfo> tensors_;
+  size_t n_params_ = 0;
+  long n_arena_ = 0;
+
+  DeviceBlock arena_;
+  float* W_ = nullptr;
+  float* v_ = nullptr;
+  float* g_ = nullptr;
+  void* what_[2] = {nullptr, nullptr};
+  int* flag_host_ = nullptr;   // pinned, mapped: set by the update kernel on a non-finite value
+  int* flag_dev_ = nullptr;
+
+  std::vector<Slot> slots_;
+  std::vector<DeviceBlock> slot_blocks_;
+  std::vector<size_t> stash_off_;
+  DeviceBlock ws_block_;
+  std::vector<size_t> ws_off_;
+  bool g_pending_ = false;
+};
+
+}  // namespace spx

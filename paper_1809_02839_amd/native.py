@@ -1,0 +1,163 @@
+"""ctypes binding of libspectrain.so: one Python function per C ABI entry point
+(argument marshalling only; every step of the stage runs in the library).
+
+Device buffers are passed as torch tensors (their data pointers) and streams
+as torch.cuda.Stream objects; host arrays as float32 NumPy arrays.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspectrain.so")
+
+ABI_VERSION = 1
+OK, EINVAL, ENOMEM, EHIP, ESTATE, ENONFINITE = range(6)
+STATUS_NAMES = {OK: "OK", EINVAL: "EINVAL", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE",
+                ENONFINITE: "ENONFINITE"}
+FP32, BF16 = 0, 1
+KIND_FC, KIND_CONV3X3, KIND_BOTTLENECK, KIND_TRANSFORMER, KIND_RESLSTM = range(5)
+HEAD_NONE, HEAD_CE = 0, 1
+KIND_BY_NAME = {"fc": KIND_FC, "conv3x3": KIND_CONV3X3, "bottleneck": KIND_BOTTLENECK,
+                "transformer": KIND_TRANSFORMER, "reslstm": KIND_RESLSTM}
+
+EXPORTED = ("spectrain_version_difference", "spectrain_stage_create", "spectrain_stage_num_params",
+            "spectrain_stage_predict", "spectrain_stage_forward", "spectrain_stage_backward",
+            "spectrain_stage_update", "spectrain_stage_get_state", "spectrain_stage_set_state",
+            "spectrain_stage_get_predicted", "spectrain_stage_destroy", "spectrain_last_error")
+
+
+class StageDesc(ctypes.Structure):
+    _fields_ = [("abi_version", ctypes.c_uint32), ("kind", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("head", ctypes.c_int32), ("stage_index", ctypes.c_int32), ("num_stages", ctypes.c_int32),
+                ("batch", ctypes.c_int32), ("num_layers", ctypes.c_int32), ("dims", ctypes.c_int32 * 8),
+                ("lr", ctypes.c_float), ("momentum", ctypes.c_float)]
+
+
+class SpecTrainError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    """Open libspectrain.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_1809_02839_amd.build.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        fp = ctypes.POINTER(ctypes.c_float)
+        sig = {
+            "spectrain_version_difference": (i32, [i32, i32, i32]),
+            "spectrain_stage_create": (ctypes.c_int, [ctypes.POINTER(StageDesc), fp, sz, vp, ctypes.POINTER(vp)]),
+            "spectrain_stage_num_params": (ctypes.c_int, [vp, ctypes.POINTER(sz)]),
+            "spectrain_stage_predict": (ctypes.c_int, [vp, i32, i32]),
+            "spectrain_stage_forward": (ctypes.c_int, [vp, i64, vp, vp, vp, vp]),
+            "spectrain_stage_backward": (ctypes.c_int, [vp, i64, vp, vp]),
+            "spectrain_stage_update": (ctypes.c_int, [vp, i32, i32]),
+            "spectrain_stage_get_state": (ctypes.c_int, [vp, fp, fp]),
+            "spectrain_stage_set_state": (ctypes.c_int, [vp, fp, fp]),
+            "spectrain_stage_get_predicted": (ctypes.c_int, [vp, i32, fp]),
+            "spectrain_stage_destroy": (ctypes.c_int, [vp]),
+            "spectrain_last_error": (ctypes.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def _check(code):
+    if code != OK:
+        raise SpecTrainError(code, lib().spectrain_last_error().decode())
+
+
+def _fptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+def _dptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def version_difference(k: int, N: int, forward: bool) -> int:
+    return int(lib().spectrain_version_difference(k, N, 1 if forward else 0))
+
+
+def make_desc(kind, dtype, head, stage_index, num_stages, batch, num_layers, dims, lr, momentum) -> StageDesc:
+    d = StageDesc()
+    d.abi_version = ABI_VERSION
+    d.kind = KIND_BY_NAME[kind] if isinstance(kind, str) else int(kind)
+    d.dtype = {"fp32": FP32, "bf16": BF16}[dtype] if isinstance(dtype, str) else int(dtype)
+    d.head = {"none": HEAD_NONE, "ce": HEAD_CE}[head] if isinstance(head, str) else int(head)
+    d.stage_index, d.num_stages, d.batch, d.num_layers = stage_index, num_stages, batch, num_layers
+    for i, v in enumerate(dims):
+        d.dims[i] = int(v)
+    d.lr, d.momentum = lr, momentum
+    return d
+
+
+def desc_from_spec(spec) -> StageDesc:
+    return make_desc(spec.kind, spec.dtype, spec.head, spec.stage_index, spec.num_stages, spec.batch,
+                     spec.num_layers, spec.dims, spec.lr, spec.momentum)
+
+
+class Stage:
+    """Owner of one spectrain_stage_t; methods map 1:1 to the C entry points."""
+
+    def __init__(self, desc: StageDesc, W0: np.ndarray, stream=None):
+        W0 = np.ascontiguousarray(W0, dtype=np.float32)
+        self._stream = stream
+        handle = ctypes.c_void_p()
+        sptr = ctypes.c_void_p(stream.cuda_stream) if stream is not None else None
+        _check(lib().spectrain_stage_create(ctypes.byref(desc), _fptr(W0), W0.size, sptr, ctypes.byref(handle)))
+        self.h = handle
+        self.desc = desc
+        n = ctypes.c_size_t()
+        _check(lib().spectrain_stage_num_params(self.h, ctypes.byref(n)))
+        self.n_params = n.value
+
+    def predict(self, s: int, slot: int):
+        _check(lib().spectrain_stage_predict(self.h, s, slot))
+
+    def forward(self, mb: int, x, y=None, labels=None, loss=None):
+        _check(lib().spectrain_stage_forward(self.h, mb, _dptr(x), _dptr(y), _dptr(labels), _dptr(loss)))
+
+    def backward(self, mb: int, dy=None, dx=None):
+        _check(lib().spectrain_stage_backward(self.h, mb, _dptr(dy), _dptr(dx)))
+
+    def update(self, s_next_fwd: int, s_next_bwd: int):
+        _check(lib().spectrain_stage_update(self.h, s_next_fwd, s_next_bwd))
+
+    def get_state(self):
+        W = np.empty(self.n_params, np.float32)
+        v = np.empty(self.n_params, np.float32)
+        _check(lib().spectrain_stage_get_state(self.h, _fptr(W), _fptr(v)))
+        return W, v
+
+    def set_state(self, W: np.ndarray, v=None):
+        W = np.ascontiguousarray(W, dtype=np.float32)
+        v = None if v is None else np.ascontiguousarray(v, dtype=np.float32)
+        _check(lib().spectrain_stage_set_state(self.h, _fptr(W), _fptr(v)))
+
+    def get_predicted(self, slot: int):
+        out = np.empty(self.n_params, np.float32)
+        _check(lib().spectrain_stage_get_predicted(self.h, slot, _fptr(out)))
+        return out
+
+    def destroy(self):
+        if self.h is not None and self.h.value:
+            _check(lib().spectrain_stage_destroy(self.h))
+        self.h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass

@@ -1,0 +1,87 @@
+"""Comparison helpers for the GPU-vs-oracle parity tests.
+
+Metric: relative error of a whole tensor in the 2-norm,
+    rel(a, b) = ||a - b||_2 / ||b||_2      (b: the oracle's value),
+taken per tensor and per step; the bound applies to the maximum over steps:
+1e-4 for float32 stages and 2e-2 for bf16 stages. The max-abs normwise error
+max|a - b| / max|b| is reported alongside as a diagnostic.
+
+Why the 2-norm: every contraction feeding a ReLU decides a mask from a value
+both sides compute correctly but in different summation orders. Where that
+value sits within rounding noise of zero, the two sides can legitimately take
+opposite decisions; with random-sign upstream gradients each weight-gradient
+element is a random-walk sum of n terms, so one such decision moves one
+element by about 1/sqrt(n) of its size (6 % at n = 256) while moving the whole
+tensor by a negligible amount in the 2-norm.
+
+The weight change W_t - W_0 gets one more term: W is stored in float32 on both
+sides, so a value computed on opposite sides of a float32 rounding boundary is
+stored one float32 step apart, at most 2^-23 |W| per element. The bound on the
+weight change is therefore tol + 2^-23 ||W_t|| / ||W_t - W_0||, which matters
+only in the first steps of float32 stages (one step of the float32 MLP moves W
+by ~1e-3 of its norm).
+"""
+import numpy as np
+
+import synth
+from oracle import trajectory
+
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64).reshape(-1)
+    b = np.asarray(b, np.float64).reshape(-1)
+    if b.size == 0:
+        return 0.0
+    return float(np.linalg.norm(a - b) / max(float(np.linalg.norm(b)), 1e-300))
+
+
+def normwise(a, b):
+    a = np.asarray(a, np.float64).reshape(-1)
+    b = np.asarray(b, np.float64).reshape(-1)
+    if b.size == 0:
+        return 0.0
+    return float(np.max(np.abs(a - b)) / max(float(np.max(np.abs(b))), 1e-300))
+
+
+def dw_bound(tol, W_t, W0):
+    dW = np.linalg.norm(np.asarray(W_t, np.float64) - np.asarray(W0, np.float64))
+    return tol + 2.0 ** -23 * float(np.linalg.norm(W_t)) / max(float(dW), 1e-300)
+
+
+class Worst:
+    """Running maxima of both metrics per quantity, with the bound checked."""
+
+    def __init__(self, name):
+        self.name = name
+        self.rel = {}
+        self.nw = {}
+
+    def check(self, key, a, b, bound, where=""):
+        r, n = rel(a, b), normwise(a, b)
+        self.rel[key] = max(self.rel.get(key, 0.0), r)
+        self.nw[key] = max(self.nw.get(key, 0.0), n)
+        assert r <= bound, (self.name, key, where, r, bound)
+
+    def note(self, key, a, b):
+        """Record both metrics without a bound (diagnostic only)."""
+        self.rel[key] = max(self.rel.get(key, 0.0), rel(a, b))
+        self.nw[key] = max(self.nw.get(key, 0.0), normwise(a, b))
+
+    def report(self):
+        return ", ".join(f"{k}: rel {self.rel[k]:.2e} maxabs {self.nw[k]:.2e}" for k in self.rel)
+
+
+def synthetic_inputs(spec, m):
+    x = synth.stage_input(spec, m)
+    dy = synth.upstream_grad(spec, m) if spec.head == "none" else None
+    lab = synth.labels(spec, m) if spec.head == "ce" else None
+    return x, dy, lab
+
+
+def oracle_trajectory(wl, steps=None, keep_io=True):
+    states = {}
+    r = trajectory.run(wl, steps=steps, keep_io=keep_io,
+                       on_update=lambda k, u, W, v: states.__setitem__((k, u), (W.copy(), v.copy())))
+    return r, states

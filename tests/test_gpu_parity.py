@@ -1,0 +1,128 @@
+"""GPU parity: the HIP stage step, driven through the C ABI in the
+one-forward-one-backward order, against the CPU oracle on the same seeded
+inputs (every stage kind, reduced sizes spanning several GEMM tiles with
+ragged tails, plus the full-size float32 MLP pipeline)."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import method, stages
+from parity import TOL, Worst, dw_bound, oracle_trajectory, synthetic_inputs
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _pipeline(wl, **kw):
+    from paper_1809_02839_amd.pipeline import Pipeline
+    return Pipeline(wl.stages, [synth.initial_params(s) for s in wl.stages], **kw)
+
+
+def _gpu_trajectory(wl, steps=None):
+    pipe = _pipeline(wl)
+    states = {}
+
+    def cb(k, u, st):
+        states[(k, u)] = st.get_state()
+
+    out = pipe.run(wl.steps if steps is None else steps, synthetic_inputs, on_update=cb, keep_io=True)
+    torch.cuda.synchronize()
+    return pipe, out, states
+
+
+# Free-running 20-step trajectories, gated for the workloads whose oracle
+# conditioning probe (a 2^-24 relative perturbation of W0 carried through the
+# same 20 steps) stays far below the bound; the ReLU-dominated reduced conv,
+# bottleneck and transformer stages amplify single mask decisions and are
+# covered step by step in test_gpu_stepwise.py.
+TRAJ = ["mlp3", "mlp3_small", "reslstm_small"]
+
+
+@pytest.mark.parametrize("name", TRAJ)
+def test_trajectory_matches_oracle(name):
+    wl = synth.ALL_WORKLOADS[name]
+    tol = TOL[wl.stages[0].dtype]
+    print(f"[parity] {name}", flush=True)
+    ref, ref_states = oracle_trajectory(wl)
+    pipe, out, states = _gpu_trajectory(wl)
+    worst = Worst(name)
+    for spec in wl.stages:
+        k = spec.stage_index
+        W0 = synth.initial_params(spec).astype(np.float64)
+        for u in range(1, wl.steps + 1):
+            Wg, vg = states[(k, u)]
+            Wo, vo = ref_states[(k, u)]
+            worst.check("W", Wg, Wo, tol, f"k{k} u{u}")
+            worst.check("v", vg, vo, tol, f"k{k} u{u}")
+            worst.check("W-W0", Wg - W0, Wo - W0, dw_bound(tol, Wo, W0), f"k{k} u{u}")
+    for (k, m), y in out["y"].items():
+        worst.check("y", y.float().cpu().numpy(), ref["y"][(k, m)], tol, f"k{k} m{m}")
+    for (k, m), dx in out["dx"].items():
+        worst.check("dx", dx.float().cpu().numpy(), ref["dx"][(k, m)], tol, f"k{k} m{m}")
+    if ref["loss"]:
+        ms = sorted(ref["loss"])
+        worst.check("loss", [out["loss"][m].item() for m in ms], [ref["loss"][m] for m in ms], tol)
+    print(f"[parity] {name}: {worst.report()}", flush=True)
+    pipe.destroy()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("s", [0, 1, 2, 3, 7])
+def test_predict_matches_eq4(dtype, s):
+    """spectrain_stage_predict: What = W - s eta v rounded to the operand dtype."""
+    from paper_1809_02839_amd import native
+    spec = synth.StageSpec("fc", dtype, "none", 0, 4, 4, 2, (40, 24, 64), 0.0123, 0.9)
+    n = synth.num_params(spec)
+    rng = np.random.default_rng(s)
+    W = rng.standard_normal(n).astype(np.float32)
+    v = (rng.standard_normal(n) * 0.5).astype(np.float32)
+    st = native.Stage(native.desc_from_spec(spec), W)
+    st.set_state(W, v)
+    st.predict(s, 0)
+    st.predict(max(s - 1, 0), 1)
+    got0, got1 = st.get_predicted(0), st.get_predicted(1)
+    lr = float(np.float32(spec.lr))
+    exp0 = stages.weight_rounder(spec)(method.predict(W, v, s, lr))
+    exp1 = stages.weight_rounder(spec)(method.predict(W, v, max(s - 1, 0), lr))
+    if dtype == "fp32":
+        np.testing.assert_allclose(got0, exp0, rtol=1.2e-7, atol=1e-30)
+        np.testing.assert_allclose(got1, exp1, rtol=1.2e-7, atol=1e-30)
+    else:
+        # the kernel rounds its float32 result; a value may differ by one bf16 step
+        # only where the float32 rounding of W - s eta v sits on a bf16 tie
+        assert np.mean(got0 != exp0) < 1e-3 and np.max(np.abs(got0 - exp0) / (np.abs(exp0) + 1e-30)) <= 2 ** -7
+        assert np.mean(got1 != exp1) < 1e-3
+    st.destroy()
+
+
+@pytest.mark.parametrize("k,N", [(0, 3), (1, 3), (2, 3), (1, 4), (3, 4)])
+def test_closed_form_through_abi_is_bitwise(k, N):
+    """Dyadic constant-gradient case: after t updates W_t = W0 - t eta g exactly,
+    v stays g, and the predicted slots hold W_{t+s_f} and W_{t+s_b} exactly."""
+    from paper_1809_02839_amd import native
+    from paper_1809_02839_amd.pipeline import Pipeline
+    batch, fin, fout = 8, 16, 8
+    spec = synth.StageSpec("fc", "fp32", "none", k, N, batch, 1, (fin, fout, fout), 2.0 ** -7, 0.875)
+    rng = np.random.default_rng(7)
+    X = (rng.integers(-1, 2, size=(batch, fin)) * 2.0 ** -3).astype(np.float32)
+    dY = (rng.integers(-1, 2, size=(batch, fout)) * 2.0 ** -5).astype(np.float32)
+    W0 = np.concatenate([rng.integers(-64, 65, size=fout * fin) * 2.0 ** -12, np.full(fout, 4.0)]).astype(np.float32)
+    g = np.concatenate([(dY.T.astype(np.float64) @ X).reshape(-1), dY.sum(axis=0)]).astype(np.float32)
+    pipe = Pipeline([spec], [W0], v0s=[g])
+    eta = np.float32(spec.lr)
+    sf, sb = method.version_difference(k, N, True), method.version_difference(k, N, False)
+    seen = []
+
+    def cb(kk, u, st):
+        W, v = st.get_state()
+        assert np.array_equal(v, g)
+        assert np.array_equal(W, (W0.astype(np.float64) - u * float(eta) * g).astype(np.float32))
+        for slot, s in ((0, sf), (1, sb)):
+            assert np.array_equal(st.get_predicted(slot),
+                                  (W0.astype(np.float64) - (u + s) * float(eta) * g).astype(np.float32))
+        seen.append(u)
+
+    pipe.run(10, lambda sp, m: (X, dY, None), on_update=cb)
+    assert seen == list(range(1, 11))
+    pipe.destroy()

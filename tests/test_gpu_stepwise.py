@@ -1,0 +1,36 @@
+"""GPU stepwise parity: every forward, backward and update of the HIP path
+against the oracle's recomputation of the same task from the GPU's state, for
+every stage kind at reduced sizes (20 mini-batches, several GEMM tiles and
+ragged tails) and at the full benchmark sizes (enough mini-batches to reach a
+forward that uses a non-trivial prediction; bf16 gradient quantities there
+are held to the accuracy of the oracle's own bf16 emulation, see
+stepwise.run_stepwise)."""
+import pytest
+
+import synth
+from stepwise import run_stepwise
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.mark.parametrize("name", ["mlp3_small", "vgg_conv_small", "resnet_bottleneck_small",
+                                  "transformer_enc_small", "reslstm_small"])
+def test_stepwise_small(name):
+    wl = synth.ALL_WORKLOADS[name]
+    print(f"[stepwise] {name}", flush=True)
+    worst = run_stepwise(wl, wl.steps, torch)
+    print(f"[stepwise] {name}: {worst.report()}", flush=True)
+
+
+# steps: the stage's N - k warm-up forwards, one backward + update, then a
+# forward against a prediction from a non-zero smoothed gradient
+FULL = {"mlp3": 20, "vgg_conv": 4, "resnet_bottleneck": 3, "transformer_enc": 4, "reslstm": 2}
+
+
+@pytest.mark.parametrize("name", list(FULL))
+def test_stepwise_full_size(name):
+    wl = synth.WORKLOADS[name]
+    print(f"[stepwise-full] {name} steps={FULL[name]}", flush=True)
+    worst = run_stepwise(wl, FULL[name], torch, derived=wl.stages[0].dtype == "bf16")
+    print(f"[stepwise-full] {name}: {worst.report()}", flush=True)
