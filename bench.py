@@ -1,0 +1,242 @@
+"""Benchmark of one SpecTrain pipeline stage's steady-state step on one MI355X.
+
+A step is one pass of the whole stage path over one mini-batch: the backward
+of the oldest mini-batch in flight (data and weight gradients against the
+backward-predicted weights), the fused momentum update that re-predicts both
+weight slots (Eq. 1, Eq. 4), and the forward of the next mini-batch (against
+the forward-predicted weights, Eq. 5 difference). The stage keeps N - k
+mini-batches in flight, as in the one-forward-one-backward schedule.
+
+Default workload: the VGG-16-style 3x3-conv stage (4 conv layers,
+256->512->512->512->512 channels, 8x8 maps, batch 128, bf16 operands with
+float32 master weights, stage 2 of 4). Inputs are synthetic (seeded normal
+draws, already resident in HBM when the timed region starts; a ring of eight
+mini-batches whose second half repeats the first with negated upstream
+gradients, so the weights stay bounded over hundreds of steps).
+
+Output: one JSON line on stdout. `value` is samples per second; `roofline`
+describes the kernel family with the largest share of the step time, measured
+in a separate pass with HIP events around each launch on the stage's stream;
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0    # dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3     # dense fp32 MFMA
+PEAK_HBM_GBPS = 8000.0
+METRIC = "stage samples/sec (fwd+bwd+predict+update); MFMA util %; predict/update GB/s"
+
+DESCRIPTIONS = {
+    "vgg_conv": "VGG-16-style conv stage: 4x conv3x3 256->512->512->512->512, 8x8 maps, NHWC, ReLU",
+    "resnet_bottleneck": "ResNet-152-style stage: 8 bottlenecks 1024->256->256->1024, 14x14 maps, identity skip",
+    "transformer_enc": "Transformer encoder stage: 3 post-LN layers, d=512, 8 heads, FFN 2048, seq 128",
+    "reslstm": "Residual LSTM stage: 2 layers, input=hidden=1024, T=35, vocab-10000 softmax-CE head",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class StageLoop:
+    """Steady-state driver of one stage through the C ABI with a device ring of inputs."""
+
+    def __init__(self, spec, torch, native, stream, ring=8):
+        import numpy as np
+        import synth
+        self.torch, self.spec, self.stream = torch, spec, stream
+        dev = torch.device("cuda")
+        dt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
+        self.st = native.Stage(native.desc_from_spec(spec), synth.initial_params(spec), stream)
+        k, N = spec.stage_index, spec.num_stages
+        self.sf, self.sb = native.version_difference(k, N, True), native.version_difference(k, N, False)
+        self.depth = N - k
+        self.ring = ring
+        with torch.cuda.stream(stream):
+            self.st.predict(self.sf, 0)
+            self.st.predict(self.sb, 1)
+            # Antithetic ring: entries h and h + ring/2 share x, and their upstream
+            # gradients have opposite signs, so hundreds of steps over the ring
+            # do not drive the weights of the (unbounded) synthetic objective
+            # systematically in one direction.
+            half = ring // 2
+            self.x = [torch.from_numpy(synth.stage_input(spec, m % half)).to(dev).to(dt) for m in range(ring)]
+            if spec.head == "ce":
+                self.lab = [torch.from_numpy(synth.labels(spec, m % half)).to(dev) for m in range(ring)]
+                self.loss = [torch.zeros(1, device=dev) for _ in range(ring)]
+                self.dy = None
+                self.y = None
+            else:
+                self.dy = [torch.from_numpy(synth.upstream_grad(spec, m % half) * (1 if m < half else -1)).to(dev).to(dt)
+                           for m in range(ring)]
+                self.y = [torch.empty(spec.output_shape(), device=dev, dtype=dt) for _ in range(self.depth + 1)]
+            self.dx = torch.empty(spec.input_shape(), device=dev, dtype=dt)
+        self.next_b = 0
+        for m in range(self.depth):
+            self._forward(m)
+        stream.synchronize()
+        _ = np
+
+    def _forward(self, m):
+        r = m % self.ring
+        if self.spec.head == "ce":
+            self.st.forward(m, self.x[r], None, self.lab[r], self.loss[r])
+        else:
+            self.st.forward(m, self.x[r], self.y[m % (self.depth + 1)])
+
+    def steps(self, n):
+        for _ in range(n):
+            m = self.next_b
+            self.st.backward(m, None if self.dy is None else self.dy[m % self.ring], self.dx)
+            self.st.update(self.sf, self.sb)
+            self._forward(m + self.depth)
+            self.next_b += 1
+
+
+def cpu_baseline(spec, n_steps):
+    """The oracle as it stands, timed on the host: n_steps (forward, backward,
+    update) of the same stage at full size."""
+    import numpy as np
+    import synth
+    from oracle import method, stages
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    k, N = spec.stage_index, spec.num_stages
+    lr, gamma = float(np.float32(spec.lr)), float(np.float32(spec.momentum))
+    W = synth.initial_params(spec).astype(np.float64)
+    v = np.zeros_like(W)
+    rnd = stages.weight_rounder(spec)
+    sf, sb = method.version_difference(k, N, True), method.version_difference(k, N, False)
+    t0 = time.perf_counter()
+    for m in range(n_steps):
+        x = synth.stage_input(spec, m)
+        dy = synth.upstream_grad(spec, m) if spec.head == "none" else None
+        lab = synth.labels(spec, m) if spec.head == "ce" else None
+        _, _, st = stages.forward(spec, stages.unpack(spec, rnd(method.predict(W, v, sf, lr))), x, lab)
+        _, g = stages.backward(spec, stages.unpack(spec, rnd(method.predict(W, v, sb, lr))), st, dy)
+        W, v = method.momentum_sgd_step(W, v, stages.pack(spec, g), lr, gamma)
+    dt = time.perf_counter() - t0
+    per_step = dt / n_steps
+    return {"value": spec.batch / per_step, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n_steps} full-size steps (forward, backward, update) of the same stage, "
+                      f"float64 NumPy, {per_step:.2f} s per step"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default="vgg_conv", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--profile-steps", type=int, default=20)
+    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs one pipeline stage on one GPU; --gpus above 1 is not supported "
+              "(the multi-GPU pipeline is simulated in order on one device)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    from paper_1809_02839_amd import native
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    spec = synth.WORKLOADS[args.workload].stages[0]
+    stream = torch.cuda.Stream()
+    loop = StageLoop(spec, torch, native, stream)
+
+    loop.steps(args.warmup)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    loop.steps(args.steps)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / args.steps
+    value = spec.batch / (ms_step / 1e3)
+    log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {value:.0f} samples/s")
+
+    # per-kernel pass (events around every launch, separate from the timed region)
+    loop.st.profile(True)
+    loop.steps(args.profile_steps)
+    prof = loop.st.profile_read()
+    loop.st.profile(False)
+    torch.cuda.synchronize()
+    fam_ms = {k: v["ms_total"] / args.profile_steps for k, v in prof.items()}
+    for k, v in prof.items():
+        extra = ""
+        if v["flops_total"]:
+            extra = f"  {v['flops_total'] / v['ms_total'] / 1e9:.1f} TFLOP/s"
+        elif v["bytes_total"]:
+            extra = f"  {v['bytes_total'] / v['ms_total'] / 1e6:.0f} GB/s"
+        log(f"[bench]   {k:22s} {v['launches'] / args.profile_steps:5.1f}/step "
+            f"{v['ms_total'] / v['launches'] * 1e3:9.1f} us/launch {fam_ms[k] * 1e3:9.1f} us/step{extra}")
+    dom = max(prof, key=lambda k: prof[k]["ms_total"])
+    d = prof[dom]
+    peak_mfma = PEAK_BF16_TFLOPS if spec.dtype == "bf16" else PEAK_FP32_TFLOPS
+    if d["flops_total"] > 0:
+        achieved = d["flops_total"] / (d["ms_total"] / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak_mfma, "unit": "TFLOP/s",
+                "frac": round(achieved / peak_mfma, 4), "traffic": None}
+    else:
+        achieved = d["bytes_total"] / (d["ms_total"] / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None}
+    roof["kernel"] = dom
+    roof["launches_per_step"] = d["launches"] / args.profile_steps
+    roof["us_per_launch"] = round(d["ms_total"] / d["launches"] * 1e3, 2)
+    gemm_flops = sum(v["flops_total"] for v in prof.values())
+    gemm_ms = sum(v["ms_total"] for k, v in prof.items() if v["flops_total"] > 0)
+    upd = prof.get("fused_update")
+    upd_gbps = upd["bytes_total"] / (upd["ms_total"] / 1e3) / 1e9 if upd else None
+
+    cpu = None
+    if not args.no_cpu:
+        log(f"[bench] timing the CPU oracle on {args.cpu_steps} steps ...")
+        cpu = cpu_baseline(spec, args.cpu_steps)
+        log(f"[bench] oracle: {cpu['value']:.2f} samples/s on {cpu['cores']} threads")
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": spec.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {DESCRIPTIONS[args.workload]}", "batch": spec.batch,
+                   "stage_index": spec.stage_index, "num_stages": spec.num_stages,
+                   "s_forward": loop.sf, "s_backward": loop.sb, "params": synth.num_params(spec)},
+        "mfma_util_pct": round(100.0 * gemm_flops / (gemm_ms / 1e3) / 1e12 / peak_mfma, 2) if gemm_ms else None,
+        "mfma_util_pct_of_step": round(100.0 * gemm_flops / args.profile_steps / (ms_step / 1e3) / 1e12 / peak_mfma, 2),
+        "predict_update_GBps": round(upd_gbps, 1) if upd_gbps else None,
+        "predict_update_frac_hbm": round(upd_gbps / PEAK_HBM_GBPS, 4) if upd_gbps else None,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    loop.st.destroy()
+
+
+if __name__ == "__main__":
+    main()

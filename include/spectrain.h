@@ -156,6 +156,30 @@ int spectrain_stage_set_state(spectrain_stage_t st, const float* W_host, const f
  * Synchronises the stream. */
 int spectrain_stage_get_predicted(spectrain_stage_t st, int32_t slot, float* What_host);
 
+/* Per-kernel launch statistics of a stage, collected between
+ * spectrain_stage_profile(st, 1) and a read. Durations come from HIP events
+ * recorded around every launch on the stage's stream (which serialises the
+ * launches: use a separate pass, not the timed one). flops and bytes are the
+ * algorithmic work of the launches: 2*M*N*K per GEMM (3x3 convolutions count
+ * all 9 taps), and for the fused update 12 bytes read plus 8 + 2*sizeof(operand)
+ * written per parameter. */
+typedef struct {
+  char name[48];        /* kernel family, e.g. "conv3x3_fwd", "fused_update" */
+  int64_t launches;
+  double ms_total;      /* summed event-to-event duration */
+  double flops_total;   /* algorithmic floating-point operations (0 if not a contraction) */
+  double bytes_total;   /* algorithmic HBM bytes (0 if not counted) */
+} spectrain_kernel_stat;
+
+/* enable != 0: clear the statistics and time every following launch;
+ * enable == 0: stop timing (statistics are kept for reading). */
+int spectrain_stage_profile(spectrain_stage_t st, int32_t enable);
+
+/* Copy up to capacity kernel families into out (in first-launch order) and
+ * store the number of families in *count. Synchronises the stream. */
+int spectrain_stage_profile_read(spectrain_stage_t st, spectrain_kernel_stat* out, int32_t capacity,
+                                 int32_t* count);
+
 /* Release every device buffer of the stage. Synchronises the stream.
  * Passing NULL returns EINVAL. */
 int spectrain_stage_destroy(spectrain_stage_t st);

@@ -104,6 +104,15 @@ int spectrain_stage_get_predicted(spectrain_stage_t st, int32_t slot, float* Wha
   return guarded(st, [&](spx::Stage& x) { x.get_predicted(slot, What_host); }, false);
 }
 
+int spectrain_stage_profile(spectrain_stage_t st, int32_t enable) {
+  return guarded(st, [&](spx::Stage& x) { x.profile(enable != 0); }, false);
+}
+
+int spectrain_stage_profile_read(spectrain_stage_t st, spectrain_kernel_stat* out, int32_t capacity, int32_t* count) {
+  if (!count || (capacity > 0 && !out)) return set_error(SPECTRAIN_EINVAL, "out and count must not be NULL");
+  return guarded(st, [&](spx::Stage& x) { *count = x.profile_read(out, capacity); }, false);
+}
+
 int spectrain_stage_destroy(spectrain_stage_t st) {
   if (!st) return set_error(SPECTRAIN_EINVAL, "stage handle is NULL");
   delete st->impl;

@@ -148,8 +148,61 @@ const void* Stage::wf(int i) const { return static_cast<const char*>(what_[0]) +
 const void* Stage::wb(int i) const { return static_cast<const char*>(what_[1]) + tensors_[i].off * esz_; }
 
 void Stage::gemm(const GemmDesc& d) {
-  hip_check(dt_ ? gemm_bf16(d, s_) : gemm_f32(d, s_), "gemm launch");
+  const char* name = "gemm";
+  const int ma = d.A.mode, mb = d.B.mode;
+  if (ma == OP_K_CONV_FWD) name = "conv3x3_fwd";
+  else if (ma == OP_K_CONV_DGRAD) name = "conv3x3_dgrad";
+  else if (mb == OP_R_CONV_WGRAD) name = "conv3x3_wgrad";
+  else if (d.batch > 1) name = dt_ ? "gemm_bf16_batched" : "gemm_f32_batched";
+  else if (ma == OP_K_PLAIN && mb == OP_K_PLAIN) name = dt_ ? "gemm_bf16_xwT" : "gemm_f32_xwT";
+  else if (ma == OP_K_PLAIN && mb == OP_R_PLAIN) name = dt_ ? "gemm_bf16_dyW" : "gemm_f32_dyW";
+  else if (ma == OP_R_PLAIN && mb == OP_R_PLAIN) name = dt_ ? "gemm_bf16_dyTx" : "gemm_f32_dyTx";
+  const double flops = 2.0 * d.M * d.N * static_cast<double>(d.K) * d.batch;
+  LAUNCH(name, flops, 0, dt_ ? gemm_bf16(d, s_) : gemm_f32(d, s_));
 }
+
+// ------------------------------------------------------------ profiling ----
+hipEvent_t Stage::prof_event() {
+  if (prof_used_ == prof_pool_.size()) {
+    hipEvent_t e;
+    hip_check(hipEventCreate(&e), "hipEventCreate");
+    prof_pool_.push_back(e);
+  }
+  return prof_pool_[prof_used_++];
+}
+
+void Stage::prof_collect() {
+  if (prof_recs_.empty()) return;
+  sync();
+  for (const ProfRec& r : prof_recs_) {
+    float ms = 0.0f;
+    hip_check(hipEventElapsedTime(&ms, r.a, r.b), "hipEventElapsedTime");
+    spectrain_kernel_stat& k = prof_stats_[r.family];
+    k.launches += 1;
+    k.ms_total += ms;
+    k.flops_total += r.flops;
+    k.bytes_total += r.bytes;
+  }
+  prof_recs_.clear();
+  prof_used_ = 0;
+}
+
+void Stage::profile(bool enable) {
+  if (enable) {
+    prof_collect();
+    prof_stats_.clear();
+    prof_index_.clear();
+  }
+  prof_on_ = enable;
+}
+
+int Stage::profile_read(spectrain_kernel_stat* out, int capacity) {
+  prof_collect();
+  const int n = static_cast<int>(prof_stats_.size());
+  for (int i = 0; i < n && i < capacity; ++i) out[i] = prof_stats_[i];
+  return n;
+}
+
 
 // Sizes of the stash slot buffers and workspace buffers of each kind.
 void Stage::plan_buffers() {
@@ -323,6 +376,7 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
 
 Stage::~Stage() {
   (void)hipStreamSynchronize(s_);
+  for (hipEvent_t e : prof_pool_) (void)hipEventDestroy(e);
   if (flag_host_) (void)hipHostFree(flag_host_);
 }
 
@@ -389,13 +443,14 @@ void Stage::get_predicted(int slot, float* out) {
 void Stage::predict(int s, int slot) {
   if (s < 0) fail("version difference must be >= 0");
   if (slot < 0 || slot > 1) fail("slot must be 0 or 1");
-  hip_check(predict_slot(W_, v_, what_[slot], dt_, n_arena_, d_.lr, s, s_), "predict launch");
+  LAUNCH("predict", 0, static_cast<double>(n_params_) * (8 + esz_), predict_slot(W_, v_, what_[slot], dt_, n_arena_, d_.lr, s, s_));
 }
 
 void Stage::update(int s_f, int s_b) {
   if (!g_pending_) throw StageError(SPECTRAIN_ESTATE, "update without a gradient from a backward pass");
-  hip_check(fused_update(W_, v_, g_, what_[0], what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_dev_, s_),
-            "update launch");
+  const double bytes = static_cast<double>(n_params_) * (12 + 8 + (s_f >= 0) * esz_ + (s_b >= 0) * esz_);
+  LAUNCH("fused_update", 0, bytes,
+         fused_update(W_, v_, g_, what_[0], what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_dev_, s_));
   g_pending_ = false;
 }
 
@@ -465,8 +520,7 @@ void Stage::fwd_fc(int slot, const void* x, void* y, const int32_t* labels, floa
     a = out;
   }
   if (ce)
-    hip_check(softmax_ce(ws<float>(0), labels, B, d_.dims[1], stash<void>(slot, L - 1), dt_, loss, ws<float>(3), s_),
-              "softmax_ce");
+    LAUNCH("softmax_ce", 0, 0, softmax_ce(ws<float>(0), labels, B, d_.dims[1], stash<void>(slot, L - 1), dt_, loss, ws<float>(3), s_));
 }
 
 void Stage::bwd_fc(int slot, const void* dy, void* dx) {
@@ -478,7 +532,7 @@ void Stage::bwd_fc(int slot, const void* dy, void* dx) {
   if (d_.head == SPECTRAIN_HEAD_CE) {
     dz = stash<void>(slot, L - 1);
   } else {
-    hip_check(mask_relu_grad(dy, sl.y, ws<void>(1), static_cast<long>(B) * d_.dims[1], dt_, s_), "mask");
+    LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(1), static_cast<long>(B) * d_.dims[1], dt_, s_));
     dz = ws<void>(1);
   }
   int pp = 2;
@@ -487,7 +541,7 @@ void Stage::bwd_fc(int slot, const void* dy, void* dx) {
     GemmDesc gw = gd(fout, fin, B, opR(dz, fout), opR(act(l), fin), fin);
     gw.epi.out_f32 = grad(2 * l);
     gemm(gw);
-    hip_check(column_sum(dz, dt_, B, fout, fout, grad(2 * l + 1), 0, ws<float>(4), s_), "bias grad");
+    LAUNCH("bias_grad", 0, 0, column_sum(dz, dt_, B, fout, fout, grad(2 * l + 1), 0, ws<float>(4), s_));
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
     GemmDesc gx = gd(B, fin, fout, opK(dz, fout), opR(wb(2 * l), fin), fin);
@@ -521,7 +575,7 @@ void Stage::bwd_conv(int slot, const void* dy, void* dx) {
   const int P = B * H * W;
   const Slot& sl = slots_[slot];
   auto act = [&](int l) -> const void* { return l == 0 ? sl.x : (l == L ? sl.y : stash<void>(slot, l - 1)); };
-  hip_check(mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * Cout, 1, s_), "mask");
+  LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * Cout, 1, s_));
   const void* dz = ws<void>(0);
   int pp = 1;
   for (int l = L - 1; l >= 0; --l) {
@@ -574,7 +628,7 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
   const Slot& sl = slots_[slot];
   auto xin = [&](int l) -> const void* { return l == 0 ? sl.x : stash<void>(slot, 3 * (l - 1) + 2); };
   // dr: gradient at the block's pre-ReLU output (after the output mask)
-  hip_check(mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * C, 1, s_), "mask");
+  LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * C, 1, s_));
   int cur = 0;
   bf16_t* dt2 = ws<bf16_t>(2);
   bf16_t* dt1 = ws<bf16_t>(3);
@@ -648,7 +702,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y) {
     sc.epi.alpha = scale;
     sc.epi.out_f32 = ws<float>(0);
     gemm(sc);
-    hip_check(softmax_rows(ws<float>(0), B * Hh * S, S, P, Pb, s_), "softmax");
+    LAUNCH("softmax", 0, 0, softmax_rows(ws<float>(0), B * Hh * S, S, P, Pb, s_));
     // ctx[b, :, h] = P V
     Operand pa = opK(Pb, S), vb = opR(qkv + 2 * d, 3 * d);
     pa.bs1 = static_cast<long>(Hh) * S * S;
@@ -667,9 +721,8 @@ void Stage::fwd_tfm(int slot, const void* x, void* y) {
     go.epi.res_bf16 = static_cast<const bf16_t*>(a);
     go.epi.out_bf16 = r1;
     gemm(go);
-    hip_check(layernorm_fwd(r1, static_cast<const bf16_t*>(wf(p + 4)), static_cast<const bf16_t*>(wf(p + 5)), T, d,
-                            LN_EPS, h, stash<float>(slot, q + 5), stash<float>(slot, q + 6), s_),
-              "layernorm");
+    LAUNCH("layernorm", 0, 0, layernorm_fwd(r1, static_cast<const bf16_t*>(wf(p + 4)), static_cast<const bf16_t*>(wf(p + 5)), T, d,
+                            LN_EPS, h, stash<float>(slot, q + 5), stash<float>(slot, q + 6), s_));
     GemmDesc g1 = gd(T, F, d, opK(h, d), opK(wf(p + 6), d), F);
     g1.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 7));
     g1.epi.relu = 1;
@@ -680,10 +733,9 @@ void Stage::fwd_tfm(int slot, const void* x, void* y) {
     g2.epi.res_bf16 = h;
     g2.epi.out_bf16 = r2;
     gemm(g2);
-    hip_check(layernorm_fwd(r2, static_cast<const bf16_t*>(wf(p + 10)), static_cast<const bf16_t*>(wf(p + 11)), T, d,
+    LAUNCH("layernorm", 0, 0, layernorm_fwd(r2, static_cast<const bf16_t*>(wf(p + 10)), static_cast<const bf16_t*>(wf(p + 11)), T, d,
                             LN_EPS, static_cast<bf16_t*>(out), stash<float>(slot, q + 10), stash<float>(slot, q + 11),
-                            s_),
-              "layernorm");
+                            s_));
     a = out;
   }
 }
@@ -716,13 +768,12 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     bf16_t* dctx = ws<bf16_t>(8);
     bf16_t* dqkv = ws<bf16_t>(9);
 
-    hip_check(layernorm_bwd(static_cast<const bf16_t*>(gy), r2, stash<float>(slot, q + 10), stash<float>(slot, q + 11),
-                            static_cast<const bf16_t*>(wb(p + 10)), T, d, dr2, grad(p + 10), grad(p + 11), part, s_),
-              "layernorm bwd");
+    LAUNCH("layernorm_bwd", 0, 0, layernorm_bwd(static_cast<const bf16_t*>(gy), r2, stash<float>(slot, q + 10), stash<float>(slot, q + 11),
+                            static_cast<const bf16_t*>(wb(p + 10)), T, d, dr2, grad(p + 10), grad(p + 11), part, s_));
     GemmDesc w2 = gd(d, F, T, opR(dr2, d), opR(f1, F), F);
     w2.epi.out_f32 = grad(p + 8);
     gemm(w2);
-    hip_check(column_sum(dr2, 1, T, d, d, grad(p + 9), 0, part, s_), "bias grad");
+    LAUNCH("bias_grad", 0, 0, column_sum(dr2, 1, T, d, d, grad(p + 9), 0, part, s_));
     GemmDesc x2 = gd(T, F, d, opK(dr2, d), opR(wb(p + 8), F), F);
     x2.epi.mask = f1;
     x2.epi.out_bf16 = df1;
@@ -730,18 +781,17 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     GemmDesc w1 = gd(F, d, T, opR(df1, F), opR(h, d), d);
     w1.epi.out_f32 = grad(p + 6);
     gemm(w1);
-    hip_check(column_sum(df1, 1, T, F, F, grad(p + 7), 0, part, s_), "bias grad");
+    LAUNCH("bias_grad", 0, 0, column_sum(df1, 1, T, F, F, grad(p + 7), 0, part, s_));
     GemmDesc x1 = gd(T, d, F, opK(df1, F), opR(wb(p + 6), d), d);
     x1.epi.res_bf16 = dr2;
     x1.epi.out_bf16 = dhh;
     gemm(x1);
-    hip_check(layernorm_bwd(dhh, r1, stash<float>(slot, q + 5), stash<float>(slot, q + 6),
-                            static_cast<const bf16_t*>(wb(p + 4)), T, d, dr1, grad(p + 4), grad(p + 5), part, s_),
-              "layernorm bwd");
+    LAUNCH("layernorm_bwd", 0, 0, layernorm_bwd(dhh, r1, stash<float>(slot, q + 5), stash<float>(slot, q + 6),
+                            static_cast<const bf16_t*>(wb(p + 4)), T, d, dr1, grad(p + 4), grad(p + 5), part, s_));
     GemmDesc wo = gd(d, d, T, opR(dr1, d), opR(ctx, d), d);
     wo.epi.out_f32 = grad(p + 2);
     gemm(wo);
-    hip_check(column_sum(dr1, 1, T, d, d, grad(p + 3), 0, part, s_), "bias grad");
+    LAUNCH("bias_grad", 0, 0, column_sum(dr1, 1, T, d, d, grad(p + 3), 0, part, s_));
     GemmDesc xo = gd(T, d, d, opK(dr1, d), opR(wb(p + 2), d), d);
     xo.epi.out_bf16 = dctx;
     gemm(xo);
@@ -777,7 +827,7 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
       g.epi.out_f32 = ws<float>(0);
       gemm(g);
     }
-    hip_check(softmax_bwd(P, ws<float>(0), B * Hh * S, S, ws<bf16_t>(1), s_), "softmax bwd");
+    LAUNCH("softmax_bwd", 0, 0, softmax_bwd(P, ws<float>(0), B * Hh * S, S, ws<bf16_t>(1), s_));
     {  // dQ = dS K * scale
       Operand A = opK(ws<bf16_t>(1), S), Bk = opR(qkv + d, 3 * d);
       A.bs1 = sHSS;
@@ -811,7 +861,7 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     GemmDesc wq = gd(3 * d, d, T, opR(dqkv, 3 * d), opR(a, d), d);
     wq.epi.out_f32 = grad(p);
     gemm(wq);
-    hip_check(column_sum(dqkv, 1, T, 3 * d, 3 * d, grad(p + 1), 0, part, s_), "bias grad");
+    LAUNCH("bias_grad", 0, 0, column_sum(dqkv, 1, T, 3 * d, 3 * d, grad(p + 1), 0, part, s_));
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
     GemmDesc xq = gd(T, d, 3 * d, opK(dqkv, 3 * d), opR(wb(p), d), d);
@@ -853,12 +903,11 @@ void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, fl
         gh.epi.out_f32 = zt;
         gemm(gh);
       }
-      hip_check(lstm_cell_fwd(zt, t > 0 ? c + static_cast<long>(t - 1) * B * H : nullptr, B, H,
+      LAUNCH("lstm_cell", 0, 0, lstm_cell_fwd(zt, t > 0 ? c + static_cast<long>(t - 1) * B * H : nullptr, B, H,
                               gates + static_cast<long>(t) * B * 4 * H, c + static_cast<long>(t) * B * H,
-                              hs + static_cast<long>(t) * B * H, s_),
-                "lstm cell");
+                              hs + static_cast<long>(t) * B * H, s_));
     }
-    hip_check(add_bf16(static_cast<const bf16_t*>(u), hs, static_cast<bf16_t*>(out), TB * H, s_), "residual");
+    LAUNCH("residual", 0, 0, add_bf16(static_cast<const bf16_t*>(u), hs, static_cast<bf16_t*>(out), TB * H, s_));
     u = out;
   }
   if (ce) {
@@ -866,9 +915,8 @@ void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, fl
     gv.epi.bias_bf16 = static_cast<const bf16_t*>(wf(3 * L + 1));
     gv.epi.out_f32 = ws<float>(1);
     gemm(gv);
-    hip_check(softmax_ce(ws<float>(1), labels, static_cast<int>(TB), V, stash<void>(slot, 4 * L), 1, loss, ws<float>(7),
-                         s_),
-              "softmax_ce");
+    LAUNCH("softmax_ce", 0, 0, softmax_ce(ws<float>(1), labels, static_cast<int>(TB), V, stash<void>(slot, 4 * L), 1, loss, ws<float>(7),
+                         s_));
   }
 }
 
@@ -886,7 +934,7 @@ void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
     GemmDesc gw = gd(V, H, static_cast<int>(TB), opR(dl, V), opR(uL, H), H);
     gw.epi.out_f32 = grad(3 * L);
     gemm(gw);
-    hip_check(column_sum(dl, 1, TB, V, V, grad(3 * L + 1), 0, part, s_), "bias grad");
+    LAUNCH("bias_grad", 0, 0, column_sum(dl, 1, TB, V, V, grad(3 * L + 1), 0, part, s_));
     GemmDesc gx = gd(static_cast<int>(TB), H, V, opK(dl, V), opR(wb(3 * L), H), H);
     gx.epi.out_bf16 = ws<bf16_t>(pp);
     gemm(gx);
@@ -903,12 +951,11 @@ void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
     const float* gates = stash<float>(slot, q);
     const float* c = stash<float>(slot, q + 1);
     const bf16_t* hs = stash<bf16_t>(slot, q + 2);
-    hip_check(fill_f32(dc, 0.0f, static_cast<long>(B) * H, s_), "clear dc");
+    LAUNCH("clear_dc", 0, 0, fill_f32(dc, 0.0f, static_cast<long>(B) * H, s_));
     for (int t = T - 1; t >= 0; --t) {
       const long o = static_cast<long>(t) * B;
-      hip_check(lstm_cell_bwd(static_cast<const bf16_t*>(du) + o * H, t < T - 1 ? dh_rec : nullptr, gates + o * 4 * H,
-                              c + o * H, t > 0 ? c + (o - B) * H : nullptr, B, H, dc, dz + o * 4 * H, s_),
-                "lstm cell bwd");
+      LAUNCH("lstm_cell_bwd", 0, 0, lstm_cell_bwd(static_cast<const bf16_t*>(du) + o * H, t < T - 1 ? dh_rec : nullptr, gates + o * 4 * H,
+                              c + o * H, t > 0 ? c + (o - B) * H : nullptr, B, H, dc, dz + o * 4 * H, s_));
       if (t > 0) {
         GemmDesc gh = gd(B, H, 4 * H, opK(dz + o * 4 * H, 4 * H), opR(wb(p + 1), H), H);
         gh.epi.out_f32 = dh_rec;
@@ -923,9 +970,9 @@ void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
       wh.epi.out_f32 = grad(p + 1);
       gemm(wh);
     } else {
-      hip_check(fill_f32(grad(p + 1), 0.0f, 4L * H * H, s_), "clear grad");
+      LAUNCH("clear_grad", 0, 0, fill_f32(grad(p + 1), 0.0f, 4L * H * H, s_));
     }
-    hip_check(column_sum(dz, 1, TB, 4 * H, 4 * H, grad(p + 2), 0, part, s_), "bias grad");
+    LAUNCH("bias_grad", 0, 0, column_sum(dz, 1, TB, 4 * H, 4 * H, grad(p + 2), 0, part, s_));
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
     GemmDesc gxx = gd(static_cast<int>(TB), in, 4 * H, opK(dz, 4 * H), opR(wb(p), in), in);

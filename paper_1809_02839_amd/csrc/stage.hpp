@@ -3,12 +3,16 @@
 #pragma once
 
 #include <cstdint>
+#include <cstdio>
+#include <map>
 #include <stdexcept>
 #include <string>
 #include <vector>
 
 #include "../../include/spectrain.h"
 #include "kernels.hpp"
+
+#define LAUNCH(family, flops, bytes, expr) timed(family, flops, bytes, [&]() { return (expr); })
 
 namespace spx {
 
@@ -60,6 +64,8 @@ class Stage {
   void get_predicted(int slot, float* out);
   bool nonfinite() const { return *reinterpret_cast<volatile int*>(flag_host_) != 0; }
   void sync();
+  void profile(bool enable);
+  int profile_read(spectrain_kernel_stat* out, int capacity);
 
  private:
   struct Slot {
@@ -81,6 +87,34 @@ class Stage {
   template <typename T>
   T* ws(int buf) const { return ws_block_.at<T>(ws_off_[buf]); }
   void gemm(const GemmDesc& d);
+
+  // Launch wrapper: checks the launch status and, while profiling, brackets
+  // the launch with events on the stage's stream.
+  template <typename F>
+  void timed(const char* family, double flops, double bytes, F&& launch) {
+    if (!prof_on_) {
+      hip_check(launch(), family);
+      return;
+    }
+    hipEvent_t a = prof_event(), b = prof_event();
+    hip_check(hipEventRecord(a, s_), "hipEventRecord");
+    hip_check(launch(), family);
+    hip_check(hipEventRecord(b, s_), "hipEventRecord");
+    auto it = prof_index_.find(family);
+    int fam;
+    if (it == prof_index_.end()) {
+      fam = static_cast<int>(prof_stats_.size());
+      prof_index_[family] = fam;
+      spectrain_kernel_stat k{};
+      std::snprintf(k.name, sizeof(k.name), "%s", family);
+      prof_stats_.push_back(k);
+    } else {
+      fam = it->second;
+    }
+    prof_recs_.push_back({fam, a, b, flops, bytes});
+  }
+  hipEvent_t prof_event();
+  void prof_collect();
 
   // ---- per kind
   void fwd_fc(int slot, const void* x, void* y, const int32_t* labels, float* loss);
@@ -116,6 +150,18 @@ class Stage {
   DeviceBlock ws_block_;
   std::vector<size_t> ws_off_;
   bool g_pending_ = false;
+
+  struct ProfRec {
+    int family;
+    hipEvent_t a, b;
+    double flops, bytes;
+  };
+  bool prof_on_ = false;
+  std::vector<hipEvent_t> prof_pool_;
+  size_t prof_used_ = 0;
+  std::vector<ProfRec> prof_recs_;
+  std::vector<spectrain_kernel_stat> prof_stats_;
+  std::map<std::string, int> prof_index_;
 };
 
 }  // namespace spx

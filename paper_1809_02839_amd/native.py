@@ -24,7 +24,8 @@ KIND_BY_NAME = {"fc": KIND_FC, "conv3x3": KIND_CONV3X3, "bottleneck": KIND_BOTTL
 EXPORTED = ("spectrain_version_difference", "spectrain_stage_create", "spectrain_stage_num_params",
             "spectrain_stage_predict", "spectrain_stage_forward", "spectrain_stage_backward",
             "spectrain_stage_update", "spectrain_stage_get_state", "spectrain_stage_set_state",
-            "spectrain_stage_get_predicted", "spectrain_stage_destroy", "spectrain_last_error")
+            "spectrain_stage_get_predicted", "spectrain_stage_profile", "spectrain_stage_profile_read",
+            "spectrain_stage_destroy", "spectrain_last_error")
 
 
 class StageDesc(ctypes.Structure):
@@ -32,6 +33,11 @@ class StageDesc(ctypes.Structure):
                 ("head", ctypes.c_int32), ("stage_index", ctypes.c_int32), ("num_stages", ctypes.c_int32),
                 ("batch", ctypes.c_int32), ("num_layers", ctypes.c_int32), ("dims", ctypes.c_int32 * 8),
                 ("lr", ctypes.c_float), ("momentum", ctypes.c_float)]
+
+
+class KernelStat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int64), ("ms_total", ctypes.c_double),
+                ("flops_total", ctypes.c_double), ("bytes_total", ctypes.c_double)]
 
 
 class SpecTrainError(RuntimeError):
@@ -63,6 +69,9 @@ def lib():
             "spectrain_stage_get_state": (ctypes.c_int, [vp, fp, fp]),
             "spectrain_stage_set_state": (ctypes.c_int, [vp, fp, fp]),
             "spectrain_stage_get_predicted": (ctypes.c_int, [vp, i32, fp]),
+            "spectrain_stage_profile": (ctypes.c_int, [vp, i32]),
+            "spectrain_stage_profile_read": (ctypes.c_int, [vp, ctypes.POINTER(KernelStat), i32,
+                                                            ctypes.POINTER(i32)]),
             "spectrain_stage_destroy": (ctypes.c_int, [vp]),
             "spectrain_last_error": (ctypes.c_char_p, []),
         }
@@ -150,6 +159,19 @@ class Stage:
         out = np.empty(self.n_params, np.float32)
         _check(lib().spectrain_stage_get_predicted(self.h, slot, _fptr(out)))
         return out
+
+    def profile(self, enable: bool):
+        _check(lib().spectrain_stage_profile(self.h, 1 if enable else 0))
+
+    def profile_read(self):
+        """{family: dict(launches, ms_total, flops_total, bytes_total)} in first-launch order."""
+        cap = 64
+        arr = (KernelStat * cap)()
+        n = ctypes.c_int32()
+        _check(lib().spectrain_stage_profile_read(self.h, arr, cap, ctypes.byref(n)))
+        return {arr[i].name.decode(): dict(launches=arr[i].launches, ms_total=arr[i].ms_total,
+                                           flops_total=arr[i].flops_total, bytes_total=arr[i].bytes_total)
+                for i in range(min(n.value, cap))}
 
     def destroy(self):
         if self.h is not None and self.h.value:
