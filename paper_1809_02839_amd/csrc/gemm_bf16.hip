@@ -3,169 +3,41 @@
 // layers, 3x3 convolutions as implicit GEMM (forward, data gradient, filter
 // gradient) and the batched products inside attention.
 //
-// Block tile 128 x 128, K step 32, 256 threads = 4 waves in a 2 x 2 grid, each
-// wave owning a 64 x 64 sub-tile (2 x 2 MFMA tiles of 32 x 32). Both operand
-// tiles are staged in LDS as [row][k] with k contiguous, which is the layout
-// the MFMA operand fetch wants (8 consecutive k per lane, one 16-byte
-// ds_read). Two LDS buffers: the next K step's global loads are issued before
-// the current step's MFMAs and written to the other buffer afterwards.
+// Block tile 128 x 128, K step 64, 256 threads = 4 waves in a 2 x 2 grid, each
+// wave owning a 64 x 64 sub-tile (2 x 2 MFMA tiles of 32 x 32). Operand tiles
+// are staged in LDS as [row][k] with k contiguous (8 consecutive k per lane
+// make one 16-byte MFMA operand read); the 144-byte row pitch puts eight
+// consecutive rows on disjoint banks. Global loads run two K steps ahead of
+// the MFMAs (two register stages, two LDS buffers). All global reads are
+// buffer loads whose resource spans exactly the operand tensor: an offset
+// outside it (zero padding of convolutions, ragged tile edges) reads zero.
+//
+// Split-K: a launch may divide K into `splits` ranges; each writes float32
+// partial tiles to a workspace and an elementwise pass sums the partials in a
+// fixed order and applies the epilogue, so results do not depend on timing.
+#include <algorithm>
+
 #include "kernels.hpp"
 
 namespace spx {
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 32, NT = 256;
-constexpr int PITCH = BK + 8;  // bf16 per LDS row: 80 bytes keeps 16-byte rows on distinct banks
-constexpr int TILE_ELEMS = 128 * PITCH;
+constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
+constexpr int PITCH = BK + 8;            // bf16 elements per LDS row (144 bytes)
+constexpr int TILE_ELEMS = 128 * PITCH;  // one operand tile
+constexpr int BUF_FLAGS = 0x00020000;    // gfx9 raw buffer resource word 3
+constexpr int OOB = 0x7ffffff0;          // byte offset past every resource: the load returns 0
 
-// LDS index of (row, k) inside one operand tile. The 16-byte chunk index is
-// XOR-swizzled with row/8 so that the transposed 4-byte writes of R-mode
-// operands do not all fall on one bank.
-__device__ __forceinline__ int lds_idx(int row, int k) {
-  return row * PITCH + (((k >> 3) ^ (row >> 3)) & 3) * 8 + (k & 7);
-}
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 struct OperandDev {
   const bf16_t* p;
   long ld;
+  long extent;     // elements addressable from p (batch 0)
   int rows;        // extent of the row dimension (M for A, N for B)
   int K;
   int H, W, C, C2;
   FastDiv fdC, fdC2, fdHW, fdW;
-};
-
-__device__ __forceinline__ uint4 zero4() { return make_uint4(0, 0, 0, 0); }
-
-// ---- K-mode: 8 consecutive k of one row ----------------------------------
-template <int MODE>
-struct KLoader {
-  // per-thread, per-vector constant row info
-  int row_ok[2];
-  long row_base[2];   // PLAIN: row * ld; CONV: pixel index
-  int ph[2], pw[2];   // CONV: pixel coordinates
-  int kq[2];
-
-  __device__ void init(const OperandDev& o, int row0, int tid) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      int v = tid + NT * i;
-      int r = row0 + (v >> 2);
-      kq[i] = v & 3;
-      row_ok[i] = r < o.rows;
-      if (MODE == OP_K_PLAIN) {
-        row_base[i] = static_cast<long>(r) * o.ld;
-      } else {
-        row_base[i] = r;
-        uint32_t rr = row_ok[i] ? r : 0;
-        uint32_t b = o.fdHW.div(rr);
-        uint32_t rem = rr - b * static_cast<uint32_t>(o.H * o.W);
-        uint32_t h = o.fdW.div(rem);
-        ph[i] = h;
-        pw[i] = rem - h * o.W;
-      }
-    }
-  }
-
-  __device__ __forceinline__ void load(const OperandDev& o, int k0, uint4 (&reg)[2]) const {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      int k = k0 + kq[i] * 8;
-      uint4 val = zero4();
-      if (row_ok[i] && k < o.K) {
-        if (MODE == OP_K_PLAIN) {
-          val = *reinterpret_cast<const uint4*>(o.p + row_base[i] + k);
-        } else {
-          uint32_t tap = o.fdC.div(k);
-          int c = k - static_cast<int>(tap) * o.C;
-          int kh = (tap * 11) >> 5;  // tap / 3 for tap < 9
-          int kw = tap - 3 * kh;
-          int dh = (MODE == OP_K_CONV_FWD) ? kh - 1 : 1 - kh;
-          int dw = (MODE == OP_K_CONV_FWD) ? kw - 1 : 1 - kw;
-          int hh = ph[i] + dh, ww = pw[i] + dw;
-          if (hh >= 0 && hh < o.H && ww >= 0 && ww < o.W) {
-            long pix = row_base[i] + static_cast<long>(dh) * o.W + dw;
-            val = *reinterpret_cast<const uint4*>(o.p + pix * o.C + c);
-          }
-        }
-      }
-      reg[i] = val;
-    }
-  }
-
-  __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[2], int tid) const {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      int v = tid + NT * i;
-      *reinterpret_cast<uint4*>(lds + lds_idx(v >> 2, kq[i] * 8)) = reg[i];
-    }
-  }
-};
-
-// ---- R-mode: 8 consecutive rows of one k ----------------------------------
-template <int MODE>
-struct RLoader {
-  int kp;        // this thread loads k = 2*kp and 2*kp + 1 of each K step
-  int rg;        // row group: tile rows rg*8 .. rg*8+7
-  int rows_ok;
-  long col;      // PLAIN: first row index; WGRAD: channel c; FILTER_T: first row (c)
-  int tap;       // WGRAD: filter tap of this row group
-
-  __device__ void init(const OperandDev& o, int row0, int tid) {
-    kp = tid & 15;
-    rg = tid >> 4;
-    int r = row0 + rg * 8;
-    rows_ok = r < o.rows;   // rows are a multiple of 8
-    if (MODE == OP_R_CONV_WGRAD) {
-      uint32_t rr = rows_ok ? r : 0;
-      tap = o.fdC.div(rr);
-      col = rr - tap * o.C;
-    } else {
-      tap = 0;
-      col = r;
-    }
-  }
-
-  __device__ __forceinline__ uint4 fetch(const OperandDev& o, int k) const {
-    if (!rows_ok || k >= o.K) return zero4();
-    if (MODE == OP_R_PLAIN) {
-      return *reinterpret_cast<const uint4*>(o.p + static_cast<long>(k) * o.ld + col);
-    } else if (MODE == OP_R_CONV_WGRAD) {
-      uint32_t b = o.fdHW.div(k);
-      uint32_t rem = k - b * static_cast<uint32_t>(o.H * o.W);
-      int h = o.fdW.div(rem);
-      int w = rem - h * o.W;
-      int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
-      int hh = h + kh - 1, ww = w + kw - 1;
-      if (hh < 0 || hh >= o.H || ww < 0 || ww >= o.W) return zero4();
-      long pix = static_cast<long>(k) + static_cast<long>(kh - 1) * o.W + (kw - 1);
-      return *reinterpret_cast<const uint4*>(o.p + pix * o.C + col);
-    } else {  // OP_R_FILTER_T: filter [C2][9][C], k = tap * C2 + c2
-      uint32_t t = o.fdC2.div(k);
-      int c2 = k - static_cast<int>(t) * o.C2;
-      return *reinterpret_cast<const uint4*>(o.p + (static_cast<long>(c2) * 9 + t) * o.C + col);
-    }
-  }
-
-  __device__ __forceinline__ void load(const OperandDev& o, int k0, uint4 (&reg)[2]) const {
-    reg[0] = fetch(o, k0 + 2 * kp);
-    reg[1] = fetch(o, k0 + 2 * kp + 1);
-  }
-
-  __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[2], int) const {
-    const uint32_t* a = reinterpret_cast<const uint32_t*>(&reg[0]);
-    const uint32_t* b = reinterpret_cast<const uint32_t*>(&reg[1]);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      uint32_t lo = (j & 1) ? (a[j >> 1] >> 16) : (a[j >> 1] & 0xffffu);
-      uint32_t hi = (j & 1) ? (b[j >> 1] >> 16) : (b[j >> 1] & 0xffffu);
-      *reinterpret_cast<uint32_t*>(lds + lds_idx(rg * 8 + j, 2 * kp)) = lo | (hi << 16);
-    }
-  }
-};
-
-template <int MODE>
-struct LoaderFor {
-  using type = typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE>, RLoader<MODE>>::type;
 };
 
 struct EpiDev {
@@ -182,32 +54,209 @@ struct EpiDev {
 };
 
 struct KArgs {
-  int M, N, K, zdiv, tiles_n, tiles_total;
+  int M, N, K, zdiv, tiles_n, tiles_total, batch, splits, k_per_split;
   OperandDev A, B;
   long a_bs1, a_bs2, b_bs1, b_bs2, c_bs1, c_bs2;
+  float* partial;   // splits > 1: [split][batch][M][N] float32
   EpiDev e;
 };
 
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const bf16_t* p, long elems) {
+  long bytes = elems * 2;
+  if (bytes > 0x7fffffe0L) bytes = 0x7fffffe0L;
+  if (bytes < 0) bytes = 0;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p), static_cast<short>(0), static_cast<int>(bytes),
+                                           BUF_FLAGS);
+}
+
+__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// ---- K-mode: 8 consecutive k of one row ----------------------------------
+// Thread t loads vectors v = t + 256 i (i < 4): tile row v / 8, k chunk v % 8.
+template <int MODE>
+struct KLoader {
+  int row_ok[4];
+  int row_base[4];   // PLAIN: row * ld (elements); CONV: pixel index
+  int ph[4], pw[4];  // CONV: pixel coordinates
+
+  __device__ void init(const OperandDev& o, int row0, int tid) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = tid + NT * i;
+      const int r = row0 + (v >> 3);
+      row_ok[i] = r < o.rows;
+      if (MODE == OP_K_PLAIN) {
+        row_base[i] = static_cast<int>(r * o.ld);
+      } else {
+        const uint32_t rr = row_ok[i] ? r : 0;
+        const uint32_t b = o.fdHW.div(rr);
+        const uint32_t rem = rr - b * static_cast<uint32_t>(o.H * o.W);
+        const uint32_t h = o.fdW.div(rem);
+        row_base[i] = r;
+        ph[i] = h;
+        pw[i] = rem - h * o.W;
+      }
+    }
+  }
+
+  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, int tid,
+                                       uint4 (&reg)[4]) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = k0 + ((tid + NT * i) & 7) * 8;
+      int off = OOB;
+      if (MODE == OP_K_PLAIN) {
+        if (row_ok[i] && k < o.K) off = (row_base[i] + k) * 2;
+      } else {
+        const uint32_t tap = o.fdC.div(k);
+        const int c = k - static_cast<int>(tap) * o.C;
+        const int kh = (tap * 11) >> 5;  // tap / 3 for tap < 9
+        const int kw = tap - 3 * kh;
+        const int dh = (MODE == OP_K_CONV_FWD) ? kh - 1 : 1 - kh;
+        const int dw = (MODE == OP_K_CONV_FWD) ? kw - 1 : 1 - kw;
+        const int hh = ph[i] + dh, ww = pw[i] + dw;
+        if (row_ok[i] && k < o.K && hh >= 0 && hh < o.H && ww >= 0 && ww < o.W)
+          off = ((row_base[i] + dh * o.W + dw) * o.C + c) * 2;
+      }
+      reg[i] = bload(rs, off);
+    }
+  }
+
+  __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[4], int tid) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = tid + NT * i;
+      *reinterpret_cast<uint4*>(lds + (v >> 3) * PITCH + (v & 7) * 8) = reg[i];
+    }
+  }
+};
+
+// ---- R-mode: 8 consecutive rows of one k ----------------------------------
+// Thread t loads k = k0 + 2 (t % 32) + {0, 1} for row groups t / 32 and
+// t / 32 + 8 (rows 8 g .. 8 g + 7), then writes 4-byte (k, k+1) pairs per row.
+template <int MODE>
+struct RLoader {
+  int rows_ok[2];
+  int col[2];   // PLAIN: first row index; WGRAD: channel; FILTER_T: first row
+  int tap[2];   // WGRAD: filter tap of the row group
+
+  __device__ void init(const OperandDev& o, int row0, int tid) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int r = row0 + ((tid >> 5) + 8 * j) * 8;
+      rows_ok[j] = r < o.rows;  // rows are a multiple of 8
+      if (MODE == OP_R_CONV_WGRAD) {
+        const uint32_t rr = rows_ok[j] ? r : 0;
+        tap[j] = o.fdC.div(rr);
+        col[j] = rr - tap[j] * o.C;
+      } else {
+        tap[j] = 0;
+        col[j] = r;
+      }
+    }
+  }
+
+  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, int tid,
+                                       uint4 (&reg)[4]) const {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int k = k0 + 2 * (tid & 31) + e;
+      const bool kok = k < o.K;
+      if (MODE == OP_R_PLAIN) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          reg[2 * j + e] = bload(rs, (kok && rows_ok[j]) ? static_cast<int>((k * o.ld + col[j]) * 2) : OOB);
+      } else if (MODE == OP_R_CONV_WGRAD) {
+        const uint32_t kk = kok ? k : 0;
+        const uint32_t b = o.fdHW.div(kk);
+        const uint32_t rem = kk - b * static_cast<uint32_t>(o.H * o.W);
+        const int h = o.fdW.div(rem);
+        const int w = rem - h * o.W;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int kh = (tap[j] * 11) >> 5, kw = tap[j] - 3 * kh;
+          const int hh = h + kh - 1, ww = w + kw - 1;
+          const bool ok = kok && rows_ok[j] && hh >= 0 && hh < o.H && ww >= 0 && ww < o.W;
+          reg[2 * j + e] = bload(rs, ok ? ((k + (kh - 1) * o.W + (kw - 1)) * o.C + col[j]) * 2 : OOB);
+        }
+      } else {  // OP_R_FILTER_T: filter [C2][9][C], k = tap * C2 + c2
+        const uint32_t kk = kok ? k : 0;
+        const uint32_t t = o.fdC2.div(kk);
+        const int c2 = kk - t * o.C2;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          reg[2 * j + e] = bload(rs, (kok && rows_ok[j]) ? ((c2 * 9 + static_cast<int>(t)) * o.C + col[j]) * 2 : OOB);
+      }
+    }
+  }
+
+  __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[4], int tid) const {
+    const int kcol = 2 * (tid & 31);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t* a = reinterpret_cast<const uint32_t*>(&reg[2 * j]);
+      const uint32_t* b = reinterpret_cast<const uint32_t*>(&reg[2 * j + 1]);
+      const int rbase = ((tid >> 5) + 8 * j) * 8;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const uint32_t lo = (r & 1) ? (a[r >> 1] >> 16) : (a[r >> 1] & 0xffffu);
+        const uint32_t hi = (r & 1) ? (b[r >> 1] >> 16) : (b[r >> 1] & 0xffffu);
+        *reinterpret_cast<uint32_t*>(lds + (rbase + r) * PITCH + kcol) = lo | (hi << 16);
+      }
+    }
+  }
+};
+
+template <int MODE>
+struct LoaderFor {
+  using type = typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE>, RLoader<MODE>>::type;
+};
+
+// value = acc * alpha + bias + residuals, ReLU, then float32 and/or bf16 stores
+// (the bf16 store is zeroed where the mask is not positive).
+__device__ __forceinline__ void epilogue(const EpiDev& e, long idx, int col, float acc) {
+  float v = acc * e.alpha;
+  if (e.bias) v += e.bias[col];
+  else if (e.bias_bf16) v += bf16_to_f32(e.bias_bf16[col]);
+  if (e.res_f32) v += e.res_f32[idx];
+  if (e.res_bf16) v += bf16_to_f32(e.res_bf16[idx]);
+  if (e.relu) v = fmaxf(v, 0.0f);
+  if (e.out_f32) {
+    if (e.accumulate) e.out_f32[idx] += v;
+    else e.out_f32[idx] = v;
+  }
+  if (e.out_bf16) {
+    bf16_t h = f32_to_bf16(v);
+    if (e.mask && !(bf16_to_f32(e.mask[idx]) > 0.0f)) h = 0;
+    e.out_bf16[idx] = h;
+  }
+}
+
 template <int MA, int MB>
-__global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(KArgs args) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TILE_ELEMS];  // [buffer][A|B]
 
   const int tid = threadIdx.x;
-  // XCD-aware tile order: hardware places consecutive blocks on consecutive
-  // XCDs; renumber so each XCD receives a contiguous run of tiles (rows of
-  // tiles sharing A rows then stay within one L2).
-  int bid = blockIdx.x;
+  // XCD-aware tile order: consecutive blocks land on consecutive XCDs; give
+  // each XCD a contiguous run of tiles (tiles sharing A rows share an L2).
+  const int bid = blockIdx.x;
   int tile = bid;
   if ((args.tiles_total & 7) == 0) tile = (bid & 7) * (args.tiles_total >> 3) + (bid >> 3);
   const int tm = tile / args.tiles_n, tn = tile - tm * args.tiles_n;
   const int row0 = tm * BM, col0 = tn * BN;
 
-  const int z = blockIdx.y;
+  const int zs = blockIdx.y;
+  const int z = zs / args.splits, split = zs - z * args.splits;
   const int z1 = z / args.zdiv, z2 = z - z1 * args.zdiv;
   OperandDev A = args.A, B = args.B;
-  A.p += z1 * args.a_bs1 + z2 * args.a_bs2;
-  B.p += z1 * args.b_bs1 + z2 * args.b_bs2;
-  const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
+  const long aoff = z1 * args.a_bs1 + z2 * args.a_bs2, boff = z1 * args.b_bs1 + z2 * args.b_bs2;
+  A.p += aoff;
+  B.p += boff;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A.p, A.extent - aoff);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(B.p, B.extent - boff);
 
   typename LoaderFor<MA>::type la;
   typename LoaderFor<MB>::type lb;
@@ -225,85 +274,140 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  uint4 ra[2], rb[2];
-  const int nk = (args.K + BK - 1) / BK;
-  la.load(A, 0, ra);
-  lb.load(B, 0, rb);
-  la.store(lds[0][0], ra, tid);
-  lb.store(lds[0][1], rb, tid);
-  __syncthreads();
+  const int kbeg = split * args.k_per_split;
+  const int kend = min(args.K, kbeg + args.k_per_split);
+  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      la.load(A, (kt + 1) * BK, ra);
-      lb.load(B, (kt + 1) * BK, rb);
-    }
-    const bf16_t* sa = lds[cur][0];
-    const bf16_t* sb = lds[cur][1];
+  auto compute = [&](const bf16_t* sa, const bf16_t* sb) {
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 16) {
       bf16x8_t fa[2], fb[2];
       const int kl = kk + (lane >> 5) * 8;
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        u16x8_t t = *reinterpret_cast<const u16x8_t*>(sa + lds_idx(wm * 64 + i * 32 + (lane & 31), kl));
-        fa[i] = __builtin_bit_cast(bf16x8_t, t);
-      }
+      for (int i = 0; i < 2; ++i)
+        fa[i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u16x8_t*>(
+                                                 sa + (wm * 64 + i * 32 + (lane & 31)) * PITCH + kl));
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        u16x8_t t = *reinterpret_cast<const u16x8_t*>(sb + lds_idx(wn * 64 + j * 32 + (lane & 31), kl));
-        fb[j] = __builtin_bit_cast(bf16x8_t, t);
-      }
+      for (int j = 0; j < 2; ++j)
+        fb[j] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u16x8_t*>(
+                                                 sb + (wn * 64 + j * 32 + (lane & 31)) * PITCH + kl));
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) {
-      la.store(lds[cur ^ 1][0], ra, tid);
-      lb.store(lds[cur ^ 1][1], rb, tid);
+  };
+
+  if (nk > 0) {
+    uint4 ra0[4], rb0[4], ra1[4], rb1[4];
+    la.load(A, ra, kbeg, tid, ra0);
+    lb.load(B, rb, kbeg, tid, rb0);
+    if (nk > 1) {
+      la.load(A, ra, kbeg + BK, tid, ra1);
+      lb.load(B, rb, kbeg + BK, tid, rb1);
     }
+    la.store(lds[0][0], ra0, tid);
+    lb.store(lds[0][1], rb0, tid);
     __syncthreads();
+    // registers of set 0 / 1 hold K steps of even / odd index; LDS buffer b
+    // holds the step being multiplied
+    for (int kt = 0; kt < nk; kt += 2) {
+      if (kt + 2 < nk) {
+        la.load(A, ra, kbeg + (kt + 2) * BK, tid, ra0);
+        lb.load(B, rb, kbeg + (kt + 2) * BK, tid, rb0);
+      }
+      compute(lds[0][0], lds[0][1]);
+      if (kt + 1 < nk) {
+        la.store(lds[1][0], ra1, tid);
+        lb.store(lds[1][1], rb1, tid);
+      }
+      __syncthreads();
+      if (kt + 1 >= nk) break;
+      if (kt + 3 < nk) {
+        la.load(A, ra, kbeg + (kt + 3) * BK, tid, ra1);
+        lb.load(B, rb, kbeg + (kt + 3) * BK, tid, rb1);
+      }
+      compute(lds[1][0], lds[1][1]);
+      if (kt + 2 < nk) {
+        la.store(lds[0][0], ra0, tid);
+        lb.store(lds[0][1], rb0, tid);
+      }
+      __syncthreads();
+    }
   }
 
-  // Epilogue: lane holds column (lane % 32) and rows 8*(r/4) + 4*(lane/32) + r%4.
-  const EpiDev& e = args.e;
+  // Lane holds column (lane % 32) and rows 8*(r/4) + 4*(lane/32) + r%4 of each
+  // 32 x 32 tile.
+  if (args.splits > 1) {
+    float* part = args.partial + (static_cast<long>(split) * args.batch + z) * args.M * args.N;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int col = col0 + wn * 64 + j * 32 + (lane & 31);
+        if (col >= args.N) continue;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+          if (row < args.M) part[static_cast<long>(row) * args.N + col] = acc[i][j][r];
+        }
+      }
+    return;
+  }
+  const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int col = col0 + wn * 64 + j * 32 + (lane & 31);
       if (col >= args.N) continue;
-      const float bias = e.bias ? e.bias[col] : (e.bias_bf16 ? bf16_to_f32(e.bias_bf16[col]) : 0.0f);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = row0 + wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        if (row >= args.M) continue;
-        const long idx = coff + static_cast<long>(row) * e.ldc + col;
-        float v = acc[i][j][r] * e.alpha + bias;
-        if (e.res_f32) v += e.res_f32[idx];
-        if (e.res_bf16) v += bf16_to_f32(e.res_bf16[idx]);
-        if (e.relu) v = fmaxf(v, 0.0f);
-        if (e.out_f32) {
-          if (e.accumulate) e.out_f32[idx] += v;
-          else e.out_f32[idx] = v;
-        }
-        if (e.out_bf16) {
-          bf16_t h = f32_to_bf16(v);
-          if (e.mask && !(bf16_to_f32(e.mask[idx]) > 0.0f)) h = 0;
-          e.out_bf16[idx] = h;
-        }
+        if (row < args.M) epilogue(args.e, coff + static_cast<long>(row) * args.e.ldc + col, col, acc[i][j][r]);
       }
     }
+}
+
+// Sum the split partials in split order and apply the epilogue.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(KArgs args) {
+  const long total = static_cast<long>(args.batch) * args.M * args.N;
+  const long plane = total;
+  for (long t = static_cast<long>(blockIdx.x) * 256 + threadIdx.x; t < total;
+       t += static_cast<long>(gridDim.x) * 256) {
+    float s = 0.0f;
+    for (int sp = 0; sp < args.splits; ++sp) s += args.partial[sp * plane + t];
+    const long mn = static_cast<long>(args.M) * args.N;
+    const int z = static_cast<int>(t / mn);
+    const long rem = t - z * mn;
+    const int row = static_cast<int>(rem / args.N), col = static_cast<int>(rem - static_cast<long>(row) * args.N);
+    const int z1 = z / args.zdiv, z2 = z - z1 * args.zdiv;
+    epilogue(args.e, z1 * args.c_bs1 + z2 * args.c_bs2 + static_cast<long>(row) * args.e.ldc + col, col, s);
   }
 }
 
-OperandDev make_operand(const Operand& o, int rows, int K) {
+// Elements a correct launch may read from the batch-0 base: the operand of
+// the last batch at its largest row and k (or the whole gathered tensor).
+long operand_extent(const Operand& o, int rows, int K, int batch, int zdiv) {
+  if (o.extent > 0) return o.extent;
+  long per;
+  switch (o.mode) {
+    case OP_K_PLAIN: per = static_cast<long>(rows - 1) * o.ld + K; break;
+    case OP_R_PLAIN: per = static_cast<long>(K - 1) * o.ld + rows; break;
+    case OP_R_FILTER_T: per = static_cast<long>(o.g.C2) * 9 * o.g.C; break;
+    default: per = static_cast<long>(o.g.B) * o.g.H * o.g.W * o.g.C; break;
+  }
+  const long z1max = (batch - 1) / zdiv;
+  const long z2max = batch > zdiv ? zdiv - 1 : batch - 1;
+  return per + z1max * o.bs1 + z2max * o.bs2;
+}
+
+OperandDev make_operand(const Operand& o, int rows, int K, long extent) {
   OperandDev d{};
   d.p = static_cast<const bf16_t*>(o.ptr);
   d.ld = o.ld;
+  d.extent = extent;
   d.rows = rows;
   d.K = K;
   d.H = o.g.H;
@@ -318,8 +422,8 @@ OperandDev make_operand(const Operand& o, int rows, int K) {
 }
 
 template <int MA, int MB>
-hipError_t launch(const KArgs& a, int batch, hipStream_t s) {
-  dim3 grid(a.tiles_total, batch);
+hipError_t launch(const KArgs& a, hipStream_t s) {
+  dim3 grid(a.tiles_total, a.batch * a.splits);
   hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB>), grid, dim3(NT), 0, s, a);
   return hipGetLastError();
 }
@@ -328,15 +432,36 @@ hipError_t launch(const KArgs& a, int batch, hipStream_t s) {
 
 hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s) {
   if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return hipSuccess;
+  const int zdiv = d.zdiv > 0 ? d.zdiv : 1;
+  const long ext_a = operand_extent(d.A, d.M, d.K, d.batch, zdiv);
+  const long ext_b = operand_extent(d.B, d.N, d.K, d.batch, zdiv);
+  if (d.K <= 0 || ext_a <= 0 || ext_b <= 0 || ext_a >= (1L << 30) || ext_b >= (1L << 30))
+    return hipErrorInvalidValue;   // operands are addressed with 32-bit byte offsets
   KArgs a{};
   a.M = d.M;
   a.N = d.N;
   a.K = d.K;
-  a.zdiv = d.zdiv > 0 ? d.zdiv : 1;
+  a.batch = d.batch;
+  a.zdiv = zdiv;
   a.tiles_n = (d.N + BN - 1) / BN;
   a.tiles_total = a.tiles_n * ((d.M + BM - 1) / BM);
-  a.A = make_operand(d.A, d.M, d.K);
-  a.B = make_operand(d.B, d.N, d.K);
+  // split K when the tiles cannot fill the chip and K is long: each split
+  // keeps at least 8 K steps
+  int splits = 1;
+  const long tiles = static_cast<long>(a.tiles_total) * d.batch;
+  if (d.workspace && tiles < 256 && d.K >= 2 * 8 * BK) {
+    splits = static_cast<int>((256 + tiles - 1) / tiles);
+    splits = std::min(splits, d.K / (8 * BK));
+    splits = std::min(splits, 16);
+    const long per = static_cast<long>(d.batch) * d.M * d.N * 4;
+    while (splits > 1 && per * splits > static_cast<long>(d.workspace_bytes)) --splits;
+  }
+  const int ksteps = (d.K + BK - 1) / BK;
+  a.k_per_split = ((ksteps + splits - 1) / splits) * BK;
+  a.splits = splits;
+  a.partial = d.workspace;
+  a.A = make_operand(d.A, d.M, d.K, ext_a);
+  a.B = make_operand(d.B, d.N, d.K, ext_b);
   a.a_bs1 = d.A.bs1;
   a.a_bs2 = d.A.bs2;
   a.b_bs1 = d.B.bs1;
@@ -355,13 +480,20 @@ hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s) {
   a.e.relu = d.epi.relu;
   a.e.accumulate = d.epi.accumulate;
   const int ma = d.A.mode, mb = d.B.mode;
-  if (ma == OP_K_PLAIN && mb == OP_K_PLAIN) return launch<OP_K_PLAIN, OP_K_PLAIN>(a, d.batch, s);
-  if (ma == OP_K_PLAIN && mb == OP_R_PLAIN) return launch<OP_K_PLAIN, OP_R_PLAIN>(a, d.batch, s);
-  if (ma == OP_R_PLAIN && mb == OP_R_PLAIN) return launch<OP_R_PLAIN, OP_R_PLAIN>(a, d.batch, s);
-  if (ma == OP_K_CONV_FWD && mb == OP_K_PLAIN) return launch<OP_K_CONV_FWD, OP_K_PLAIN>(a, d.batch, s);
-  if (ma == OP_K_CONV_DGRAD && mb == OP_R_FILTER_T) return launch<OP_K_CONV_DGRAD, OP_R_FILTER_T>(a, d.batch, s);
-  if (ma == OP_R_PLAIN && mb == OP_R_CONV_WGRAD) return launch<OP_R_PLAIN, OP_R_CONV_WGRAD>(a, d.batch, s);
-  return hipErrorInvalidValue;
+  hipError_t err;
+  if (ma == OP_K_PLAIN && mb == OP_K_PLAIN) err = launch<OP_K_PLAIN, OP_K_PLAIN>(a, s);
+  else if (ma == OP_K_PLAIN && mb == OP_R_PLAIN) err = launch<OP_K_PLAIN, OP_R_PLAIN>(a, s);
+  else if (ma == OP_R_PLAIN && mb == OP_R_PLAIN) err = launch<OP_R_PLAIN, OP_R_PLAIN>(a, s);
+  else if (ma == OP_K_CONV_FWD && mb == OP_K_PLAIN) err = launch<OP_K_CONV_FWD, OP_K_PLAIN>(a, s);
+  else if (ma == OP_K_CONV_DGRAD && mb == OP_R_FILTER_T) err = launch<OP_K_CONV_DGRAD, OP_R_FILTER_T>(a, s);
+  else if (ma == OP_R_PLAIN && mb == OP_R_CONV_WGRAD) err = launch<OP_R_PLAIN, OP_R_CONV_WGRAD>(a, s);
+  else return hipErrorInvalidValue;
+  if (err != hipSuccess || splits == 1) return err;
+  const long total = static_cast<long>(d.batch) * d.M * d.N;
+  long blocks = (total + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(static_cast<int>(blocks)), dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 }  // namespace spx

@@ -30,6 +30,7 @@ struct ConvGeom {
 struct Operand {
   const void* ptr = nullptr;   // bf16 (or float32 for the float32 GEMM)
   long ld = 0;
+  long extent = 0;             // elements addressable from ptr (batch 0); reads beyond it return 0
   long bs1 = 0, bs2 = 0;       // batch strides (elements) for z / zdiv and z % zdiv
   int mode = OP_K_PLAIN;
   ConvGeom g;
@@ -53,6 +54,8 @@ struct Epilogue {
 struct GemmDesc {
   int M = 0, N = 0, K = 0;
   int batch = 1, zdiv = 1;
+  float* workspace = nullptr;      // split-K partials (bf16 GEMM); NULL disables splitting
+  size_t workspace_bytes = 0;
   Operand A, B;
   Epilogue epi;
 };

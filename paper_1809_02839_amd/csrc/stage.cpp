@@ -158,7 +158,12 @@ void Stage::gemm(const GemmDesc& d) {
   else if (ma == OP_K_PLAIN && mb == OP_R_PLAIN) name = dt_ ? "gemm_bf16_dyW" : "gemm_f32_dyW";
   else if (ma == OP_R_PLAIN && mb == OP_R_PLAIN) name = dt_ ? "gemm_bf16_dyTx" : "gemm_f32_dyTx";
   const double flops = 2.0 * d.M * d.N * static_cast<double>(d.K) * d.batch;
-  LAUNCH(name, flops, 0, dt_ ? gemm_bf16(d, s_) : gemm_f32(d, s_));
+  GemmDesc dd = d;
+  if (dt_) {
+    dd.workspace = ws<float>(static_cast<int>(ws_off_.size()) - 1);
+    dd.workspace_bytes = gemm_ws_bytes_;
+  }
+  LAUNCH(name, flops, 0, dt_ ? gemm_bf16(dd, s_) : gemm_f32(dd, s_));
 }
 
 // ------------------------------------------------------------ profiling ----
@@ -278,7 +283,9 @@ void Stage::plan_buffers() {
       break;
     }
   }
-  ws.push_back(static_cast<size_t>(std::max<long>(partial, 1) * 4));  // column-sum partials: last id
+  ws.push_back(static_cast<size_t>(std::max<long>(partial, 1) * 4));  // column-sum partials
+  gemm_ws_bytes_ = dt_ ? (64u << 20) : 0;
+  ws.push_back(std::max<size_t>(gemm_ws_bytes_, 1));                   // split-K partials: last id
   DeviceBlock probe;
   for (size_t b : st) stash_off_.push_back(probe.add(std::max<size_t>(b, 1)));
   for (size_t b : ws) ws_off_.push_back(ws_block_.add(std::max<size_t>(b, 1)));

@@ -149,6 +149,7 @@ class Stage {
   std::vector<size_t> stash_off_;
   DeviceBlock ws_block_;
   std::vector<size_t> ws_off_;
+  size_t gemm_ws_bytes_ = 0;
   bool g_pending_ = false;
 
   struct ProfRec {
