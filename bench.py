@@ -141,6 +141,9 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first run one device-to-device copy of this many MiB (a known-size reference "
+                         "dispatch for scaling hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs one pipeline stage on one GPU; --gpus above 1 is not supported "
@@ -155,6 +158,14 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     spec = synth.WORKLOADS[args.workload].stages[0]
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib << 18   # float32 elements
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy: {n * 4} bytes read, {n * 4} bytes written")
+        del src, dst
     stream = torch.cuda.Stream()
     loop = StageLoop(spec, torch, native, stream)
 

@@ -75,12 +75,21 @@ __global__ void colsum_partial_kernel(const T* X, long rows, int cols, long ld, 
   __syncthreads();
   if (ty == 0 && col < cols) partial[static_cast<long>(blockIdx.y) * cols + col] = (sh[0][tx] + sh[1][tx]) + (sh[2][tx] + sh[3][tx]);
 }
+// Pass 2: 64 columns per block; the four waves split the chunks (chunk c goes
+// to wave c % 4), then the four wave sums are added in a fixed order.
 __global__ void colsum_final_kernel(const float* partial, int nchunks, int cols, float* out, int accumulate) {
-  const int col = blockIdx.x * NT + threadIdx.x;
-  if (col >= cols) return;
+  __shared__ float sh[4][64];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int col = blockIdx.x * 64 + tx;
   float s = 0.0f;
-  for (int c = 0; c < nchunks; ++c) s += partial[static_cast<long>(c) * cols + col];
-  out[col] = accumulate ? out[col] + s : s;
+  if (col < cols)
+    for (int c = ty; c < nchunks; c += 4) s += partial[static_cast<long>(c) * cols + col];
+  sh[ty][tx] = s;
+  __syncthreads();
+  if (ty == 0 && col < cols) {
+    const float v = (sh[0][tx] + sh[1][tx]) + (sh[2][tx] + sh[3][tx]);
+    out[col] = accumulate ? out[col] + v : v;
+  }
 }
 
 // ---------------------------------------------------- cross-entropy ----
@@ -333,7 +342,7 @@ hipError_t column_sum(const void* X, int dtype, long rows, int cols, long ld, fl
       hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(NT), 0, s, static_cast<const float*>(X), rows,
                          cols, ld, partial_ws);
   }
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + NT - 1) / NT), dim3(NT), 0, s, partial_ws, nchunks, cols, out,
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 63) / 64), dim3(NT), 0, s, partial_ws, nchunks, cols, out,
                      accumulate);
   return hipGetLastError();
 }
@@ -364,8 +373,8 @@ hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, c
   float* pg = partial_ws;
   float* pb = partial_ws + static_cast<long>(nb) * D;
   hipLaunchKernelGGL(layernorm_bwd_kernel, dim3(nb), dim3(NT), 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb);
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + NT - 1) / NT), dim3(NT), 0, s, pg, nb, D, dgamma, 0);
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + NT - 1) / NT), dim3(NT), 0, s, pb, nb, D, dbeta, 0);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 63) / 64), dim3(NT), 0, s, pg, nb, D, dgamma, 0);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 63) / 64), dim3(NT), 0, s, pb, nb, D, dbeta, 0);
   return hipGetLastError();
 }
 

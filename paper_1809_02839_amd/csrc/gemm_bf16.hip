@@ -37,6 +37,7 @@ struct OperandDev {
   int rows;        // extent of the row dimension (M for A, N for B)
   int K;
   int H, W, C, C2;
+  int step_h, step_w;   // WGRAD gather: BK pixels expressed as (rows, columns) inside an image
   FastDiv fdC, fdC2, fdHW, fdW;
 };
 
@@ -75,53 +76,71 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, int byte_off) {
 }
 
 // ---- K-mode: 8 consecutive k of one row ----------------------------------
-// Thread t loads vectors v = t + 256 i (i < 4): tile row v / 8, k chunk v % 8.
-template <int MODE>
+// Thread t loads vectors v = t + 256 i (i < 4): tile row v / 8, k chunk t % 8.
+// TAPK (convolutions whose channel count is a multiple of BK): every K step
+// lies inside one filter tap, so the tap and its pixel shift are uniform for
+// the whole block and each vector costs one add and a bounds check.
+template <int MODE, bool TAPK>
 struct KLoader {
   int row_ok[4];
-  int row_base[4];   // PLAIN: row * ld (elements); CONV: pixel index
+  int base[4];       // byte offset of the row (PLAIN) or of the pixel's channel 0 (CONV)
   int ph[4], pw[4];  // CONV: pixel coordinates
+  int kq8;           // this thread's k offset inside a K step
 
-  __device__ void init(const OperandDev& o, int row0, int tid) {
+  __device__ void init(const OperandDev& o, int row0, int tid, int /*k0*/) {
+    kq8 = (tid & 7) * 8;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int v = tid + NT * i;
-      const int r = row0 + (v >> 3);
+      const int r = row0 + ((tid + NT * i) >> 3);
       row_ok[i] = r < o.rows;
+      const uint32_t rr = row_ok[i] ? r : 0;
       if (MODE == OP_K_PLAIN) {
-        row_base[i] = static_cast<int>(r * o.ld);
+        base[i] = static_cast<int>(rr * o.ld * 2);
       } else {
-        const uint32_t rr = row_ok[i] ? r : 0;
         const uint32_t b = o.fdHW.div(rr);
         const uint32_t rem = rr - b * static_cast<uint32_t>(o.H * o.W);
         const uint32_t h = o.fdW.div(rem);
-        row_base[i] = r;
         ph[i] = h;
         pw[i] = rem - h * o.W;
+        base[i] = static_cast<int>(rr) * o.C * 2;
       }
     }
   }
 
-  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, int tid,
-                                       uint4 (&reg)[4]) const {
+  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, uint4 (&reg)[4]) {
+    const int k = k0 + kq8;
+    const bool kok = k < o.K;
+    if (MODE == OP_K_PLAIN) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int k = k0 + ((tid + NT * i) & 7) * 8;
-      int off = OOB;
-      if (MODE == OP_K_PLAIN) {
-        if (row_ok[i] && k < o.K) off = (row_base[i] + k) * 2;
-      } else {
-        const uint32_t tap = o.fdC.div(k);
-        const int c = k - static_cast<int>(tap) * o.C;
-        const int kh = (tap * 11) >> 5;  // tap / 3 for tap < 9
-        const int kw = tap - 3 * kh;
-        const int dh = (MODE == OP_K_CONV_FWD) ? kh - 1 : 1 - kh;
-        const int dw = (MODE == OP_K_CONV_FWD) ? kw - 1 : 1 - kw;
+      for (int i = 0; i < 4; ++i) reg[i] = bload(rs, (row_ok[i] && kok) ? base[i] + k * 2 : OOB);
+    } else if (TAPK) {
+      const int tap = static_cast<int>(o.fdC.div(k0));     // uniform
+      const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
+      const int dh = (MODE == OP_K_CONV_FWD) ? kh - 1 : 1 - kh;
+      const int dw = (MODE == OP_K_CONV_FWD) ? kw - 1 : 1 - kw;
+      const int shift = ((dh * o.W + dw) * o.C + (k0 - tap * o.C) + kq8) * 2;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
         const int hh = ph[i] + dh, ww = pw[i] + dw;
-        if (row_ok[i] && k < o.K && hh >= 0 && hh < o.H && ww >= 0 && ww < o.W)
-          off = ((row_base[i] + dh * o.W + dw) * o.C + c) * 2;
+        const bool ok = row_ok[i] && static_cast<unsigned>(hh) < static_cast<unsigned>(o.H) &&
+                        static_cast<unsigned>(ww) < static_cast<unsigned>(o.W);
+        reg[i] = bload(rs, ok ? base[i] + shift : OOB);
       }
-      reg[i] = bload(rs, off);
+    } else {
+      const uint32_t tap = o.fdC.div(kok ? k : 0);
+      const int c = k - static_cast<int>(tap) * o.C;
+      const int kh = (tap * 11) >> 5;  // tap / 3 for tap < 9
+      const int kw = tap - 3 * kh;
+      const int dh = (MODE == OP_K_CONV_FWD) ? kh - 1 : 1 - kh;
+      const int dw = (MODE == OP_K_CONV_FWD) ? kw - 1 : 1 - kw;
+      const int shift = ((dh * o.W + dw) * o.C + c) * 2;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int hh = ph[i] + dh, ww = pw[i] + dw;
+        const bool ok = row_ok[i] && kok && static_cast<unsigned>(hh) < static_cast<unsigned>(o.H) &&
+                        static_cast<unsigned>(ww) < static_cast<unsigned>(o.W);
+        reg[i] = bload(rs, ok ? base[i] + shift : OOB);
+      }
     }
   }
 
@@ -135,60 +154,85 @@ struct KLoader {
 };
 
 // ---- R-mode: 8 consecutive rows of one k ----------------------------------
-// Thread t loads k = k0 + 2 (t % 32) + {0, 1} for row groups t / 32 and
+// Thread t loads k = k0 + 2 (t % 32) + e (e < 2) for row groups t / 32 and
 // t / 32 + 8 (rows 8 g .. 8 g + 7), then writes 4-byte (k, k+1) pairs per row.
-template <int MODE>
+// Loads must be issued for consecutive K steps (the filter-gradient gather
+// advances its pixel coordinates by BK per call).
+template <int MODE, bool TAPK>
 struct RLoader {
   int rows_ok[2];
-  int col[2];   // PLAIN: first row index; WGRAD: channel; FILTER_T: first row
-  int tap[2];   // WGRAD: filter tap of the row group
+  int colb[2];   // per row group: byte offset of the first row (PLAIN), channel + tap shift (WGRAD), channel (FILTER_T)
+  int tkh[2], tkw[2];
+  int ek[2];     // 2 (t % 32) + e
+  int h[2], w[2];
 
-  __device__ void init(const OperandDev& o, int row0, int tid) {
+  __device__ void init(const OperandDev& o, int row0, int tid, int k0) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) ek[e] = 2 * (tid & 31) + e;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int r = row0 + ((tid >> 5) + 8 * j) * 8;
       rows_ok[j] = r < o.rows;  // rows are a multiple of 8
+      const uint32_t rr = rows_ok[j] ? r : 0;
       if (MODE == OP_R_CONV_WGRAD) {
-        const uint32_t rr = rows_ok[j] ? r : 0;
-        tap[j] = o.fdC.div(rr);
-        col[j] = rr - tap[j] * o.C;
+        const int tap = static_cast<int>(o.fdC.div(rr));
+        tkh[j] = (tap * 11) >> 5;
+        tkw[j] = tap - 3 * tkh[j];
+        colb[j] = (((tkh[j] - 1) * o.W + (tkw[j] - 1)) * o.C + static_cast<int>(rr) - tap * o.C) * 2;
+      } else if (MODE == OP_R_PLAIN) {
+        colb[j] = static_cast<int>(rr) * 2;
       } else {
-        tap[j] = 0;
-        col[j] = r;
+        colb[j] = static_cast<int>(rr) * 2;
+      }
+    }
+    if (MODE == OP_R_CONV_WGRAD) {
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const uint32_t kk = k0 + ek[e];
+        const uint32_t b = o.fdHW.div(kk);
+        const uint32_t rem = kk - b * static_cast<uint32_t>(o.H * o.W);
+        h[e] = o.fdW.div(rem);
+        w[e] = rem - h[e] * o.W;
       }
     }
   }
 
-  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, int tid,
-                                       uint4 (&reg)[4]) const {
+  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, uint4 (&reg)[4]) {
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      const int k = k0 + 2 * (tid & 31) + e;
+      const int k = k0 + ek[e];
       const bool kok = k < o.K;
       if (MODE == OP_R_PLAIN) {
+        const int kb = static_cast<int>(k * o.ld * 2);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          reg[2 * j + e] = bload(rs, (kok && rows_ok[j]) ? static_cast<int>((k * o.ld + col[j]) * 2) : OOB);
+        for (int j = 0; j < 2; ++j) reg[2 * j + e] = bload(rs, (kok && rows_ok[j]) ? kb + colb[j] : OOB);
       } else if (MODE == OP_R_CONV_WGRAD) {
-        const uint32_t kk = kok ? k : 0;
-        const uint32_t b = o.fdHW.div(kk);
-        const uint32_t rem = kk - b * static_cast<uint32_t>(o.H * o.W);
-        const int h = o.fdW.div(rem);
-        const int w = rem - h * o.W;
+        const int kb = k * o.C * 2;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          const int kh = (tap[j] * 11) >> 5, kw = tap[j] - 3 * kh;
-          const int hh = h + kh - 1, ww = w + kw - 1;
-          const bool ok = kok && rows_ok[j] && hh >= 0 && hh < o.H && ww >= 0 && ww < o.W;
-          reg[2 * j + e] = bload(rs, ok ? ((k + (kh - 1) * o.W + (kw - 1)) * o.C + col[j]) * 2 : OOB);
+          const int hh = h[e] + tkh[j] - 1, ww = w[e] + tkw[j] - 1;
+          const bool ok = kok && rows_ok[j] && static_cast<unsigned>(hh) < static_cast<unsigned>(o.H) &&
+                          static_cast<unsigned>(ww) < static_cast<unsigned>(o.W);
+          reg[2 * j + e] = bload(rs, ok ? kb + colb[j] : OOB);
         }
+        // advance this k by one K step (BK pixels) inside its image
+        w[e] += o.step_w;
+        const int cw = w[e] >= o.W;
+        w[e] -= cw ? o.W : 0;
+        h[e] += o.step_h + cw;
+        h[e] -= h[e] >= o.H ? o.H : 0;
       } else {  // OP_R_FILTER_T: filter [C2][9][C], k = tap * C2 + c2
-        const uint32_t kk = kok ? k : 0;
-        const uint32_t t = o.fdC2.div(kk);
-        const int c2 = kk - t * o.C2;
+        int t, c2;
+        if (TAPK) {
+          t = static_cast<int>(o.fdC2.div(k0));  // uniform
+          c2 = k0 - t * o.C2 + ek[e];
+        } else {
+          t = static_cast<int>(o.fdC2.div(kok ? k : 0));
+          c2 = k - t * o.C2;
+        }
+        const int kb = (c2 * 9 + t) * o.C * 2;
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          reg[2 * j + e] = bload(rs, (kok && rows_ok[j]) ? ((c2 * 9 + static_cast<int>(t)) * o.C + col[j]) * 2 : OOB);
+        for (int j = 0; j < 2; ++j) reg[2 * j + e] = bload(rs, (kok && rows_ok[j]) ? kb + colb[j] : OOB);
       }
     }
   }
@@ -202,17 +246,19 @@ struct RLoader {
       const int rbase = ((tid >> 5) + 8 * j) * 8;
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
-        const uint32_t lo = (r & 1) ? (a[r >> 1] >> 16) : (a[r >> 1] & 0xffffu);
-        const uint32_t hi = (r & 1) ? (b[r >> 1] >> 16) : (b[r >> 1] & 0xffffu);
-        *reinterpret_cast<uint32_t*>(lds + (rbase + r) * PITCH + kcol) = lo | (hi << 16);
+        // (row r of k, row r of k+1) as one 4-byte pair: low halves for even r, high for odd
+        const uint32_t pair = (r & 1) ? __builtin_amdgcn_perm(b[r >> 1], a[r >> 1], 0x07060302u)
+                                      : __builtin_amdgcn_perm(b[r >> 1], a[r >> 1], 0x05040100u);
+        *reinterpret_cast<uint32_t*>(lds + (rbase + r) * PITCH + kcol) = pair;
       }
     }
   }
 };
 
-template <int MODE>
+template <int MODE, bool TAPK>
 struct LoaderFor {
-  using type = typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE>, RLoader<MODE>>::type;
+  using type =
+      typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE, TAPK>, RLoader<MODE, TAPK>>::type;
 };
 
 // value = acc * alpha + bias + residuals, ReLU, then float32 and/or bf16 stores
@@ -235,7 +281,7 @@ __device__ __forceinline__ void epilogue(const EpiDev& e, long idx, int col, flo
   }
 }
 
-template <int MA, int MB>
+template <int MA, int MB, bool TAPK>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(KArgs args) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TILE_ELEMS];  // [buffer][A|B]
 
@@ -258,10 +304,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(KArgs args) {
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A.p, A.extent - aoff);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(B.p, B.extent - boff);
 
-  typename LoaderFor<MA>::type la;
-  typename LoaderFor<MB>::type lb;
-  la.init(A, row0, tid);
-  lb.init(B, col0, tid);
+  const int kbeg = split * args.k_per_split;
+  const int kend = min(args.K, kbeg + args.k_per_split);
+  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+
+  typename LoaderFor<MA, TAPK>::type la;
+  typename LoaderFor<MB, TAPK>::type lb;
+  la.init(A, row0, tid, kbeg);
+  lb.init(B, col0, tid, kbeg);
 
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
@@ -273,10 +323,6 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(KArgs args) {
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  const int kbeg = split * args.k_per_split;
-  const int kend = min(args.K, kbeg + args.k_per_split);
-  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
   auto compute = [&](const bf16_t* sa, const bf16_t* sb) {
 #pragma unroll
@@ -301,33 +347,29 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(KArgs args) {
 
   if (nk > 0) {
     uint4 ra0[4], rb0[4], ra1[4], rb1[4];
-    la.load(A, ra, kbeg, tid, ra0);
-    lb.load(B, rb, kbeg, tid, rb0);
-    if (nk > 1) {
-      la.load(A, ra, kbeg + BK, tid, ra1);
-      lb.load(B, rb, kbeg + BK, tid, rb1);
-    }
+    // Prefetch loads are issued unconditionally (a step past the end reads
+    // zeros or data that is never stored), so the compiler can count the
+    // outstanding loads exactly and wait only for the older register set.
+    la.load(A, ra, kbeg, ra0);
+    lb.load(B, rb, kbeg, rb0);
+    la.load(A, ra, kbeg + BK, ra1);
+    lb.load(B, rb, kbeg + BK, rb1);
     la.store(lds[0][0], ra0, tid);
     lb.store(lds[0][1], rb0, tid);
     __syncthreads();
-    // registers of set 0 / 1 hold K steps of even / odd index; LDS buffer b
-    // holds the step being multiplied
-    for (int kt = 0; kt < nk; kt += 2) {
-      if (kt + 2 < nk) {
-        la.load(A, ra, kbeg + (kt + 2) * BK, tid, ra0);
-        lb.load(B, rb, kbeg + (kt + 2) * BK, tid, rb0);
-      }
+    // Register sets 0 / 1 hold K steps of even / odd index; LDS buffer b holds
+    // the step being multiplied. The loop body covers a pair of steps and has
+    // no exit in the middle, so the accumulators keep one register home.
+    int kt = 0;
+    for (; kt + 2 <= nk; kt += 2) {
+      la.load(A, ra, kbeg + (kt + 2) * BK, ra0);
+      lb.load(B, rb, kbeg + (kt + 2) * BK, rb0);
       compute(lds[0][0], lds[0][1]);
-      if (kt + 1 < nk) {
-        la.store(lds[1][0], ra1, tid);
-        lb.store(lds[1][1], rb1, tid);
-      }
+      la.store(lds[1][0], ra1, tid);
+      lb.store(lds[1][1], rb1, tid);
       __syncthreads();
-      if (kt + 1 >= nk) break;
-      if (kt + 3 < nk) {
-        la.load(A, ra, kbeg + (kt + 3) * BK, tid, ra1);
-        lb.load(B, rb, kbeg + (kt + 3) * BK, tid, rb1);
-      }
+      la.load(A, ra, kbeg + (kt + 3) * BK, ra1);
+      lb.load(B, rb, kbeg + (kt + 3) * BK, rb1);
       compute(lds[1][0], lds[1][1]);
       if (kt + 2 < nk) {
         la.store(lds[0][0], ra0, tid);
@@ -335,6 +377,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(KArgs args) {
       }
       __syncthreads();
     }
+    if (kt < nk) compute(lds[0][0], lds[0][1]);   // odd step count: the last step is in buffer 0
   }
 
   // Lane holds column (lane % 32) and rows 8*(r/4) + 4*(lane/32) + r%4 of each
@@ -414,6 +457,12 @@ OperandDev make_operand(const Operand& o, int rows, int K, long extent) {
   d.W = o.g.W;
   d.C = o.g.C;
   d.C2 = o.g.C2;
+  const int hw = o.g.H * o.g.W;
+  if (hw > 0) {
+    const int rem = BK % hw;
+    d.step_h = rem / o.g.W;
+    d.step_w = rem % o.g.W;
+  }
   d.fdC = FastDiv(o.g.C > 0 ? o.g.C : 1);
   d.fdC2 = FastDiv(o.g.C2 > 0 ? o.g.C2 : 1);
   d.fdHW = FastDiv(o.g.H * o.g.W > 0 ? o.g.H * o.g.W : 1);
@@ -421,10 +470,10 @@ OperandDev make_operand(const Operand& o, int rows, int K, long extent) {
   return d;
 }
 
-template <int MA, int MB>
+template <int MA, int MB, bool TAPK = false>
 hipError_t launch(const KArgs& a, hipStream_t s) {
   dim3 grid(a.tiles_total, a.batch * a.splits);
-  hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB>), grid, dim3(NT), 0, s, a);
+  hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK>), grid, dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
@@ -484,8 +533,11 @@ hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s) {
   if (ma == OP_K_PLAIN && mb == OP_K_PLAIN) err = launch<OP_K_PLAIN, OP_K_PLAIN>(a, s);
   else if (ma == OP_K_PLAIN && mb == OP_R_PLAIN) err = launch<OP_K_PLAIN, OP_R_PLAIN>(a, s);
   else if (ma == OP_R_PLAIN && mb == OP_R_PLAIN) err = launch<OP_R_PLAIN, OP_R_PLAIN>(a, s);
-  else if (ma == OP_K_CONV_FWD && mb == OP_K_PLAIN) err = launch<OP_K_CONV_FWD, OP_K_PLAIN>(a, s);
-  else if (ma == OP_K_CONV_DGRAD && mb == OP_R_FILTER_T) err = launch<OP_K_CONV_DGRAD, OP_R_FILTER_T>(a, s);
+  else if (ma == OP_K_CONV_FWD && mb == OP_K_PLAIN)
+    err = (d.A.g.C % BK == 0) ? launch<OP_K_CONV_FWD, OP_K_PLAIN, true>(a, s) : launch<OP_K_CONV_FWD, OP_K_PLAIN>(a, s);
+  else if (ma == OP_K_CONV_DGRAD && mb == OP_R_FILTER_T)
+    err = (d.A.g.C % BK == 0 && d.B.g.C2 % BK == 0) ? launch<OP_K_CONV_DGRAD, OP_R_FILTER_T, true>(a, s)
+                                                   : launch<OP_K_CONV_DGRAD, OP_R_FILTER_T>(a, s);
   else if (ma == OP_R_PLAIN && mb == OP_R_CONV_WGRAD) err = launch<OP_R_PLAIN, OP_R_CONV_WGRAD>(a, s);
   else return hipErrorInvalidValue;
   if (err != hipSuccess || splits == 1) return err;
