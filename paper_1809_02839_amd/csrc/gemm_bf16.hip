@@ -282,7 +282,7 @@ __device__ __forceinline__ void epilogue(const EpiDev& e, long idx, int col, flo
 }
 
 template <int MA, int MB, bool TAPK>
-__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(KArgs args) {
+__global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TILE_ELEMS];  // [buffer][A|B]
 
   const int tid = threadIdx.x;
@@ -494,12 +494,14 @@ hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s) {
   a.zdiv = zdiv;
   a.tiles_n = (d.N + BN - 1) / BN;
   a.tiles_total = a.tiles_n * ((d.M + BM - 1) / BM);
-  // split K when the tiles cannot fill the chip and K is long: each split
-  // keeps at least 8 K steps
+  // Split K when the tiles cannot give every CU two resident blocks (two
+  // 4-wave blocks per CU hide each other's barrier and load stalls) and K is
+  // long: each split keeps at least 8 K steps.
+  constexpr long kTargetBlocks = 2 * 256;
   int splits = 1;
   const long tiles = static_cast<long>(a.tiles_total) * d.batch;
-  if (d.workspace && tiles < 256 && d.K >= 2 * 8 * BK) {
-    splits = static_cast<int>((256 + tiles - 1) / tiles);
+  if (d.workspace && tiles < kTargetBlocks && d.K >= 2 * 8 * BK) {
+    splits = static_cast<int>((kTargetBlocks + tiles - 1) / tiles);
     splits = std::min(splits, d.K / (8 * BK));
     splits = std::min(splits, 16);
     const long per = static_cast<long>(d.batch) * d.M * d.N * 4;
