@@ -56,8 +56,38 @@ __global__ void mask_f32_kernel(const float* src, const float* mask, float* dst,
 }
 
 // --------------------------------------------------------- column sums ----
-// Pass 1: block (cb, rb) sums rows [rb*RCH, (rb+1)*RCH) of 64 columns.
+// Pass 1: block (cb, rb) sums rows [rb*RCH, (rb+1)*RCH) of its columns into
+// partial[rb][col]. bf16 inputs with cols % 8 == 0 use 16-byte loads: 32
+// column groups of 8 x 8 row lanes; otherwise 64 columns x 4 row lanes.
 constexpr int RCH = 256;
+__global__ void colsum_partial_bf16x8_kernel(const bf16_t* X, long rows, int cols, long ld, float* partial) {
+  __shared__ float sh[8][256];
+  const int cg = threadIdx.x & 31, rl = threadIdx.x >> 5;
+  const int col = blockIdx.x * 256 + cg * 8;
+  const long r0 = static_cast<long>(blockIdx.y) * RCH;
+  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (col < cols) {
+    for (long r = r0 + rl; r < r0 + RCH && r < rows; r += 8) {
+      const uint4 v = *reinterpret_cast<const uint4*>(X + r * ld + col);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[2 * q] += __uint_as_float(w[q] << 16);
+        acc[2 * q + 1] += __uint_as_float(w[q] & 0xffff0000u);
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) sh[rl][cg * 8 + q] = acc[q];
+  __syncthreads();
+  const int c = threadIdx.x;   // 256 columns of this block
+  if (blockIdx.x * 256 + c < cols) {
+    float t = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) t += sh[q][c];
+    partial[static_cast<long>(blockIdx.y) * cols + blockIdx.x * 256 + c] = t;
+  }
+}
 template <typename T>
 __global__ void colsum_partial_kernel(const T* X, long rows, int cols, long ld, float* partial) {
   __shared__ float sh[4][64];
@@ -75,19 +105,23 @@ __global__ void colsum_partial_kernel(const T* X, long rows, int cols, long ld, 
   __syncthreads();
   if (ty == 0 && col < cols) partial[static_cast<long>(blockIdx.y) * cols + col] = (sh[0][tx] + sh[1][tx]) + (sh[2][tx] + sh[3][tx]);
 }
-// Pass 2: 64 columns per block; the four waves split the chunks (chunk c goes
-// to wave c % 4), then the four wave sums are added in a fixed order.
-__global__ void colsum_final_kernel(const float* partial, int nchunks, int cols, float* out, int accumulate) {
-  __shared__ float sh[4][64];
+// Pass 2: 64 columns per block of 16 waves; chunk c goes to wave c % 16, and
+// the 16 wave sums are added in a fixed order.
+constexpr int FIN_WAVES = 16;
+__global__ __launch_bounds__(64 * FIN_WAVES) void colsum_final_kernel(const float* partial, int nchunks, int cols,
+                                                                      float* out, int accumulate) {
+  __shared__ float sh[FIN_WAVES][64];
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   const int col = blockIdx.x * 64 + tx;
   float s = 0.0f;
   if (col < cols)
-    for (int c = ty; c < nchunks; c += 4) s += partial[static_cast<long>(c) * cols + col];
+    for (int c = ty; c < nchunks; c += FIN_WAVES) s += partial[static_cast<long>(c) * cols + col];
   sh[ty][tx] = s;
   __syncthreads();
   if (ty == 0 && col < cols) {
-    const float v = (sh[0][tx] + sh[1][tx]) + (sh[2][tx] + sh[3][tx]);
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < FIN_WAVES; ++w) v += sh[w][tx];
     out[col] = accumulate ? out[col] + v : v;
   }
 }
@@ -126,100 +160,118 @@ __global__ __launch_bounds__(NT) void mean_kernel(const float* x, int n, float* 
 }
 
 // ---------------------------------------------------------- layer norm ----
-// One wave per row; D is a multiple of 64 up to 64 * 32.
-constexpr int LN_MAXV = 32;
+// One wave per row; lane l owns the VPL = D/64 consecutive columns
+// [l*VPL, (l+1)*VPL), read and written with the widest aligned accesses.
+template <int VPL>
+__device__ __forceinline__ void ld_row(const bf16_t* p, float (&v)[VPL]) {
+  if constexpr (VPL % 8 == 0) {
+#pragma unroll
+    for (int q = 0; q < VPL / 8; ++q) {
+      const uint4 u = reinterpret_cast<const uint4*>(p)[q];
+      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        v[q * 8 + 2 * t] = __uint_as_float(w[t] << 16);
+        v[q * 8 + 2 * t + 1] = __uint_as_float(w[t] & 0xffff0000u);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) v[j] = bf16_to_f32(p[j]);
+  }
+}
+template <int VPL>
+__device__ __forceinline__ void st_row(bf16_t* p, const float (&v)[VPL]) {
+  if constexpr (VPL % 8 == 0) {
+#pragma unroll
+    for (int q = 0; q < VPL / 8; ++q) {
+      uint4 u;
+      u.x = f32_to_bf16(v[q * 8 + 0]) | (static_cast<uint32_t>(f32_to_bf16(v[q * 8 + 1])) << 16);
+      u.y = f32_to_bf16(v[q * 8 + 2]) | (static_cast<uint32_t>(f32_to_bf16(v[q * 8 + 3])) << 16);
+      u.z = f32_to_bf16(v[q * 8 + 4]) | (static_cast<uint32_t>(f32_to_bf16(v[q * 8 + 5])) << 16);
+      u.w = f32_to_bf16(v[q * 8 + 6]) | (static_cast<uint32_t>(f32_to_bf16(v[q * 8 + 7])) << 16);
+      reinterpret_cast<uint4*>(p)[q] = u;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) p[j] = f32_to_bf16(v[j]);
+  }
+}
+
+template <int VPL>
 __global__ __launch_bounds__(NT) void layernorm_fwd_kernel(const bf16_t* r, const bf16_t* gamma, const bf16_t* beta,
                                                            int R, int D, float eps, bf16_t* y, float* mean,
                                                            float* rstd) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= R) return;
-  const bf16_t* x = r + static_cast<long>(row) * D;
-  const int per = D / 64;
-  float v[LN_MAXV];
+  const long base = static_cast<long>(row) * D + lane * VPL;
+  float v[VPL], g[VPL], b[VPL];
+  ld_row<VPL>(r + base, v);
+  ld_row<VPL>(gamma + lane * VPL, g);
+  ld_row<VPL>(beta + lane * VPL, b);
   float s = 0.0f;
 #pragma unroll
-  for (int j = 0; j < LN_MAXV; ++j)
-    if (j < per) {
-      v[j] = bf16_to_f32(x[j * 64 + lane]);
-      s += v[j];
-    }
+  for (int j = 0; j < VPL; ++j) s += v[j];
   const float mu = wave_sum(s) / static_cast<float>(D);
   float q = 0.0f;
 #pragma unroll
-  for (int j = 0; j < LN_MAXV; ++j)
-    if (j < per) {
-      const float d = v[j] - mu;
-      q += d * d;
-    }
+  for (int j = 0; j < VPL; ++j) q += (v[j] - mu) * (v[j] - mu);
   const float rs = rsqrtf(wave_sum(q) / static_cast<float>(D) + eps);
 #pragma unroll
-  for (int j = 0; j < LN_MAXV; ++j)
-    if (j < per) {
-      const int c = j * 64 + lane;
-      y[static_cast<long>(row) * D + c] = f32_to_bf16(bf16_to_f32(gamma[c]) * ((v[j] - mu) * rs) + bf16_to_f32(beta[c]));
-    }
+  for (int j = 0; j < VPL; ++j) v[j] = g[j] * ((v[j] - mu) * rs) + b[j];
+  st_row<VPL>(y + base, v);
   if (lane == 0) {
     mean[row] = mu;
     rstd[row] = rs;
   }
 }
 
-// Rows per block in the backward; partial dgamma/dbeta per block.
+// Rows per block in the backward; per-block partial dgamma/dbeta.
 constexpr int LNB_ROWS = 32;
+template <int VPL>
 __global__ __launch_bounds__(NT) void layernorm_bwd_kernel(const bf16_t* dy, const bf16_t* r, const float* mean,
                                                            const float* rstd, const bf16_t* gamma, int R, int D,
                                                            bf16_t* dr, float* part_g, float* part_b) {
-  __shared__ float shg[4][64 * 8];
-  __shared__ float shb[4][64 * 8];
+  __shared__ float shg[4][64 * VPL];
+  __shared__ float shb[4][64 * VPL];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int per = D / 64;
-  float pg[LN_MAXV], pb[LN_MAXV];
+  float gm[VPL], pg[VPL], pb[VPL];
+  ld_row<VPL>(gamma + lane * VPL, gm);
 #pragma unroll
-  for (int j = 0; j < LN_MAXV; ++j) pg[j] = pb[j] = 0.0f;
+  for (int j = 0; j < VPL; ++j) pg[j] = pb[j] = 0.0f;
   for (int rr = w; rr < LNB_ROWS; rr += 4) {
     const int row = blockIdx.x * LNB_ROWS + rr;
     if (row >= R) break;
-    const long base = static_cast<long>(row) * D;
+    const long base = static_cast<long>(row) * D + lane * VPL;
     const float mu = mean[row], rs = rstd[row];
-    float xh[LN_MAXV], g[LN_MAXV];
+    float d[VPL], xh[VPL];
+    ld_row<VPL>(dy + base, d);
+    ld_row<VPL>(r + base, xh);
     float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
-    for (int j = 0; j < LN_MAXV; ++j)
-      if (j < per) {
-        const int c = j * 64 + lane;
-        const float d = bf16_to_f32(dy[base + c]);
-        xh[j] = (bf16_to_f32(r[base + c]) - mu) * rs;
-        g[j] = d * bf16_to_f32(gamma[c]);
-        s1 += g[j];
-        s2 += g[j] * xh[j];
-        pg[j] += d * xh[j];
-        pb[j] += d;
-      }
+    for (int j = 0; j < VPL; ++j) {
+      xh[j] = (xh[j] - mu) * rs;
+      pg[j] += d[j] * xh[j];
+      pb[j] += d[j];
+      d[j] *= gm[j];          // dy * gamma
+      s1 += d[j];
+      s2 += d[j] * xh[j];
+    }
     const float m1 = wave_sum(s1) / static_cast<float>(D), m2 = wave_sum(s2) / static_cast<float>(D);
 #pragma unroll
-    for (int j = 0; j < LN_MAXV; ++j)
-      if (j < per) dr[base + j * 64 + lane] = f32_to_bf16(rs * (g[j] - m1 - xh[j] * m2));
+    for (int j = 0; j < VPL; ++j) d[j] = rs * (d[j] - m1 - xh[j] * m2);
+    st_row<VPL>(dr + base, d);
   }
-  // combine the four waves in a fixed order, 8 column groups of 64 at a time
 #pragma unroll
-  for (int j0 = 0; j0 < LN_MAXV; j0 += 8) {
-    if (j0 >= per) break;  // uniform across the block
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (j0 + j < per) {
-        shg[w][j * 64 + lane] = pg[j0 + j];
-        shb[w][j * 64 + lane] = pb[j0 + j];
-      }
-    __syncthreads();
-    for (int i = threadIdx.x; i < 8 * 64; i += NT) {
-      const int c = j0 * 64 + i;
-      if (c < D) {
-        part_g[static_cast<long>(blockIdx.x) * D + c] = (shg[0][i] + shg[1][i]) + (shg[2][i] + shg[3][i]);
-        part_b[static_cast<long>(blockIdx.x) * D + c] = (shb[0][i] + shb[1][i]) + (shb[2][i] + shb[3][i]);
-      }
-    }
-    __syncthreads();
+  for (int j = 0; j < VPL; ++j) {
+    shg[w][lane * VPL + j] = pg[j];
+    shb[w][lane * VPL + j] = pb[j];
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < D; c += NT) {
+    part_g[static_cast<long>(blockIdx.x) * D + c] = (shg[0][c] + shg[1][c]) + (shg[2][c] + shg[3][c]);
+    part_b[static_cast<long>(blockIdx.x) * D + c] = (shb[0][c] + shb[1][c]) + (shb[2][c] + shb[3][c]);
   }
 }
 
@@ -334,16 +386,19 @@ hipError_t column_sum(const void* X, int dtype, long rows, int cols, long ld, fl
   if (cols <= 0) return hipSuccess;
   const int nchunks = rows > 0 ? static_cast<int>((rows + RCH - 1) / RCH) : 0;
   if (nchunks > 0) {
-    dim3 grid((cols + 63) / 64, nchunks);
-    if (dtype == 1)
-      hipLaunchKernelGGL(colsum_partial_kernel<bf16_t>, grid, dim3(NT), 0, s, static_cast<const bf16_t*>(X), rows,
-                         cols, ld, partial_ws);
-    else
-      hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(NT), 0, s, static_cast<const float*>(X), rows,
-                         cols, ld, partial_ws);
+    if (dtype == 1 && cols % 8 == 0 && ld % 8 == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0) {
+      hipLaunchKernelGGL(colsum_partial_bf16x8_kernel, dim3((cols + 255) / 256, nchunks), dim3(NT), 0, s,
+                         static_cast<const bf16_t*>(X), rows, cols, ld, partial_ws);
+    } else if (dtype == 1) {
+      hipLaunchKernelGGL(colsum_partial_kernel<bf16_t>, dim3((cols + 63) / 64, nchunks), dim3(NT), 0, s,
+                         static_cast<const bf16_t*>(X), rows, cols, ld, partial_ws);
+    } else {
+      hipLaunchKernelGGL(colsum_partial_kernel<float>, dim3((cols + 63) / 64, nchunks), dim3(NT), 0, s,
+                         static_cast<const float*>(X), rows, cols, ld, partial_ws);
+    }
   }
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 63) / 64), dim3(NT), 0, s, partial_ws, nchunks, cols, out,
-                     accumulate);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 63) / 64), dim3(64 * FIN_WAVES), 0, s, partial_ws, nchunks,
+                     cols, out, accumulate);
   return hipGetLastError();
 }
 
@@ -360,21 +415,38 @@ hipError_t softmax_ce(const float* logits, const int32_t* labels, int R, int C, 
 
 hipError_t layernorm_fwd(const bf16_t* r, const bf16_t* gamma, const bf16_t* beta, int R, int D, float eps, bf16_t* y,
                          float* mean, float* rstd, hipStream_t s) {
-  if (D % 64 || D > 64 * LN_MAXV) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(layernorm_fwd_kernel, dim3((R + 3) / 4), dim3(NT), 0, s, r, gamma, beta, R, D, eps, y, mean,
-                     rstd);
+  if (D % 64 || D > 64 * 32) return hipErrorInvalidValue;
+  const dim3 grid((R + 3) / 4), block(NT);
+  switch (D / 64) {
+    case 1: hipLaunchKernelGGL(layernorm_fwd_kernel<1>, grid, block, 0, s, r, gamma, beta, R, D, eps, y, mean, rstd); break;
+    case 2: hipLaunchKernelGGL(layernorm_fwd_kernel<2>, grid, block, 0, s, r, gamma, beta, R, D, eps, y, mean, rstd); break;
+    case 4: hipLaunchKernelGGL(layernorm_fwd_kernel<4>, grid, block, 0, s, r, gamma, beta, R, D, eps, y, mean, rstd); break;
+    case 8: hipLaunchKernelGGL(layernorm_fwd_kernel<8>, grid, block, 0, s, r, gamma, beta, R, D, eps, y, mean, rstd); break;
+    case 16: hipLaunchKernelGGL(layernorm_fwd_kernel<16>, grid, block, 0, s, r, gamma, beta, R, D, eps, y, mean, rstd); break;
+    case 32: hipLaunchKernelGGL(layernorm_fwd_kernel<32>, grid, block, 0, s, r, gamma, beta, R, D, eps, y, mean, rstd); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd, const bf16_t* gamma,
                          int R, int D, bf16_t* dr, float* dgamma, float* dbeta, float* partial_ws, hipStream_t s) {
-  if (D % 64 || D > 64 * LN_MAXV) return hipErrorInvalidValue;
+  if (D % 64 || D > 64 * 32) return hipErrorInvalidValue;
   const int nb = (R + LNB_ROWS - 1) / LNB_ROWS;
   float* pg = partial_ws;
   float* pb = partial_ws + static_cast<long>(nb) * D;
-  hipLaunchKernelGGL(layernorm_bwd_kernel, dim3(nb), dim3(NT), 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb);
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 63) / 64), dim3(NT), 0, s, pg, nb, D, dgamma, 0);
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 63) / 64), dim3(NT), 0, s, pb, nb, D, dbeta, 0);
+  const dim3 grid(nb), block(NT);
+  switch (D / 64) {
+    case 1: hipLaunchKernelGGL(layernorm_bwd_kernel<1>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
+    case 2: hipLaunchKernelGGL(layernorm_bwd_kernel<2>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
+    case 4: hipLaunchKernelGGL(layernorm_bwd_kernel<4>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
+    case 8: hipLaunchKernelGGL(layernorm_bwd_kernel<8>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
+    case 16: hipLaunchKernelGGL(layernorm_bwd_kernel<16>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
+    case 32: hipLaunchKernelGGL(layernorm_bwd_kernel<32>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 63) / 64), dim3(64 * FIN_WAVES), 0, s, pg, nb, D, dgamma, 0);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 63) / 64), dim3(64 * FIN_WAVES), 0, s, pb, nb, D, dbeta, 0);
   return hipGetLastError();
 }
 

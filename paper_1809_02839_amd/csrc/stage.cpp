@@ -340,7 +340,8 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
       need(4);
       if (!dt_) fail("transformer stages run in bf16 only");
       if (dm[0] % dm[1]) fail("d_model must be divisible by heads");
-      if (dm[0] % 64 || dm[0] > 2048) fail("d_model must be a multiple of 64 up to 2048");
+      if (dm[0] % 64 || dm[0] > 2048 || ((dm[0] / 64) & (dm[0] / 64 - 1)))
+        fail("d_model must be 64 times a power of two, up to 2048");
       mult8(dm[0] / dm[1], "head dimension");
       mult8(dm[2], "ffn");
       mult8(dm[3], "seq");

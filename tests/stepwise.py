@@ -10,9 +10,10 @@ full pipeline a stage's input and upstream gradient are the GPU's neighbouring
 outputs. Every task is thus compared against an exact recomputation of the
 same step, with no divergence carried from earlier steps.
 
-With derived=True (the full-size runs) the gradient quantities (v, the step's
-weight change, dX) are also recomputed without any bf16 rounding and the GPU
-is held to the accuracy the oracle's own bf16 emulation reaches:
+With derived=True (every bf16 run) the gradient quantities (v, the step's
+weight change, dX) pass when they are within tol of the oracle's bf16
+emulation, or else when the GPU is as accurate as that emulation: they are
+also recomputed without any bf16 rounding and
     rel(gpu, exact) <= max(tol, 1.5 * rel(oracle_bf16, exact)).
 Over many layers the two bf16 computations take different ReLU decisions on
 activations within bf16 noise of zero, and each such decision moves a whole
@@ -89,6 +90,9 @@ def run_stepwise(wl, steps, torch, derived=False):
                         pairs.append(("dx", dx_gpu[(k, m)], dx, dxe))
                     for key, a, b, e in pairs:
                         worst.note(key, a, b)
+                        if rel(a, b) <= tol:
+                            worst.note(key + " vs exact", a, e)
+                            continue
                         bound = max(tol, 1.5 * rel(b, e))
                         worst.check(key + " vs exact", a, e, bound, f"k{k} u{u} (oracle bf16 vs exact {rel(b, e):.2e})")
                 else:

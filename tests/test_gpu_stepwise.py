@@ -19,7 +19,7 @@ torch = pytest.importorskip("torch")
 def test_stepwise_small(name):
     wl = synth.ALL_WORKLOADS[name]
     print(f"[stepwise] {name}", flush=True)
-    worst = run_stepwise(wl, wl.steps, torch)
+    worst = run_stepwise(wl, wl.steps, torch, derived=wl.stages[0].dtype == "bf16")
     print(f"[stepwise] {name}: {worst.report()}", flush=True)
 
 
