@@ -4,10 +4,11 @@
 // gradient) and the batched products inside attention.
 //
 // Block tile 128 x 128, K step 64, 256 threads = 4 waves in a 2 x 2 grid, each
-// wave owning a 64 x 64 sub-tile (2 x 2 MFMA tiles of 32 x 32). Operand tiles
-// are staged in LDS as [row][k] with k contiguous (8 consecutive k per lane
-// make one 16-byte MFMA operand read); the 144-byte row pitch puts eight
-// consecutive rows on disjoint banks. Global loads run two K steps ahead of
+// wave owning a 64 x 64 sub-tile (2 x 2 MFMA tiles of 32 x 32). K-mode operand
+// tiles are staged in LDS as [row][k] (8 consecutive k per lane make one
+// 16-byte MFMA operand read; the 144-byte row pitch puts eight consecutive
+// rows on disjoint banks); R-mode tiles (rows contiguous in memory) are staged
+// as [k][row] as loaded and transposed by the LDS reads. Global loads run two K steps ahead of
 // the MFMAs (two register stages, two LDS buffers). All global reads are
 // buffer loads whose resource spans exactly the operand tensor: an offset
 // outside it (zero padding of convolutions, ragged tile edges) reads zero.
@@ -23,12 +24,39 @@ namespace spx {
 namespace {
 
 constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
-constexpr int PITCH = BK + 8;            // bf16 elements per LDS row (144 bytes)
-constexpr int TILE_ELEMS = 128 * PITCH;  // one operand tile
+constexpr int PITCH = BK + 8;            // K-mode tile [row][k]: bf16 per row (144 bytes)
+constexpr int RPITCH = 128 + 16;         // R-mode tile [k][row]: bf16 per k row (288 bytes)
+constexpr int TILE_ELEMS = 128 * PITCH;  // one operand tile (= BK * RPITCH)
+static_assert(TILE_ELEMS == BK * RPITCH, "both tile layouts occupy the same LDS");
 constexpr int BUF_FLAGS = 0x00020000;    // gfx9 raw buffer resource word 3
 constexpr int OOB = 0x7ffffff0;          // byte offset past every resource: the load returns 0
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+
+// MFMA operand (8 consecutive k of one row) from a K-mode tile [row][PITCH].
+__device__ __forceinline__ bf16x8_t frag_k(const bf16_t* s, int row, int k) {
+  return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u16x8_t*>(s + row * PITCH + k));
+}
+
+// The same operand from an R-mode tile [k][RPITCH] with two transposing LDS
+// reads (ds_read_b64_tr_b16). Within each group of 16 lanes, lane i receives
+// element i % 4 of the 8-byte chunk addressed by lane 4 q + i / 4, for q < 4.
+// Lane (group g, index i) therefore addresses k row k0 + 8 (g / 2) + i / 4 at
+// rows m0 + 16 (g % 2) + 4 (i % 4): it receives rows m0 + 16 (g % 2) + i and
+// k0 + 8 (g / 2) + q, which is the MFMA operand layout (row lane % 32, k half
+// lane / 32). The second read takes the next four k.
+__device__ __forceinline__ bf16x8_t frag_r(const bf16_t* s, int m0, int k0, int lane) {
+  const int g = lane >> 4, i = lane & 15;
+  const bf16_t* p = s + (k0 + 8 * (g >> 1) + (i >> 2)) * RPITCH + m0 + 16 * (g & 1) + 4 * (i & 3);
+  const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p));
+  const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p + 4 * RPITCH));
+  const u16x8_t v = {static_cast<uint16_t>(lo[0]), static_cast<uint16_t>(lo[1]), static_cast<uint16_t>(lo[2]),
+                     static_cast<uint16_t>(lo[3]), static_cast<uint16_t>(hi[0]), static_cast<uint16_t>(hi[1]),
+                     static_cast<uint16_t>(hi[2]), static_cast<uint16_t>(hi[3])};
+  return __builtin_bit_cast(bf16x8_t, v);
+}
 
 struct OperandDev {
   const bf16_t* p;
@@ -154,104 +182,85 @@ struct KLoader {
 };
 
 // ---- R-mode: 8 consecutive rows of one k ----------------------------------
-// Thread t loads k = k0 + 2 (t % 32) + e (e < 2) for row groups t / 32 and
-// t / 32 + 8 (rows 8 g .. 8 g + 7), then writes 4-byte (k, k+1) pairs per row.
+// The tile is kept in LDS as [k][row] (rows contiguous, RPITCH elements per k)
+// exactly as loaded, and the MFMA operand reads transpose it (see frag_r).
+// Thread t loads row group t % 16 (rows 8 (t % 16) .. + 7) at
+// k = k0 + t / 16 + 16 i (i < 4): sixteen lanes cover one k row of the tile.
 // Loads must be issued for consecutive K steps (the filter-gradient gather
 // advances its pixel coordinates by BK per call).
 template <int MODE, bool TAPK>
 struct RLoader {
-  int rows_ok[2];
-  int colb[2];   // per row group: byte offset of the first row (PLAIN), channel + tap shift (WGRAD), channel (FILTER_T)
-  int tkh[2], tkw[2];
-  int ek[2];     // 2 (t % 32) + e
-  int h[2], w[2];
+  int rows_ok;
+  int colb;      // byte offset of the row group (PLAIN, FILTER_T) or of its channel + tap shift (WGRAD)
+  int tkh, tkw;  // WGRAD: filter tap of the row group
+  int kk0;       // t / 16
+  int h[4], w[4];
 
   __device__ void init(const OperandDev& o, int row0, int tid, int k0) {
-#pragma unroll
-    for (int e = 0; e < 2; ++e) ek[e] = 2 * (tid & 31) + e;
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int r = row0 + ((tid >> 5) + 8 * j) * 8;
-      rows_ok[j] = r < o.rows;  // rows are a multiple of 8
-      const uint32_t rr = rows_ok[j] ? r : 0;
-      if (MODE == OP_R_CONV_WGRAD) {
-        const int tap = static_cast<int>(o.fdC.div(rr));
-        tkh[j] = (tap * 11) >> 5;
-        tkw[j] = tap - 3 * tkh[j];
-        colb[j] = (((tkh[j] - 1) * o.W + (tkw[j] - 1)) * o.C + static_cast<int>(rr) - tap * o.C) * 2;
-      } else if (MODE == OP_R_PLAIN) {
-        colb[j] = static_cast<int>(rr) * 2;
-      } else {
-        colb[j] = static_cast<int>(rr) * 2;
-      }
-    }
+    kk0 = tid >> 4;
+    const int r = row0 + (tid & 15) * 8;
+    rows_ok = r < o.rows;  // rows are a multiple of 8
+    const uint32_t rr = rows_ok ? r : 0;
+    tkh = tkw = 0;
     if (MODE == OP_R_CONV_WGRAD) {
+      const int tap = static_cast<int>(o.fdC.div(rr));
+      tkh = (tap * 11) >> 5;
+      tkw = tap - 3 * tkh;
+      colb = (((tkh - 1) * o.W + (tkw - 1)) * o.C + static_cast<int>(rr) - tap * o.C) * 2;
 #pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const uint32_t kk = k0 + ek[e];
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t kk = k0 + kk0 + 16 * i;
         const uint32_t b = o.fdHW.div(kk);
         const uint32_t rem = kk - b * static_cast<uint32_t>(o.H * o.W);
-        h[e] = o.fdW.div(rem);
-        w[e] = rem - h[e] * o.W;
+        h[i] = o.fdW.div(rem);
+        w[i] = rem - h[i] * o.W;
       }
+    } else {
+      colb = static_cast<int>(rr) * 2;
     }
   }
 
   __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, uint4 (&reg)[4]) {
+    int t0 = 0, c0 = 0;
+    if (MODE == OP_R_FILTER_T && TAPK) {
+      t0 = static_cast<int>(o.fdC2.div(k0));  // uniform
+      c0 = k0 - t0 * o.C2;
+    }
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int k = k0 + ek[e];
-      const bool kok = k < o.K;
+    for (int i = 0; i < 4; ++i) {
+      const int k = k0 + kk0 + 16 * i;
+      const bool kok = rows_ok && k < o.K;
       if (MODE == OP_R_PLAIN) {
-        const int kb = static_cast<int>(k * o.ld * 2);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) reg[2 * j + e] = bload(rs, (kok && rows_ok[j]) ? kb + colb[j] : OOB);
+        reg[i] = bload(rs, kok ? static_cast<int>(k * o.ld * 2) + colb : OOB);
       } else if (MODE == OP_R_CONV_WGRAD) {
-        const int kb = k * o.C * 2;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int hh = h[e] + tkh[j] - 1, ww = w[e] + tkw[j] - 1;
-          const bool ok = kok && rows_ok[j] && static_cast<unsigned>(hh) < static_cast<unsigned>(o.H) &&
-                          static_cast<unsigned>(ww) < static_cast<unsigned>(o.W);
-          reg[2 * j + e] = bload(rs, ok ? kb + colb[j] : OOB);
-        }
+        const int hh = h[i] + tkh - 1, ww = w[i] + tkw - 1;
+        const bool ok = kok && static_cast<unsigned>(hh) < static_cast<unsigned>(o.H) &&
+                        static_cast<unsigned>(ww) < static_cast<unsigned>(o.W);
+        reg[i] = bload(rs, ok ? k * o.C * 2 + colb : OOB);
         // advance this k by one K step (BK pixels) inside its image
-        w[e] += o.step_w;
-        const int cw = w[e] >= o.W;
-        w[e] -= cw ? o.W : 0;
-        h[e] += o.step_h + cw;
-        h[e] -= h[e] >= o.H ? o.H : 0;
+        w[i] += o.step_w;
+        const int cw = w[i] >= o.W;
+        w[i] -= cw ? o.W : 0;
+        h[i] += o.step_h + cw;
+        h[i] -= h[i] >= o.H ? o.H : 0;
       } else {  // OP_R_FILTER_T: filter [C2][9][C], k = tap * C2 + c2
         int t, c2;
         if (TAPK) {
-          t = static_cast<int>(o.fdC2.div(k0));  // uniform
-          c2 = k0 - t * o.C2 + ek[e];
+          t = t0;
+          c2 = c0 + kk0 + 16 * i;
         } else {
-          t = static_cast<int>(o.fdC2.div(kok ? k : 0));
+          t = static_cast<int>(o.fdC2.div(k < o.K ? k : 0));
           c2 = k - t * o.C2;
         }
-        const int kb = (c2 * 9 + t) * o.C * 2;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) reg[2 * j + e] = bload(rs, (kok && rows_ok[j]) ? kb + colb[j] : OOB);
+        reg[i] = bload(rs, kok ? (c2 * 9 + t) * o.C * 2 + colb : OOB);
       }
     }
   }
 
   __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[4], int tid) const {
-    const int kcol = 2 * (tid & 31);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const uint32_t* a = reinterpret_cast<const uint32_t*>(&reg[2 * j]);
-      const uint32_t* b = reinterpret_cast<const uint32_t*>(&reg[2 * j + 1]);
-      const int rbase = ((tid >> 5) + 8 * j) * 8;
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        // (row r of k, row r of k+1) as one 4-byte pair: low halves for even r, high for odd
-        const uint32_t pair = (r & 1) ? __builtin_amdgcn_perm(b[r >> 1], a[r >> 1], 0x07060302u)
-                                      : __builtin_amdgcn_perm(b[r >> 1], a[r >> 1], 0x05040100u);
-        *reinterpret_cast<uint32_t*>(lds + (rbase + r) * PITCH + kcol) = pair;
-      }
-    }
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<uint4*>(lds + ((tid >> 4) + 16 * i) * RPITCH + (tid & 15) * 8) = reg[i];
   }
 };
 
@@ -331,12 +340,12 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
       const int kl = kk + (lane >> 5) * 8;
 #pragma unroll
       for (int i = 0; i < 2; ++i)
-        fa[i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u16x8_t*>(
-                                                 sa + (wm * 64 + i * 32 + (lane & 31)) * PITCH + kl));
+        fa[i] = (MA <= OP_K_CONV_DGRAD) ? frag_k(sa, wm * 64 + i * 32 + (lane & 31), kl)
+                                        : frag_r(sa, wm * 64 + i * 32, kk, lane);
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        fb[j] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u16x8_t*>(
-                                                 sb + (wn * 64 + j * 32 + (lane & 31)) * PITCH + kl));
+        fb[j] = (MB <= OP_K_CONV_DGRAD) ? frag_k(sb, wn * 64 + j * 32 + (lane & 31), kl)
+                                        : frag_r(sb, wn * 64 + j * 32, kk, lane);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
