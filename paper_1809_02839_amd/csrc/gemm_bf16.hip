@@ -538,12 +538,13 @@ hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s) {
   a.tiles_total = a.tiles_n * ((d.M + BM - 1) / BM);
   // Split K when the tiles cannot give every CU two resident blocks (two
   // 4-wave blocks per CU hide each other's barrier and load stalls) and K is
-  // long: each split keeps at least 8 K steps.
+  // long: as many splits as keep all blocks resident at once, each with at
+  // least 8 K steps.
   constexpr long kTargetBlocks = 2 * 256;
   int splits = 1;
   const long tiles = static_cast<long>(a.tiles_total) * d.batch;
   if (d.workspace && tiles < kTargetBlocks && d.K >= 2 * 8 * BK) {
-    splits = static_cast<int>((kTargetBlocks + tiles - 1) / tiles);
+    splits = static_cast<int>(kTargetBlocks / tiles);   // all blocks resident in one round
     splits = std::min(splits, d.K / (8 * BK));
     splits = std::min(splits, 16);
     const long per = static_cast<long>(d.batch) * d.M * d.N * 4;
