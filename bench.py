@@ -41,6 +41,32 @@ DESCRIPTIONS = {
 }
 
 
+# Kernel (rocprofv3 short name prefix) behind each launch family of the stage.
+FAMILY_KERNEL = {
+    "conv3x3_fwd": "gemm_bf16_kernel<1, 0",
+    "conv3x3_dgrad": "gemm_bf16_kernel<2, 5",
+    "conv3x3_wgrad": "gemm_bf16_kernel<3, 4",
+    "gemm_bf16_xwT": "gemm_bf16_kernel<0, 0",
+    "gemm_bf16_dyW": "gemm_bf16_kernel<0, 3",
+    "gemm_bf16_dyTx": "gemm_bf16_kernel<3, 3",
+    "splitk_reduce": "splitk_reduce",
+    "fused_update": "fused_update_kernel",
+}
+
+
+def traffic_per_launch(workload, family):
+    """HBM bytes per launch of the family's kernel from the committed counter
+    summary of this workload, or None when there is none or the kernel
+    sources changed since the counters were taken."""
+    from paper_1809_02839_amd import profiling
+    digest, table = profiling.read_traffic(os.path.join(ROOT, "profiles", f"stage_kernels_{workload}_hbm_traffic.md"))
+    prefix = FAMILY_KERNEL.get(family)
+    if digest is None or prefix is None or digest != profiling.source_digest():
+        return None
+    hits = [v for k, v in table.items() if k.startswith(prefix)]
+    return round(hits[0]) if len(hits) == 1 else None
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -139,7 +165,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="vgg_conv", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--profile-steps", type=int, default=20)
-    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--cpu-steps", type=int, default=8)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (a known-size reference "
@@ -162,9 +188,9 @@ def main():
         n = args.copy_calibration_mib << 18   # float32 elements
         src = torch.ones(n, device="cuda")
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.neg(src, out=dst)   # one elementwise kernel: n*4 bytes read, n*4 written
         torch.cuda.synchronize()
-        log(f"[bench] calibration copy: {n * 4} bytes read, {n * 4} bytes written")
+        log(f"[bench] calibration kernel (neg): {n * 4} bytes read, {n * 4} bytes written")
         del src, dst
     stream = torch.cuda.Stream()
     loop = StageLoop(spec, torch, native, stream)
@@ -208,6 +234,7 @@ def main():
         achieved = d["bytes_total"] / (d["ms_total"] / 1e3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None}
+    roof["traffic"] = traffic_per_launch(args.workload, dom)
     roof["kernel"] = dom
     roof["launches_per_step"] = d["launches"] / args.profile_steps
     roof["us_per_launch"] = round(d["ms_total"] / d["launches"] * 1e3, 2)

@@ -521,14 +521,22 @@ hipError_t launch(const KArgs& a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s) {
-  if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return hipSuccess;
+namespace {
+
+// Launch parameters of one GEMM: tile counts, the split of K and the device
+// view of both operands. Returns false (with err set) for a shape the kernel
+// cannot address; err stays hipSuccess for an empty problem.
+bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
+  err = hipSuccess;
+  if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return false;
   const int zdiv = d.zdiv > 0 ? d.zdiv : 1;
   const long ext_a = operand_extent(d.A, d.M, d.K, d.batch, zdiv);
   const long ext_b = operand_extent(d.B, d.N, d.K, d.batch, zdiv);
-  if (d.K <= 0 || ext_a <= 0 || ext_b <= 0 || ext_a >= (1L << 30) || ext_b >= (1L << 30))
-    return hipErrorInvalidValue;   // operands are addressed with 32-bit byte offsets
-  KArgs a{};
+  if (d.K <= 0 || ext_a <= 0 || ext_b <= 0 || ext_a >= (1L << 30) || ext_b >= (1L << 30)) {
+    err = hipErrorInvalidValue;   // operands are addressed with 32-bit byte offsets
+    return false;
+  }
+  a = KArgs{};
   a.M = d.M;
   a.N = d.N;
   a.K = d.K;
@@ -573,21 +581,27 @@ hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s) {
   a.e.alpha = d.epi.alpha;
   a.e.relu = d.epi.relu;
   a.e.accumulate = d.epi.accumulate;
+  return true;
+}
+
+hipError_t launch_main(const GemmDesc& d, const KArgs& a, hipStream_t s) {
   const int ma = d.A.mode, mb = d.B.mode;
-  hipError_t err;
-  if (ma == OP_K_PLAIN && mb == OP_K_PLAIN) err = launch<OP_K_PLAIN, OP_K_PLAIN>(a, s);
-  else if (ma == OP_K_PLAIN && mb == OP_R_PLAIN) err = launch<OP_K_PLAIN, OP_R_PLAIN>(a, s);
-  else if (ma == OP_R_PLAIN && mb == OP_R_PLAIN) err = launch<OP_R_PLAIN, OP_R_PLAIN>(a, s);
-  else if (ma == OP_K_CONV_FWD && mb == OP_K_PLAIN)
-    err = (d.A.g.C % BK == 0) ? launch<OP_K_CONV_FWD, OP_K_PLAIN, true>(a, s) : launch<OP_K_CONV_FWD, OP_K_PLAIN>(a, s);
-  else if (ma == OP_K_CONV_DGRAD && mb == OP_R_FILTER_T)
-    err = (d.A.g.C % BK == 0 && d.B.g.C2 % BK == 0) ? launch<OP_K_CONV_DGRAD, OP_R_FILTER_T, true>(a, s)
-                                                   : launch<OP_K_CONV_DGRAD, OP_R_FILTER_T>(a, s);
-  else if (ma == OP_R_PLAIN && mb == OP_R_CONV_WGRAD) err = launch<OP_R_PLAIN, OP_R_CONV_WGRAD>(a, s);
-  else return hipErrorInvalidValue;
-  if (err != hipSuccess || splits == 1) return err;
-  const long total = static_cast<long>(d.batch) * d.M * d.N;
-  if (d.N % 4 == 0) {
+  if (ma == OP_K_PLAIN && mb == OP_K_PLAIN) return launch<OP_K_PLAIN, OP_K_PLAIN>(a, s);
+  if (ma == OP_K_PLAIN && mb == OP_R_PLAIN) return launch<OP_K_PLAIN, OP_R_PLAIN>(a, s);
+  if (ma == OP_R_PLAIN && mb == OP_R_PLAIN) return launch<OP_R_PLAIN, OP_R_PLAIN>(a, s);
+  if (ma == OP_K_CONV_FWD && mb == OP_K_PLAIN)
+    return (d.A.g.C % BK == 0) ? launch<OP_K_CONV_FWD, OP_K_PLAIN, true>(a, s)
+                               : launch<OP_K_CONV_FWD, OP_K_PLAIN>(a, s);
+  if (ma == OP_K_CONV_DGRAD && mb == OP_R_FILTER_T)
+    return (d.A.g.C % BK == 0 && d.B.g.C2 % BK == 0) ? launch<OP_K_CONV_DGRAD, OP_R_FILTER_T, true>(a, s)
+                                                    : launch<OP_K_CONV_DGRAD, OP_R_FILTER_T>(a, s);
+  if (ma == OP_R_PLAIN && mb == OP_R_CONV_WGRAD) return launch<OP_R_PLAIN, OP_R_CONV_WGRAD>(a, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_reduce(const KArgs& a, hipStream_t s) {
+  const long total = static_cast<long>(a.batch) * a.M * a.N;
+  if (a.N % 4 == 0) {
     const long blocks = std::min<long>((total / 4 + 255) / 256, 8192);
     hipLaunchKernelGGL(splitk_reduce4_kernel, dim3(static_cast<int>(blocks)), dim3(256), 0, s, a);
   } else {
@@ -595,6 +609,26 @@ hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s) {
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3(static_cast<int>(blocks)), dim3(256), 0, s, a);
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+int gemm_bf16_splits(const GemmDesc& d) {
+  KArgs a;
+  hipError_t err;
+  return plan(d, a, err) ? a.splits : 1;
+}
+
+hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s, int phases) {
+  KArgs a;
+  hipError_t err;
+  if (!plan(d, a, err)) return err;
+  if (phases & GEMM_MAIN) {
+    err = launch_main(d, a, s);
+    if (err != hipSuccess) return err;
+  }
+  if ((phases & GEMM_REDUCE) && a.splits > 1) return launch_reduce(a, s);
+  return hipSuccess;
 }
 
 }  // namespace spx

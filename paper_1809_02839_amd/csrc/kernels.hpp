@@ -60,7 +60,12 @@ struct GemmDesc {
   Epilogue epi;
 };
 
-hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s);
+// bf16 GEMM in up to two launches: the tiled MFMA kernel (GEMM_MAIN) and,
+// when K is split across blocks, the ordered reduction of the float32
+// partials through the epilogue (GEMM_REDUCE).
+enum { GEMM_MAIN = 1, GEMM_REDUCE = 2, GEMM_ALL = 3 };
+hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s, int phases = GEMM_ALL);
+int gemm_bf16_splits(const GemmDesc& d);   // K splits the launch will use (1 = none)
 hipError_t gemm_f32(const GemmDesc& d, hipStream_t s);
 
 // ------------------------------------------------------- update/predict ----

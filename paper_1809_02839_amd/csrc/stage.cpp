@@ -163,7 +163,19 @@ void Stage::gemm(const GemmDesc& d) {
     dd.workspace = ws<float>(static_cast<int>(ws_off_.size()) - 1);
     dd.workspace_bytes = gemm_ws_bytes_;
   }
-  LAUNCH(name, flops, 0, dt_ ? gemm_bf16(dd, s_) : gemm_f32(dd, s_));
+  if (!dt_) {
+    LAUNCH(name, flops, 0, gemm_f32(dd, s_));
+    return;
+  }
+  LAUNCH(name, flops, 0, gemm_bf16(dd, s_, GEMM_MAIN));
+  const int splits = gemm_bf16_splits(dd);
+  if (splits > 1) {
+    // partials read once, output written once (read too when accumulating)
+    const double mn = static_cast<double>(d.M) * d.N * d.batch;
+    const double out = d.epi.out_f32 ? 4.0 : 2.0;
+    const double bytes = mn * (4.0 * splits + out * (d.epi.accumulate ? 2 : 1));
+    LAUNCH("splitk_reduce", 0, bytes, gemm_bf16(dd, s_, GEMM_REDUCE));
+  }
 }
 
 // ------------------------------------------------------------ profiling ----
