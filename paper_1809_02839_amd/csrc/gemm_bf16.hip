@@ -86,7 +86,8 @@ struct KArgs {
   int M, N, K, zdiv, tiles_n, tiles_total, batch, splits, k_per_split;
   OperandDev A, B;
   long a_bs1, a_bs2, b_bs1, b_bs2, c_bs1, c_bs2;
-  float* partial;   // splits > 1: [split][batch][M][N] float32
+  float* partial;        // splits > 1: [split][batch][M][N] float32
+  int vec_epi;           // output, bias, residual and mask allow the four-column epilogue
   EpiDev e;
 };
 
@@ -140,7 +141,7 @@ struct KLoader {
     const bool kok = k < o.K;
     if (MODE == OP_K_PLAIN) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) reg[i] = bload(rs, (row_ok[i] && kok) ? base[i] + k * 2 : OOB);
+      for (int i = 0; i < 4; ++i) reg[i] = bload(rs, (row_ok[i] & kok) ? base[i] + k * 2 : OOB);
     } else if (TAPK) {
       const int tap = static_cast<int>(o.fdC.div(k0));     // uniform
       const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
@@ -150,8 +151,8 @@ struct KLoader {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int hh = ph[i] + dh, ww = pw[i] + dw;
-        const bool ok = row_ok[i] && static_cast<unsigned>(hh) < static_cast<unsigned>(o.H) &&
-                        static_cast<unsigned>(ww) < static_cast<unsigned>(o.W);
+        const bool ok = row_ok[i] & (static_cast<unsigned>(hh) < static_cast<unsigned>(o.H)) &
+                        (static_cast<unsigned>(ww) < static_cast<unsigned>(o.W));
         reg[i] = bload(rs, ok ? base[i] + shift : OOB);
       }
     } else {
@@ -165,8 +166,8 @@ struct KLoader {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int hh = ph[i] + dh, ww = pw[i] + dw;
-        const bool ok = row_ok[i] && kok && static_cast<unsigned>(hh) < static_cast<unsigned>(o.H) &&
-                        static_cast<unsigned>(ww) < static_cast<unsigned>(o.W);
+        const bool ok = row_ok[i] & kok & (static_cast<unsigned>(hh) < static_cast<unsigned>(o.H)) &
+                        (static_cast<unsigned>(ww) < static_cast<unsigned>(o.W));
         reg[i] = bload(rs, ok ? base[i] + shift : OOB);
       }
     }
@@ -229,13 +230,13 @@ struct RLoader {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int k = k0 + kk0 + 16 * i;
-      const bool kok = rows_ok && k < o.K;
+      const bool kok = rows_ok & (k < o.K);
       if (MODE == OP_R_PLAIN) {
         reg[i] = bload(rs, kok ? static_cast<int>(k * o.ld * 2) + colb : OOB);
       } else if (MODE == OP_R_CONV_WGRAD) {
         const int hh = h[i] + tkh - 1, ww = w[i] + tkw - 1;
-        const bool ok = kok && static_cast<unsigned>(hh) < static_cast<unsigned>(o.H) &&
-                        static_cast<unsigned>(ww) < static_cast<unsigned>(o.W);
+        const bool ok = kok & (static_cast<unsigned>(hh) < static_cast<unsigned>(o.H)) &
+                        (static_cast<unsigned>(ww) < static_cast<unsigned>(o.W));
         reg[i] = bload(rs, ok ? k * o.C * 2 + colb : OOB);
         // advance this k by one K step (BK pixels) inside its image
         w[i] += o.step_w;
@@ -287,6 +288,61 @@ __device__ __forceinline__ void epilogue(const EpiDev& e, long idx, int col, flo
     bf16_t h = f32_to_bf16(v);
     if (e.mask && !(bf16_to_f32(e.mask[idx]) > 0.0f)) h = 0;
     e.out_bf16[idx] = h;
+  }
+}
+
+// The epilogue for four consecutive columns of one row with vector loads and
+// stores; needs idx and col multiples of 4 and 16-byte aligned float32 (8-byte
+// aligned bf16) tensors, which the host checks.
+__device__ __forceinline__ void epilogue4(const EpiDev& e, long idx, int col, float4 a) {
+  float v[4] = {a.x * e.alpha, a.y * e.alpha, a.z * e.alpha, a.w * e.alpha};
+  auto unpack = [](uint2 u, float (&f)[4]) {
+    f[0] = bf16_to_f32(static_cast<bf16_t>(u.x & 0xffff));
+    f[1] = bf16_to_f32(static_cast<bf16_t>(u.x >> 16));
+    f[2] = bf16_to_f32(static_cast<bf16_t>(u.y & 0xffff));
+    f[3] = bf16_to_f32(static_cast<bf16_t>(u.y >> 16));
+  };
+  float t[4];
+  if (e.bias) {
+    const float4 b = *reinterpret_cast<const float4*>(e.bias + col);
+    v[0] += b.x; v[1] += b.y; v[2] += b.z; v[3] += b.w;
+  } else if (e.bias_bf16) {
+    unpack(*reinterpret_cast<const uint2*>(e.bias_bf16 + col), t);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] += t[q];
+  }
+  if (e.res_f32) {
+    const float4 r = *reinterpret_cast<const float4*>(e.res_f32 + idx);
+    v[0] += r.x; v[1] += r.y; v[2] += r.z; v[3] += r.w;
+  }
+  if (e.res_bf16) {
+    unpack(*reinterpret_cast<const uint2*>(e.res_bf16 + idx), t);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] += t[q];
+  }
+  if (e.relu) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = fmaxf(v[q], 0.0f);
+  }
+  if (e.out_f32) {
+    float4* o = reinterpret_cast<float4*>(e.out_f32 + idx);
+    if (e.accumulate) {
+      const float4 old = *o;
+      v[0] += old.x; v[1] += old.y; v[2] += old.z; v[3] += old.w;
+    }
+    *o = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  if (e.out_bf16) {
+    uint32_t h[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) h[q] = f32_to_bf16(v[q]);
+    if (e.mask) {
+      unpack(*reinterpret_cast<const uint2*>(e.mask + idx), t);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (!(t[q] > 0.0f)) h[q] = 0;
+    }
+    *reinterpret_cast<uint2*>(e.out_bf16 + idx) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
   }
 }
 
@@ -350,8 +406,9 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
+    __builtin_amdgcn_iglp_opt(0);
   };
 
   if (nk > 0) {
@@ -389,20 +446,30 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
     if (kt < nk) compute(lds[0][0], lds[0][1]);   // odd step count: the last step is in buffer 0
   }
 
-  // Lane holds column (lane % 32) and rows 8*(r/4) + 4*(lane/32) + r%4 of each
-  // 32 x 32 tile.
+  // With B as the first MFMA operand, lane l holds row (l % 32) and columns
+  // 8 (r / 4) + 4 (l / 32) + r % 4 of each 32 x 32 tile: four consecutive
+  // columns per register group.
   if (args.splits > 1) {
     float* part = args.partial + (static_cast<long>(split) * args.batch + z) * args.M * args.N;
+    const bool vec = (args.N & 3) == 0;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const int col = col0 + wn * 64 + j * 32 + (lane & 31);
-        if (col >= args.N) continue;
+        const int row = row0 + wm * 64 + i * 32 + (lane & 31);
+        if (row >= args.M) continue;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = row0 + wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-          if (row < args.M) part[static_cast<long>(row) * args.N + col] = acc[i][j][r];
+        for (int g = 0; g < 4; ++g) {
+          const int col = col0 + wn * 64 + j * 32 + 8 * g + 4 * (lane >> 5);
+          float* o = part + static_cast<long>(row) * args.N + col;
+          if (vec && col + 3 < args.N) {
+            *reinterpret_cast<float4*>(o) =
+                make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              if (col + q < args.N) o[q] = acc[i][j][4 * g + q];
+          }
         }
       }
     return;
@@ -412,12 +479,21 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int col = col0 + wn * 64 + j * 32 + (lane & 31);
-      if (col >= args.N) continue;
+      const int row = row0 + wm * 64 + i * 32 + (lane & 31);
+      if (row >= args.M) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = row0 + wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        if (row < args.M) epilogue(args.e, coff + static_cast<long>(row) * args.e.ldc + col, col, acc[i][j][r]);
+      for (int g = 0; g < 4; ++g) {
+        const int col = col0 + wn * 64 + j * 32 + 8 * g + 4 * (lane >> 5);
+        const long idx = coff + static_cast<long>(row) * args.e.ldc + col;
+        const float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+        if (args.vec_epi && col + 3 < args.N) {
+          epilogue4(args.e, idx, col, v);
+        } else {
+          if (col < args.N) epilogue(args.e, idx, col, v.x);
+          if (col + 1 < args.N) epilogue(args.e, idx + 1, col + 1, v.y);
+          if (col + 2 < args.N) epilogue(args.e, idx + 2, col + 2, v.z);
+          if (col + 3 < args.N) epilogue(args.e, idx + 3, col + 3, v.w);
+        }
       }
     }
 }
@@ -425,6 +501,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
 // Sum the split partials in split order and apply the epilogue. Four
 // consecutive columns per thread (N % 4 == 0) with 16-byte partial loads;
 // the row / batch decomposition is done once per four elements.
+template <bool VEC_EPI>
 __global__ __launch_bounds__(256) void splitk_reduce4_kernel(KArgs args) {
   const long mn = static_cast<long>(args.M) * args.N;
   const long plane = static_cast<long>(args.batch) * mn;
@@ -449,10 +526,14 @@ __global__ __launch_bounds__(256) void splitk_reduce4_kernel(KArgs args) {
     const int row = static_cast<int>(rem / args.N), col = static_cast<int>(rem - static_cast<long>(row) * args.N);
     const int z1 = z / args.zdiv, z2 = z - z1 * args.zdiv;
     const long o = z1 * args.c_bs1 + z2 * args.c_bs2 + static_cast<long>(row) * args.e.ldc + col;
-    epilogue(args.e, o, col, acc.x);
-    epilogue(args.e, o + 1, col + 1, acc.y);
-    epilogue(args.e, o + 2, col + 2, acc.z);
-    epilogue(args.e, o + 3, col + 3, acc.w);
+    if (VEC_EPI) {
+      epilogue4(args.e, o, col, acc);
+    } else {
+      epilogue(args.e, o, col, acc.x);
+      epilogue(args.e, o + 1, col + 1, acc.y);
+      epilogue(args.e, o + 2, col + 2, acc.z);
+      epilogue(args.e, o + 3, col + 3, acc.w);
+    }
   }
 }
 
@@ -581,6 +662,10 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   a.e.alpha = d.epi.alpha;
   a.e.relu = d.epi.relu;
   a.e.accumulate = d.epi.accumulate;
+  auto al = [](const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) & (n - 1)) == 0; };
+  const EpiDev& e = a.e;
+  a.vec_epi = e.ldc % 4 == 0 && a.c_bs1 % 4 == 0 && a.c_bs2 % 4 == 0 && al(e.out_f32, 16) && al(e.out_bf16, 8) &&
+              al(e.bias, 16) && al(e.bias_bf16, 8) && al(e.res_f32, 16) && al(e.res_bf16, 8) && al(e.mask, 8);
   return true;
 }
 
@@ -603,7 +688,8 @@ hipError_t launch_reduce(const KArgs& a, hipStream_t s) {
   const long total = static_cast<long>(a.batch) * a.M * a.N;
   if (a.N % 4 == 0) {
     const long blocks = std::min<long>((total / 4 + 255) / 256, 8192);
-    hipLaunchKernelGGL(splitk_reduce4_kernel, dim3(static_cast<int>(blocks)), dim3(256), 0, s, a);
+    if (a.vec_epi) hipLaunchKernelGGL(splitk_reduce4_kernel<true>, dim3(static_cast<int>(blocks)), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(splitk_reduce4_kernel<false>, dim3(static_cast<int>(blocks)), dim3(256), 0, s, a);
   } else {
     const long blocks = std::min<long>((total + 255) / 256, 8192);
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3(static_cast<int>(blocks)), dim3(256), 0, s, a);
