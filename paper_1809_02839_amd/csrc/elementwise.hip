@@ -59,7 +59,7 @@ __global__ void mask_f32_kernel(const float* src, const float* mask, float* dst,
 // Pass 1: block (cb, rb) sums rows [rb*RCH, (rb+1)*RCH) of its columns into
 // partial[rb][col]. bf16 inputs with cols % 8 == 0 use 16-byte loads: 32
 // column groups of 8 x 8 row lanes; otherwise 64 columns x 4 row lanes.
-constexpr int RCH = 256;
+constexpr int RCH = COLSUM_ROWS;
 __global__ void colsum_partial_bf16x8_kernel(const bf16_t* X, long rows, int cols, long ld, float* partial) {
   __shared__ float sh[8][256];
   const int cg = threadIdx.x & 31, rl = threadIdx.x >> 5;
@@ -105,23 +105,23 @@ __global__ void colsum_partial_kernel(const T* X, long rows, int cols, long ld, 
   __syncthreads();
   if (ty == 0 && col < cols) partial[static_cast<long>(blockIdx.y) * cols + col] = (sh[0][tx] + sh[1][tx]) + (sh[2][tx] + sh[3][tx]);
 }
-// Pass 2: 64 columns per block of 16 waves; chunk c goes to wave c % 16, and
-// the 16 wave sums are added in a fixed order.
-constexpr int FIN_WAVES = 16;
-__global__ __launch_bounds__(64 * FIN_WAVES) void colsum_final_kernel(const float* partial, int nchunks, int cols,
-                                                                      float* out, int accumulate) {
-  __shared__ float sh[FIN_WAVES][64];
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  const int col = blockIdx.x * 64 + tx;
+// Pass 2: 16 columns per block of 256 threads; thread t sums chunks
+// c = t / 16 (mod 16) of column t % 16, and the 16 sums of a column are added
+// in a fixed order.
+__global__ __launch_bounds__(256) void colsum_final_kernel(const float* partial, int nchunks, int cols, float* out,
+                                                           int accumulate) {
+  __shared__ float sh[16][16];
+  const int cx = threadIdx.x & 15, cy = threadIdx.x >> 4;
+  const int col = blockIdx.x * 16 + cx;
   float s = 0.0f;
   if (col < cols)
-    for (int c = ty; c < nchunks; c += FIN_WAVES) s += partial[static_cast<long>(c) * cols + col];
-  sh[ty][tx] = s;
+    for (int c = cy; c < nchunks; c += 16) s += partial[static_cast<long>(c) * cols + col];
+  sh[cy][cx] = s;
   __syncthreads();
-  if (ty == 0 && col < cols) {
+  if (cy == 0 && col < cols) {
     float v = 0.0f;
 #pragma unroll
-    for (int w = 0; w < FIN_WAVES; ++w) v += sh[w][tx];
+    for (int w = 0; w < 16; ++w) v += sh[w][cx];
     out[col] = accumulate ? out[col] + v : v;
   }
 }
@@ -228,7 +228,6 @@ __global__ __launch_bounds__(NT) void layernorm_fwd_kernel(const bf16_t* r, cons
 }
 
 // Rows per block in the backward; per-block partial dgamma/dbeta.
-constexpr int LNB_ROWS = 32;
 template <int VPL>
 __global__ __launch_bounds__(NT) void layernorm_bwd_kernel(const bf16_t* dy, const bf16_t* r, const float* mean,
                                                            const float* rstd, const bf16_t* gamma, int R, int D,
@@ -397,7 +396,7 @@ hipError_t column_sum(const void* X, int dtype, long rows, int cols, long ld, fl
                          static_cast<const float*>(X), rows, cols, ld, partial_ws);
     }
   }
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 63) / 64), dim3(64 * FIN_WAVES), 0, s, partial_ws, nchunks,
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 15) / 16), dim3(256), 0, s, partial_ws, nchunks,
                      cols, out, accumulate);
   return hipGetLastError();
 }
@@ -445,8 +444,8 @@ hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, c
     case 32: hipLaunchKernelGGL(layernorm_bwd_kernel<32>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
     default: return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 63) / 64), dim3(64 * FIN_WAVES), 0, s, pg, nb, D, dgamma, 0);
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 63) / 64), dim3(64 * FIN_WAVES), 0, s, pb, nb, D, dbeta, 0);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 15) / 16), dim3(256), 0, s, pg, nb, D, dgamma, 0);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 15) / 16), dim3(256), 0, s, pb, nb, D, dbeta, 0);
   return hipGetLastError();
 }
 

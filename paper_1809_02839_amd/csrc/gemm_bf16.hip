@@ -30,6 +30,7 @@ constexpr int TILE_ELEMS = 128 * PITCH;  // one operand tile (= BK * RPITCH)
 static_assert(TILE_ELEMS == BK * RPITCH, "both tile layouts occupy the same LDS");
 constexpr int BUF_FLAGS = 0x00020000;    // gfx9 raw buffer resource word 3
 constexpr int OOB = 0x7ffffff0;          // byte offset past every resource: the load returns 0
+constexpr int MAX_SPLITS = 16;           // K slices of one split-K launch
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
@@ -499,32 +500,36 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
 }
 
 // Sum the split partials in split order and apply the epilogue. Four
-// consecutive columns per thread (N % 4 == 0) with 16-byte partial loads;
-// the row / batch decomposition is done once per four elements.
+// consecutive columns per thread (N % 4 == 0) with 16-byte partial loads, all
+// of a thread's loads issued before the ordered sum. The partial plane is
+// below 2^31 elements (the workspace bounds it), so indices are 32-bit.
 template <bool VEC_EPI>
 __global__ __launch_bounds__(256) void splitk_reduce4_kernel(KArgs args) {
-  const long mn = static_cast<long>(args.M) * args.N;
-  const long plane = static_cast<long>(args.batch) * mn;
-  const long total4 = plane >> 2;
-  for (long t = static_cast<long>(blockIdx.x) * 256 + threadIdx.x; t < total4;
-       t += static_cast<long>(gridDim.x) * 256) {
-    const long e = t << 2;
-    float4 acc = *reinterpret_cast<const float4*>(args.partial + e);
-    for (int sp = 1; sp < args.splits; ++sp) {
-      const float4 v = *reinterpret_cast<const float4*>(args.partial + sp * plane + e);
-      acc.x += v.x;
-      acc.y += v.y;
-      acc.z += v.z;
-      acc.w += v.w;
-    }
-    int z = 0;
-    long rem = e;
+  const uint32_t mn = static_cast<uint32_t>(args.M) * args.N;
+  const uint32_t plane = static_cast<uint32_t>(args.batch) * mn;
+  const uint32_t total4 = plane >> 2;
+  for (uint32_t t = blockIdx.x * 256 + threadIdx.x; t < total4; t += gridDim.x * 256) {
+    const uint32_t e = t << 2;
+    float4 v[MAX_SPLITS];
+#pragma unroll
+    for (int sp = 0; sp < MAX_SPLITS; ++sp)
+      if (sp < args.splits) v[sp] = *reinterpret_cast<const float4*>(args.partial + sp * plane + e);
+    float4 acc = v[0];
+#pragma unroll
+    for (int sp = 1; sp < MAX_SPLITS; ++sp)
+      if (sp < args.splits) {
+        acc.x += v[sp].x;
+        acc.y += v[sp].y;
+        acc.z += v[sp].z;
+        acc.w += v[sp].w;
+      }
+    uint32_t z = 0, rem = e;
     if (args.batch > 1) {
-      z = static_cast<int>(e / mn);
+      z = e / mn;
       rem = e - z * mn;
     }
-    const int row = static_cast<int>(rem / args.N), col = static_cast<int>(rem - static_cast<long>(row) * args.N);
-    const int z1 = z / args.zdiv, z2 = z - z1 * args.zdiv;
+    const uint32_t row = rem / static_cast<uint32_t>(args.N), col = rem - row * args.N;
+    const uint32_t z1 = z / args.zdiv, z2 = z - z1 * args.zdiv;
     const long o = z1 * args.c_bs1 + z2 * args.c_bs2 + static_cast<long>(row) * args.e.ldc + col;
     if (VEC_EPI) {
       epilogue4(args.e, o, col, acc);
@@ -635,7 +640,7 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   if (d.workspace && tiles < kTargetBlocks && d.K >= 2 * 8 * BK) {
     splits = static_cast<int>(kTargetBlocks / tiles);   // all blocks resident in one round
     splits = std::min(splits, d.K / (8 * BK));
-    splits = std::min(splits, 16);
+    splits = std::min(splits, MAX_SPLITS);
     const long per = static_cast<long>(d.batch) * d.M * d.N * 4;
     while (splits > 1 && per * splits > static_cast<long>(d.workspace_bytes)) --splits;
   }

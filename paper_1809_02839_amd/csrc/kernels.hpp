@@ -77,6 +77,13 @@ hipError_t fused_update(float* W, float* v, const float* g, void* what_f, void* 
 hipError_t predict_slot(const float* W, const float* v, void* what, int what_dtype, long n, float lr, int s_pred,
                         hipStream_t s);
 
+// Row chunking of the two-pass column reductions (column sums, layer-norm
+// parameter gradients) and the float32 workspace each pass needs.
+constexpr int COLSUM_ROWS = 64;   // rows summed per block in the first pass
+constexpr int LNB_ROWS = 16;      // rows per block of the layer-norm backward
+inline long column_sum_ws_floats(long rows, long cols) { return ((rows + COLSUM_ROWS - 1) / COLSUM_ROWS) * cols; }
+inline long layernorm_bwd_ws_floats(long rows, long d) { return 2 * ((rows + LNB_ROWS - 1) / LNB_ROWS) * d; }
+
 // ------------------------------------------------------------ elementwise ----
 // dst[i] = src[i] * (mask[i] > 0), bf16 (dtype 1) or float32 (dtype 0).
 hipError_t mask_relu_grad(const void* src, const void* mask, void* dst, long n, int dtype, hipStream_t s);

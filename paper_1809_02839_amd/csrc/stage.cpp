@@ -227,7 +227,7 @@ void Stage::plan_buffers() {
   const int L = d_.num_layers;
   const long B = d_.batch;
   std::vector<size_t> st, ws;   // byte sizes, indexed by buffer id
-  auto partial_floats = [](long rows, long cols) { return ((rows + 255) / 256) * cols; };
+  auto partial_floats = [](long rows, long cols) { return column_sum_ws_floats(rows, cols); };
   long partial = 0;
   switch (d_.kind) {
     case SPECTRAIN_KIND_FC: {
@@ -274,7 +274,7 @@ void Stage::plan_buffers() {
             static_cast<size_t>(T * d * 2), static_cast<size_t>(T * d * 2), static_cast<size_t>(T * d * 2),
             static_cast<size_t>(T * 3 * d * 2)};
       partial = std::max(partial_floats(T, 3 * d), partial_floats(T, F));
-      partial = std::max(partial, 2 * ((T + 31) / 32) * d);
+      partial = std::max(partial, layernorm_bwd_ws_floats(T, d));
       break;
     }
     case SPECTRAIN_KIND_RESLSTM: {
