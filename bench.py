@@ -20,6 +20,7 @@ in a separate pass with HIP events around each launch on the stage's stream;
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
 """
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -82,7 +83,7 @@ class StageLoop:
         dt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
         self.st = native.Stage(native.desc_from_spec(spec), synth.initial_params(spec), stream)
         k, N = spec.stage_index, spec.num_stages
-        self.sf, self.sb = native.version_difference(k, N, True), native.version_difference(k, N, False)
+        self.sf, self.sb = native.policy_versions(spec.policy, k, N)
         self.depth = N - k
         self.ring = ring
         with torch.cuda.stream(stream):
@@ -142,7 +143,7 @@ def cpu_baseline(spec, n_steps):
     W = synth.initial_params(spec).astype(np.float64)
     v = np.zeros_like(W)
     rnd = stages.weight_rounder(spec)
-    sf, sb = method.version_difference(k, N, True), method.version_difference(k, N, False)
+    sf, sb = method.staleness_versions(spec.policy, k, N)
     t0 = time.perf_counter()
     for m in range(n_steps):
         x = synth.stage_input(spec, m)
@@ -167,6 +168,9 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--cpu-steps", type=int, default=8)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--policy", default="spectrain", choices=["spectrain", "vanilla", "stash"],
+                    help="weight staleness treatment (Section 4.2): SpecTrain prediction (default), Vanilla "
+                         "pipelining (latest weights) or weight stashing (backward reuses the forward's weights)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (a known-size reference "
                          "dispatch for scaling hardware byte counters)")
@@ -183,7 +187,7 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
-    spec = synth.WORKLOADS[args.workload].stages[0]
+    spec = dataclasses.replace(synth.WORKLOADS[args.workload].stages[0], policy=args.policy)
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib << 18   # float32 elements
         src = torch.ones(n, device="cuda")
@@ -262,7 +266,8 @@ def main():
         "vs_baseline": None,
         "dtype": spec.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: {DESCRIPTIONS[args.workload]}", "batch": spec.batch,
+        "config": {"workload": f"{args.workload}: {DESCRIPTIONS[args.workload]}", "policy": args.policy,
+                   "batch": spec.batch,
                    "stage_index": spec.stage_index, "num_stages": spec.num_stages,
                    "s_forward": loop.sf, "s_backward": loop.sb, "params": synth.num_params(spec)},
         "mfma_util_pct": round(100.0 * gemm_flops / (gemm_ms / 1e3) / 1e12 / peak_mfma, 2) if gemm_ms else None,

@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SPECTRAIN_ABI_VERSION 1u
+#define SPECTRAIN_ABI_VERSION 2u
 
 /* Status codes. */
 enum {
@@ -84,6 +84,18 @@ typedef enum {
   SPECTRAIN_HEAD_CE = 1     /* mean softmax cross-entropy over rows; caller passes int32 labels */
 } spectrain_head;
 
+/* Which weights the backward pass of a mini-batch uses (Section 4.2 compares
+ * the three ways a pipeline stage can treat weight staleness):
+ *   PREDICT - the backward-predicted slot 1 (SpecTrain, s from Eq. 6; with
+ *             s = 0 for both passes this is the unmitigated pipeline, the
+ *             paper's Vanilla model parallelism);
+ *   STASH   - the weights its own forward pass used (weight stashing, as in
+ *             PipeDream, Section 3.2): every forward copies slot 0 into a ring
+ *             of N - k weight versions, one per mini-batch in flight, and the
+ *             matching backward reads that copy. The caller passes s = 0 to
+ *             the update so that each forward sees the latest weights. */
+typedef enum { SPECTRAIN_POLICY_PREDICT = 0, SPECTRAIN_POLICY_STASH = 1 } spectrain_weight_policy;
+
 typedef struct {
   uint32_t abi_version;     /* SPECTRAIN_ABI_VERSION */
   int32_t kind;             /* spectrain_kind */
@@ -96,6 +108,7 @@ typedef struct {
   int32_t dims[8];          /* kind-specific, see spectrain_kind; unused entries 0 */
   float lr;                 /* eta > 0 */
   float momentum;           /* gamma, 0 < gamma <= 1 */
+  int32_t weight_policy;    /* spectrain_weight_policy */
 } spectrain_stage_desc;
 
 /* Eq. 5 (is_forward != 0) or Eq. 6: version difference s for stage k of N.
@@ -120,7 +133,8 @@ int spectrain_stage_num_params(spectrain_stage_t st, size_t* n);
  * s < 0 or a bad slot. */
 int spectrain_stage_predict(spectrain_stage_t st, int32_t s, int32_t slot);
 
-/* Forward pass of mini-batch mb_id against slot 0. x_dev: input activations.
+/* Forward pass of mini-batch mb_id against slot 0 (with STASH, slot 0 is also
+ * copied into the mini-batch's weight stash). x_dev: input activations.
  * y_dev: output activations (HEAD_NONE; NULL with a CE head). labels_dev and
  * loss_dev (one float32, the mean CE) are used with a CE head only. The stage
  * keeps references to x_dev and y_dev until the matching backward returns:
@@ -129,8 +143,8 @@ int spectrain_stage_predict(spectrain_stage_t st, int32_t s, int32_t slot);
 int spectrain_stage_forward(spectrain_stage_t st, int64_t mb_id, const void* x_dev, void* y_dev,
                             const int32_t* labels_dev, float* loss_dev);
 
-/* Backward pass of mini-batch mb_id against slot 1 (dX) and the stashed
- * activations (g). dy_dev: dL/dY (HEAD_NONE; ignored with a CE head).
+/* Backward pass of mini-batch mb_id against slot 1 (PREDICT) or the weights
+ * its forward used (STASH) for dX, and the stashed activations (g). dy_dev: dL/dY (HEAD_NONE; ignored with a CE head).
  * dx_dev: dL/dX output, or NULL to skip it (e.g. at k = 0). Overwrites g with
  * this mini-batch's gradient and frees its stash slot. ESTATE when mb_id is
  * not in flight or a previous gradient is still waiting for its update. */

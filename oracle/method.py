@@ -28,6 +28,20 @@ def version_difference(k: int, N: int, forward: bool) -> int:
     return k // 2
 
 
+def staleness_versions(policy: str, k: int, N: int):
+    """Version differences (before a forward, before a backward) under the three
+    ways Section 4.2 compares a pipeline stage treating weight staleness:
+    SpecTrain predicts (Eq. 5, Eq. 6); Vanilla model parallelism and PipeDream's
+    weight stashing start every forward from the latest weights (no prediction,
+    s = 0). Under stashing the backward reuses the forward's weights, which the
+    caller keeps; under Vanilla it takes the latest weights at its own time."""
+    if policy == "spectrain":
+        return version_difference(k, N, True), version_difference(k, N, False)
+    if policy in ("vanilla", "stash"):
+        return 0, 0
+    raise ValueError(f"unknown policy {policy!r}")
+
+
 def predict(W, v, s: int, lr: float):
     """Eq. 4: W^_{t+s} = W_t - s * eta * v_{t-1}, from the current stored pair
     (W_t, v_{t-1}); the result is held as float32 like the master weights."""

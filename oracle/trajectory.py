@@ -4,7 +4,10 @@ At every task the stage predicts its weights from its current (W, v) with the
 version difference of Eq. 5 (forward) or Eq. 6 (backward) and Eq. 4, rounds
 them to the operand format, and runs the pass; each backward is followed by
 the momentum update of Eq. 1 and W <- W - eta v (Section 3.2). Initial v is
-zero, so every prediction before the first update returns W0.
+zero, so every prediction before the first update returns W0. A stage whose
+spec names the "vanilla" or "stash" policy (the comparison of Section 4.2)
+uses s = 0 instead; under "stash" the backward of a mini-batch reuses the
+weights its forward used.
 
 A workload either simulates all N stages of a pipeline (mini-batch m enters
 stage 0 with its synthetic input; each stage's output feeds the next; the last
@@ -32,8 +35,9 @@ class StageState:
         self.gamma = float(np.float32(spec.momentum))
 
     def predicted(self, forward: bool):
-        s = method.version_difference(self.spec.stage_index, self.spec.num_stages, forward)
-        What = method.predict(self.W, self.v, s, self.lr)
+        s_f, s_b = method.staleness_versions(getattr(self.spec, "policy", "spectrain"),
+                                             self.spec.stage_index, self.spec.num_stages)
+        What = method.predict(self.W, self.v, s_f if forward else s_b, self.lr)
         return stages.unpack(self.spec, stages.weight_rounder(self.spec)(What))
 
 
@@ -88,6 +92,8 @@ def run(workload, steps: Optional[int] = None, exact: bool = False,
             P = S.predicted(forward=True)
             y, loss, stash = stages.forward(spec, P, x, lab, exact=exact)
             stash["dy"] = dy
+            if getattr(spec, "policy", "spectrain") == "stash":
+                stash["weights"] = P         # the backward of m reuses these (weight stashing)
             S.stash[m] = stash
             if loss is not None:
                 out["loss"][m] = loss
@@ -100,7 +106,7 @@ def run(workload, steps: Optional[int] = None, exact: bool = False,
             dy = stash["dy"]
             if full and k < N - 1:
                 dy = handoff_dx.pop((k + 1, m))
-            P = S.predicted(forward=False)
+            P = stash["weights"] if "weights" in stash else S.predicted(forward=False)
             dx, grads = stages.backward(spec, P, stash, dy, exact=exact)
             g = stages.pack(spec, grads)
             S.W, S.v = method.momentum_sgd_step(S.W, S.v, g, S.lr, S.gamma)

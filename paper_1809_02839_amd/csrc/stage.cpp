@@ -145,7 +145,7 @@ void Stage::build_layout() {
 }
 
 const void* Stage::wf(int i) const { return static_cast<const char*>(what_[0]) + tensors_[i].off * esz_; }
-const void* Stage::wb(int i) const { return static_cast<const char*>(what_[1]) + tensors_[i].off * esz_; }
+const void* Stage::wb(int i) const { return static_cast<const char*>(bwd_weights_) + tensors_[i].off * esz_; }
 
 void Stage::gemm(const GemmDesc& d) {
   const char* name = "gemm";
@@ -318,6 +318,8 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
   if (d.batch < 1 || d.num_layers < 1) fail("batch and num_layers must be >= 1");
   if (!(d.lr > 0.0f) || !std::isfinite(d.lr)) fail("lr must be a positive finite number");
   if (!(d.momentum > 0.0f && d.momentum <= 1.0f)) fail("momentum must lie in (0, 1]");
+  if (d.weight_policy != SPECTRAIN_POLICY_PREDICT && d.weight_policy != SPECTRAIN_POLICY_STASH)
+    fail("weight_policy must be PREDICT or STASH");
   if (d.dtype != SPECTRAIN_FP32 && d.dtype != SPECTRAIN_BF16) fail("unknown dtype");
   if (d.head != SPECTRAIN_HEAD_NONE && d.head != SPECTRAIN_HEAD_CE) fail("unknown head");
   if (d.head == SPECTRAIN_HEAD_CE && d.kind != SPECTRAIN_KIND_FC && d.kind != SPECTRAIN_KIND_RESLSTM)
@@ -388,6 +390,10 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
   *flag_host_ = 0;
   hip_check(hipHostGetDevicePointer(reinterpret_cast<void**>(&flag_dev_), flag_host_, 0), "hipHostGetDevicePointer");
   plan_buffers();
+  if (d.weight_policy == SPECTRAIN_POLICY_STASH) {
+    for (size_t i = 0; i < slots_.size(); ++i) wstash_off_.push_back(wstash_.add(n_arena_ * esz_));
+    wstash_.allocate();
+  }
 
   hip_check(fill_f32(v_, 0.0f, n_arena_, s_), "clear v");
   hip_check(fill_f32(g_, 0.0f, n_arena_, s_), "clear g");
@@ -486,6 +492,10 @@ void Stage::forward(int64_t mb, const void* x, void* y, const int32_t* labels, f
     if (!slots_[i].used && free_slot < 0) free_slot = static_cast<int>(i);
   }
   if (free_slot < 0) throw StageError(SPECTRAIN_ESTATE, "N - k mini-batches already in flight");
+  if (d_.weight_policy == SPECTRAIN_POLICY_STASH)
+    hip_check(hipMemcpyAsync(wstash_.at<char>(wstash_off_[free_slot]), what_[0], n_arena_ * esz_,
+                             hipMemcpyDeviceToDevice, s_),
+              "stash weights");
   switch (d_.kind) {
     case SPECTRAIN_KIND_FC: fwd_fc(free_slot, x, y, labels, loss); break;
     case SPECTRAIN_KIND_CONV3X3: fwd_conv(free_slot, x, y); break;
@@ -503,6 +513,7 @@ void Stage::backward(int64_t mb, const void* dy, void* dx) {
   if (slot < 0) throw StageError(SPECTRAIN_ESTATE, "backward of a mini-batch that is not in flight");
   if (g_pending_) throw StageError(SPECTRAIN_ESTATE, "the previous gradient has not been applied by an update");
   if (d_.head != SPECTRAIN_HEAD_CE && !dy) fail("dy_dev is NULL");
+  bwd_weights_ = d_.weight_policy == SPECTRAIN_POLICY_STASH ? wstash_.at<char>(wstash_off_[slot]) : what_[1];
   switch (d_.kind) {
     case SPECTRAIN_KIND_FC: bwd_fc(slot, dy, dx); break;
     case SPECTRAIN_KIND_CONV3X3: bwd_conv(slot, dy, dx); break;

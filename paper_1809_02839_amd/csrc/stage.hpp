@@ -80,7 +80,7 @@ class Stage {
   void plan_buffers();
   long tensor_off(int i) const { return tensors_[i].off; }
   const void* wf(int i) const;   // predicted slot 0 (forward) of tensor i
-  const void* wb(int i) const;   // predicted slot 1 (backward) of tensor i
+  const void* wb(int i) const;   // backward weights of tensor i (slot 1, or the mini-batch's stash)
   float* grad(int i) const { return g_ + tensors_[i].off; }
   template <typename T>
   T* stash(int slot, int buf) const { return slot_blocks_[slot].at<T>(stash_off_[buf]); }
@@ -141,6 +141,9 @@ class Stage {
   float* v_ = nullptr;
   float* g_ = nullptr;
   void* what_[2] = {nullptr, nullptr};
+  DeviceBlock wstash_;                   // STASH policy: one weight copy per stash slot
+  std::vector<size_t> wstash_off_;
+  const void* bwd_weights_ = nullptr;    // base of the weights the current backward reads
   int* flag_host_ = nullptr;   // pinned, mapped: set by the update kernel on a non-finite value
   int* flag_dev_ = nullptr;
 

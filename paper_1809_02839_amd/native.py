@@ -11,13 +11,15 @@ import numpy as np
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspectrain.so")
 
-ABI_VERSION = 1
+ABI_VERSION = 2
 OK, EINVAL, ENOMEM, EHIP, ESTATE, ENONFINITE = range(6)
 STATUS_NAMES = {OK: "OK", EINVAL: "EINVAL", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE",
                 ENONFINITE: "ENONFINITE"}
 FP32, BF16 = 0, 1
 KIND_FC, KIND_CONV3X3, KIND_BOTTLENECK, KIND_TRANSFORMER, KIND_RESLSTM = range(5)
 HEAD_NONE, HEAD_CE = 0, 1
+POLICY_PREDICT, POLICY_STASH = 0, 1
+POLICIES = ("spectrain", "vanilla", "stash")
 KIND_BY_NAME = {"fc": KIND_FC, "conv3x3": KIND_CONV3X3, "bottleneck": KIND_BOTTLENECK,
                 "transformer": KIND_TRANSFORMER, "reslstm": KIND_RESLSTM}
 
@@ -32,7 +34,7 @@ class StageDesc(ctypes.Structure):
     _fields_ = [("abi_version", ctypes.c_uint32), ("kind", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("head", ctypes.c_int32), ("stage_index", ctypes.c_int32), ("num_stages", ctypes.c_int32),
                 ("batch", ctypes.c_int32), ("num_layers", ctypes.c_int32), ("dims", ctypes.c_int32 * 8),
-                ("lr", ctypes.c_float), ("momentum", ctypes.c_float)]
+                ("lr", ctypes.c_float), ("momentum", ctypes.c_float), ("weight_policy", ctypes.c_int32)]
 
 
 class KernelStat(ctypes.Structure):
@@ -99,7 +101,20 @@ def version_difference(k: int, N: int, forward: bool) -> int:
     return int(lib().spectrain_version_difference(k, N, 1 if forward else 0))
 
 
-def make_desc(kind, dtype, head, stage_index, num_stages, batch, num_layers, dims, lr, momentum) -> StageDesc:
+def policy_versions(policy: str, k: int, N: int):
+    """(s before a forward, s before a backward) of stage k of N: Eq. 5 and
+    Eq. 6 for SpecTrain; 0 for both under the Vanilla and stashing policies
+    (every pass starts from the latest weights; with stashing the backward
+    then reads the copy its forward used)."""
+    if policy == "spectrain":
+        return version_difference(k, N, True), version_difference(k, N, False)
+    if policy in ("vanilla", "stash"):
+        return 0, 0
+    raise ValueError(f"unknown policy {policy!r}")
+
+
+def make_desc(kind, dtype, head, stage_index, num_stages, batch, num_layers, dims, lr, momentum,
+              weight_policy=POLICY_PREDICT) -> StageDesc:
     d = StageDesc()
     d.abi_version = ABI_VERSION
     d.kind = KIND_BY_NAME[kind] if isinstance(kind, str) else int(kind)
@@ -109,12 +124,17 @@ def make_desc(kind, dtype, head, stage_index, num_stages, batch, num_layers, dim
     for i, v in enumerate(dims):
         d.dims[i] = int(v)
     d.lr, d.momentum = lr, momentum
+    d.weight_policy = int(weight_policy)
     return d
 
 
 def desc_from_spec(spec) -> StageDesc:
+    policy = getattr(spec, "policy", "spectrain")
+    if policy not in POLICIES:
+        raise ValueError(f"unknown policy {policy!r}")
     return make_desc(spec.kind, spec.dtype, spec.head, spec.stage_index, spec.num_stages, spec.batch,
-                     spec.num_layers, spec.dims, spec.lr, spec.momentum)
+                     spec.num_layers, spec.dims, spec.lr, spec.momentum,
+                     POLICY_STASH if policy == "stash" else POLICY_PREDICT)
 
 
 class Stage:

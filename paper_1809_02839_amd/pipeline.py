@@ -7,7 +7,9 @@ weight update per backward). Each stage sees exactly the weight versions it
 would see on its own GPU: before its forward it uses weights predicted with the
 forward version difference (Eq. 5) and before its backward the ones predicted
 with the backward difference (Eq. 6); the fused update after every backward
-refreshes W and v and re-predicts both (Eq. 1, Eq. 4).
+refreshes W and v and re-predicts both (Eq. 1, Eq. 4). A stage whose spec
+names the Vanilla or stashing policy uses s = 0 instead (Section 4.2), the
+latter with the library's weight stash for its backward passes.
 
 Device memory and streams come from torch; every step of the stage runs in
 libspectrain.so through the C ABI.
@@ -102,8 +104,10 @@ class Pipeline:
         if v0s is not None:
             for spec, W0, v0 in zip(self.specs, W0s, v0s):
                 self.stages[spec.stage_index].set_state(W0, v0)
-        self.s_f = {k: native.version_difference(k, self.N, True) for k in self.stages}
-        self.s_b = {k: native.version_difference(k, self.N, False) for k in self.stages}
+        versions = {k: native.policy_versions(getattr(self.spec_of[k], "policy", "spectrain"), k, self.N)
+                    for k in self.stages}
+        self.s_f = {k: versions[k][0] for k in self.stages}
+        self.s_b = {k: versions[k][1] for k in self.stages}
         # the first tasks see predictions from the initial (W, v) (Eq. 4)
         for k, st in self.stages.items():
             st.predict(self.s_f[k], 0)

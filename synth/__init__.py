@@ -48,6 +48,10 @@ class StageSpec:
     dims: Tuple[int, ...]
     lr: float
     momentum: float
+    # how a pass treats weight staleness: "spectrain" (predicted weights),
+    # "vanilla" (the latest weights at every pass) or "stash" (the backward
+    # reuses the weights of its own forward)
+    policy: str = "spectrain"
 
     # ----- shapes -------------------------------------------------------
     def fc_widths(self) -> List[int]:

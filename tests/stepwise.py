@@ -8,7 +8,9 @@ difference), a backward plus update from the state before that backward
 (Eq. 6's difference) and the oracle's own stash of the same mini-batch; in a
 full pipeline a stage's input and upstream gradient are the GPU's neighbouring
 outputs. Every task is thus compared against an exact recomputation of the
-same step, with no divergence carried from earlier steps.
+same step, with no divergence carried from earlier steps. Under the Vanilla
+and stashing policies the differences are 0 and a stashing backward reuses
+the weights the oracle's forward of the same mini-batch used.
 
 With derived=True (every bf16 run) the gradient quantities (v, the step's
 weight change, dX) pass when they are within tol of the oracle's bf16
@@ -53,7 +55,8 @@ def run_stepwise(wl, steps, torch, derived=False):
         k = spec.stage_index
         lr = float(np.float32(spec.lr))
         gamma = float(np.float32(spec.momentum))
-        sf, sb = method.version_difference(k, N, True), method.version_difference(k, N, False)
+        policy = getattr(spec, "policy", "spectrain")
+        sf, sb = method.staleness_versions(policy, k, N)
         W = W0s[k].astype(np.float64)
         v = np.zeros_like(W)
         u = 0
@@ -67,6 +70,8 @@ def run_stepwise(wl, steps, torch, derived=False):
                 P = stages.unpack(spec, rnd(method.predict(W, v, sf, lr)))
                 y, loss, st = stages.forward(spec, P, x, lab)
                 stash[m] = st
+                if policy == "stash":
+                    stash[("weights", m)] = P   # the backward reuses the forward's weights
                 if derived:
                     stash[("exact", m)] = stages.forward(spec, P, x, lab, exact=True)[2]
                 if spec.head == "ce":
@@ -76,7 +81,10 @@ def run_stepwise(wl, steps, torch, derived=False):
             else:
                 if full and k < N - 1:
                     dy = dx_gpu[(k + 1, m)]
-                P = stages.unpack(spec, rnd(method.predict(W, v, sb, lr)))
+                if policy == "stash":
+                    P = stash.pop(("weights", m))
+                else:
+                    P = stages.unpack(spec, rnd(method.predict(W, v, sb, lr)))
                 dx, grads = stages.backward(spec, P, stash.pop(m), dy)
                 W1, v1 = method.momentum_sgd_step(W, v, stages.pack(spec, grads), lr, gamma)
                 u += 1

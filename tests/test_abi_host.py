@@ -62,6 +62,8 @@ def _create(desc, n=None, W=None):
     (dict(dtype=0), "bf16 only"),
     (dict(head=1), "CE head"),
     (dict(dims=(250, 512, 8, 8)), "multiple of 8"),
+    (dict(weight_policy=2), "weight_policy"),
+    (dict(weight_policy=-1), "weight_policy"),
 ])
 def test_bad_descriptor_is_rejected_before_any_device_work(change, needle):
     spec = synth.WORKLOADS["vgg_conv"].stages[0]

@@ -2,6 +2,8 @@
 one-forward-one-backward order, against the CPU oracle on the same seeded
 inputs (every stage kind, reduced sizes spanning several GEMM tiles with
 ragged tails, plus the full-size float32 MLP pipeline)."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -125,4 +127,66 @@ def test_closed_form_through_abi_is_bitwise(k, N):
 
     pipe.run(10, lambda sp, m: (X, dY, None), on_update=cb)
     assert seen == list(range(1, 11))
+    pipe.destroy()
+
+
+@pytest.mark.parametrize("policy", ["vanilla", "stash"])
+@pytest.mark.parametrize("name", ["mlp3_small", "reslstm_small"])
+def test_policy_trajectory_matches_oracle(name, policy):
+    """Free-running Vanilla and weight-stashing trajectories (Section 4.2) of
+    the well-conditioned workloads against the oracle under the same policy."""
+    base = synth.ALL_WORKLOADS[name]
+    wl = synth.Workload(f"{name}/{policy}", tuple(dataclasses.replace(s, policy=policy) for s in base.stages),
+                        base.steps)
+    tol = TOL[wl.stages[0].dtype]
+    print(f"[parity] {wl.name}", flush=True)
+    ref, ref_states = oracle_trajectory(wl)
+    pipe, out, states = _gpu_trajectory(wl)
+    worst = Worst(wl.name)
+    for spec in wl.stages:
+        k = spec.stage_index
+        W0 = synth.initial_params(spec).astype(np.float64)
+        for u in range(1, wl.steps + 1):
+            Wg, vg = states[(k, u)]
+            Wo, vo = ref_states[(k, u)]
+            worst.check("W", Wg, Wo, tol, f"k{k} u{u}")
+            worst.check("v", vg, vo, tol, f"k{k} u{u}")
+            worst.check("W-W0", Wg - W0, Wo - W0, dw_bound(tol, Wo, W0), f"k{k} u{u}")
+    for (k, m), dx in out["dx"].items():
+        worst.check("dx", dx.float().cpu().numpy(), ref["dx"][(k, m)], tol, f"k{k} m{m}")
+    print(f"[parity] {wl.name}: {worst.report()}", flush=True)
+    pipe.destroy()
+
+
+@pytest.mark.parametrize("k,N", [(0, 3), (1, 3), (0, 4), (2, 4)])
+def test_stash_closed_form_through_abi_is_bitwise(k, N):
+    """Dyadic constant-gradient case under weight stashing: every forward runs
+    on the current weights W_t = W0 - t eta g and the backward of the same
+    mini-batch computes dX from exactly those weights, although the stage has
+    applied N - 1 - k further updates in between."""
+    from paper_1809_02839_amd.pipeline import Pipeline, stage_task_order
+    batch, fin, fout = 8, 16, 8
+    spec = synth.StageSpec("fc", "fp32", "none", k, N, batch, 1, (fin, fout, fout), 2.0 ** -7, 0.875, "stash")
+    rng = np.random.default_rng(7)
+    X = (rng.integers(-1, 2, size=(batch, fin)) * 2.0 ** -3).astype(np.float32)
+    dY = (rng.integers(-1, 2, size=(batch, fout)) * 2.0 ** -5).astype(np.float32)
+    W0 = np.concatenate([rng.integers(-64, 65, size=fout * fin) * 2.0 ** -12, np.full(fout, 4.0)]).astype(np.float32)
+    g = np.concatenate([(dY.T.astype(np.float64) @ X).reshape(-1), dY.sum(axis=0)]).astype(np.float32)
+    pipe = Pipeline([spec], [W0], v0s=[g])
+    eta = float(np.float32(spec.lr))
+    M = 10
+    out = pipe.run(M, lambda sp, m: (X, dY, None), keep_io=True)
+    torch.cuda.synchronize()
+    done, at_forward = 0, {}
+    for kind, m in stage_task_order(k, N, M):
+        if kind == "F":
+            at_forward[m] = done
+            Wt = (W0.astype(np.float64) - done * eta * g).astype(np.float32)
+            w, b = Wt[:fout * fin].reshape(fout, fin), Wt[fout * fin:]
+            assert np.array_equal(out["y"][(k, m)].cpu().numpy(), np.maximum(X @ w.T + b, 0))
+        else:
+            Wt = (W0.astype(np.float64) - at_forward[m] * eta * g).astype(np.float32)
+            w = Wt[:fout * fin].reshape(fout, fin)
+            assert np.array_equal(out["dx"][(k, m)].cpu().numpy(), dY @ w)
+            done += 1
     pipe.destroy()

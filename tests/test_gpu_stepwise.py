@@ -34,3 +34,29 @@ def test_stepwise_full_size(name):
     print(f"[stepwise-full] {name} steps={FULL[name]}", flush=True)
     worst = run_stepwise(wl, FULL[name], torch, derived=wl.stages[0].dtype == "bf16")
     print(f"[stepwise-full] {name}: {worst.report()}", flush=True)
+
+
+def _with_policy(wl, policy):
+    import dataclasses
+    return synth.Workload(f"{wl.name}/{policy}", tuple(dataclasses.replace(s, policy=policy) for s in wl.stages),
+                          wl.steps)
+
+
+@pytest.mark.parametrize("policy", ["vanilla", "stash"])
+@pytest.mark.parametrize("name", ["mlp3_small", "vgg_conv_small", "resnet_bottleneck_small",
+                                  "transformer_enc_small", "reslstm_small"])
+def test_stepwise_small_policies(name, policy):
+    """The Vanilla and weight-stashing pipelines of Section 4.2 on the same
+    stage kinds: every task against the oracle's recomputation of it."""
+    wl = _with_policy(synth.ALL_WORKLOADS[name], policy)
+    print(f"[stepwise] {wl.name}", flush=True)
+    worst = run_stepwise(wl, wl.steps, torch, derived=wl.stages[0].dtype == "bf16")
+    print(f"[stepwise] {wl.name}: {worst.report()}", flush=True)
+
+
+@pytest.mark.parametrize("policy", ["vanilla", "stash"])
+def test_stepwise_full_size_vgg_policies(policy):
+    wl = _with_policy(synth.WORKLOADS["vgg_conv"], policy)
+    print(f"[stepwise-full] {wl.name} steps=4", flush=True)
+    worst = run_stepwise(wl, 4, torch, derived=True)
+    print(f"[stepwise-full] {wl.name}: {worst.report()}", flush=True)

@@ -181,3 +181,65 @@ def test_s0_pipeline_equals_sequential_momentum_sgd_torch():
         opt.step()
     flat = np.concatenate([p.detach().numpy().reshape(-1) for p in params])
     np.testing.assert_allclose(r["W"][0], flat, rtol=2e-6, atol=2e-7)
+
+
+# ------------------------------------------- staleness policies (Section 4.2) ----
+
+@pytest.mark.parametrize("policy", ["vanilla", "stash"])
+@pytest.mark.parametrize("k,N", [(0, 3), (1, 3), (2, 3), (0, 4), (1, 4), (3, 4)])
+def test_closed_form_constant_gradient_policies(policy, k, N):
+    """Same dyadic closed form as above (W_t = W0 - t eta g exactly). Vanilla
+    model parallelism runs every pass on the weights current at that pass;
+    weight stashing runs the forward on the current weights and the backward on
+    the forward's weights (Section 3.2, the PipeDream example). The forward
+    outputs and backward dX must match those weight versions exactly."""
+    spec, X, dY, W0, g = _fc_closed_form_setup(k, N)
+    spec = dataclasses.replace(spec, policy=policy)
+    wl = synth.Workload("closed_form", (spec,), steps=12)
+    eta = spec.lr
+    r = trajectory.run(wl, W0=[W0], v0=[g], inputs=lambda s, m: (X, dY, None), keep_io=True)
+    done, at_forward = 0, {}
+    for kind, m in schedule.stage_tasks(k, N, wl.steps):
+        if kind == "F":
+            at_forward[m] = done
+            P = stages.unpack(spec, W0 - done * eta * g)
+            assert np.array_equal(r["y"][(k, m)], np.maximum(X @ P["fc0.weight"].T + P["fc0.bias"], 0))
+        else:
+            version = at_forward[m] if policy == "stash" else done
+            Wt = stages.unpack(spec, W0 - version * eta * g)
+            assert np.array_equal(r["dx"][(k, m)], dY @ Wt["fc0.weight"])
+            done += 1
+
+
+def test_policies_coincide_without_staleness():
+    """With one stage (N = 1) nothing is stale: F(m) and B(m) are adjacent and
+    Eq. 5 / Eq. 6 give s = 0, so SpecTrain, Vanilla and weight stashing produce
+    the same trajectory bit for bit."""
+    base = synth.StageSpec("fc", "fp32", "ce", 0, 1, 7, 3, (37, 10, 50), 0.05, 0.9)
+    runs = {}
+    for policy in ("spectrain", "vanilla", "stash"):
+        spec = dataclasses.replace(base, policy=policy)
+        runs[policy] = trajectory.run(synth.Workload("p", (spec,), steps=6), W0=[synth.initial_params(base)])
+    for policy in ("vanilla", "stash"):
+        assert np.array_equal(runs[policy]["W"][0], runs["spectrain"]["W"][0])
+        assert all(runs[policy]["loss"][m] == runs["spectrain"]["loss"][m] for m in range(6))
+
+
+@pytest.mark.parametrize("N", [2, 3, 4])
+def test_stash_staleness_is_updates_between_passes(N):
+    """Brute force over the stage order: under weight stashing the backward of
+    mini-batch m at stage k runs on weights that are as many updates old as
+    the stage performed between F_k(m) and B_k(m) (N - 1 - k in steady state),
+    while SpecTrain's backward prediction aims s_b updates ahead of the current
+    weights (Eq. 6)."""
+    M = 3 * N
+    for k in range(N):
+        tasks = schedule.stage_tasks(k, N, M)
+        pos = {t: i for i, t in enumerate(tasks)}
+        for m in range(N, M - N):
+            between = sum(1 for kind, _ in tasks[pos[("F", m)] + 1:pos[("B", m)]] if kind == "B")
+            assert between == N - 1 - k
+        assert method.staleness_versions("stash", k, N) == (0, 0)
+        assert method.staleness_versions("vanilla", k, N) == (0, 0)
+        assert method.staleness_versions("spectrain", k, N) == (method.version_difference(k, N, True),
+                                                                method.version_difference(k, N, False))
