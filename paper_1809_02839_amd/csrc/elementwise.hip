@@ -306,7 +306,6 @@ __global__ __launch_bounds__(NT) void softmax_bwd_kernel(const float* P, const f
 }
 
 // ------------------------------------------------------------ LSTM cell ----
-__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + expf(-x)); }
 
 __global__ void lstm_cell_fwd_kernel(const float* z, const float* c_prev, int B, int H, float* gates, float* c,
                                      bf16_t* h) {
@@ -314,10 +313,10 @@ __global__ void lstm_cell_fwd_kernel(const float* z, const float* c_prev, int B,
   for (long t = static_cast<long>(blockIdx.x) * NT + threadIdx.x; t < n; t += static_cast<long>(gridDim.x) * NT) {
     const int b = static_cast<int>(t / H), j = static_cast<int>(t - static_cast<long>(b) * H);
     const long zb = static_cast<long>(b) * 4 * H;
-    const float i = sigm(z[zb + j]);
-    const float f = sigm(z[zb + H + j]);
+    const float i = sigmoidf(z[zb + j]);
+    const float f = sigmoidf(z[zb + H + j]);
     const float g = tanhf(z[zb + 2 * H + j]);
-    const float o = sigm(z[zb + 3 * H + j]);
+    const float o = sigmoidf(z[zb + 3 * H + j]);
     const float cp = c_prev ? c_prev[t] : 0.0f;
     const float cn = fmaf(f, cp, i * g);
     gates[zb + j] = i;

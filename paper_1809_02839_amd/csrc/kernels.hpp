@@ -77,6 +77,17 @@ hipError_t fused_update(float* W, float* v, const float* g, void* what_f, void* 
 hipError_t predict_slot(const float* W, const float* v, void* what, int what_dtype, long n, float lr, int s_pred,
                         hipStream_t s);
 
+// Fused residual-LSTM recurrence steps (supported for B <= 64 and H a
+// multiple of 32): forward z_t = zx_t + h_{t-1} W_h^T and the cell in one
+// launch; backward dh_t = dh_out_t + dz_{t+1} W_h (W_h^T given) and the cell
+// backward in one launch. Null h_prev / dz_next / c_prev mark the first step.
+bool lstm_step_supported(int B, int H);
+hipError_t lstm_step_fwd(const float* zx_t, const bf16_t* h_prev, const bf16_t* Wh, const float* c_prev, int B, int H,
+                         float* gates_t, float* c_t, bf16_t* h_t, hipStream_t s);
+hipError_t lstm_step_bwd(const bf16_t* dz_next, const bf16_t* WhT, const bf16_t* dh_out, const float* gates_t,
+                         const float* c_t, const float* c_prev, int B, int H, float* dc, bf16_t* dz_t, hipStream_t s);
+hipError_t transpose_bf16(const bf16_t* X, int R, int C, bf16_t* Y, hipStream_t s);   // R, C multiples of 32
+
 // Row chunking of the two-pass column reductions (column sums, layer-norm
 // parameter gradients) and the float32 workspace each pass needs.
 constexpr int COLSUM_ROWS = 64;   // rows summed per block in the first pass

@@ -290,7 +290,8 @@ void Stage::plan_buffers() {
       ws = {static_cast<size_t>(TB * 4 * H * 4), static_cast<size_t>(ce ? TB * V * 4 : 0),
             static_cast<size_t>(TB * H * 2),     static_cast<size_t>(TB * H * 2),
             static_cast<size_t>(TB * 4 * H * 2), static_cast<size_t>(B * H * 4),
-            static_cast<size_t>(B * H * 4),      static_cast<size_t>(TB * 4)};
+            static_cast<size_t>(B * H * 4),      static_cast<size_t>(TB * 4),
+            static_cast<size_t>(lstm_step_supported(B, static_cast<int>(H)) ? 4 * H * H * 2 : 0)};
       partial = std::max(partial_floats(TB, 4 * H), ce ? partial_floats(TB, V) : 0);
       break;
     }
@@ -908,7 +909,9 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
 // per layer stash ids 4*l + j: 0 gates (f32 [T,B,4H]), 1 c (f32), 2 h (bf16),
 // 3 layer output u_{l+1} (bf16); id 4L: dlogits (bf16) with a CE head.
 // workspace: 0 zx (f32), 1 logits (f32), 2/3 du ping-pong, 4 dz (bf16),
-// 5 dh_rec (f32), 6 dc (f32), 7 row losses, 8 partials.
+// 5 dh_rec (f32), 6 dc (f32), 7 row losses, 8 W_h^T (bf16, fused steps),
+// 9 partials. With B <= 64 and H a multiple of 32 every recurrent step is one
+// fused launch (contraction + cell); otherwise a GEMM and a cell launch.
 void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
   const int L = d_.num_layers, B = d_.batch, I = d_.dims[0], H = d_.dims[1], T = d_.dims[2], V = d_.dims[3];
   const bool ce = d_.head == SPECTRAIN_HEAD_CE;
@@ -926,7 +929,14 @@ void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, fl
     gx.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 2));
     gx.epi.out_f32 = zx;
     gemm(gx);
-    for (int t = 0; t < T; ++t) {
+    const bool fused = lstm_step_supported(B, H);
+    for (int t = 0; t < T && fused; ++t) {
+      const long o = static_cast<long>(t) * B;
+      LAUNCH("lstm_step", t > 0 ? 8.0 * B * H * H : 0.0, 0,
+             lstm_step_fwd(zx + o * 4 * H, t > 0 ? hs + (o - B) * H : nullptr, static_cast<const bf16_t*>(wf(p + 1)),
+                           t > 0 ? c + (o - B) * H : nullptr, B, H, gates + o * 4 * H, c + o * H, hs + o * H, s_));
+    }
+    for (int t = 0; t < T && !fused; ++t) {
       float* zt = zx + static_cast<long>(t) * B * 4 * H;
       if (t > 0) {
         GemmDesc gh = gd(B, 4 * H, H, opK(hs + static_cast<long>(t - 1) * B * H, H), opK(wf(p + 1), H), 4 * H);
@@ -956,7 +966,7 @@ void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
   const bool ce = d_.head == SPECTRAIN_HEAD_CE;
   const long TB = static_cast<long>(T) * B;
   const Slot& sl = slots_[slot];
-  float* part = ws<float>(8);
+  float* part = ws<float>(9);
   const void* du = dy;
   int pp = 2;
   if (ce) {
@@ -983,7 +993,19 @@ void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
     const float* c = stash<float>(slot, q + 1);
     const bf16_t* hs = stash<bf16_t>(slot, q + 2);
     LAUNCH("clear_dc", 0, 0, fill_f32(dc, 0.0f, static_cast<long>(B) * H, s_));
-    for (int t = T - 1; t >= 0; --t) {
+    const bool fused = lstm_step_supported(B, H);
+    if (fused) {
+      bf16_t* whT = ws<bf16_t>(8);
+      LAUNCH("transpose", 0, 8.0 * H * H * 2, transpose_bf16(static_cast<const bf16_t*>(wb(p + 1)), 4 * H, H, whT, s_));
+      for (int t = T - 1; t >= 0; --t) {
+        const long o = static_cast<long>(t) * B;
+        LAUNCH("lstm_step_bwd", t < T - 1 ? 8.0 * B * H * H : 0.0, 0,
+               lstm_step_bwd(t < T - 1 ? dz + (o + B) * 4 * H : nullptr, whT, static_cast<const bf16_t*>(du) + o * H,
+                             gates + o * 4 * H, c + o * H, t > 0 ? c + (o - B) * H : nullptr, B, H, dc, dz + o * 4 * H,
+                             s_));
+      }
+    }
+    for (int t = T - 1; t >= 0 && !fused; --t) {
       const long o = static_cast<long>(t) * B;
       LAUNCH("lstm_cell_bwd", 0, 0, lstm_cell_bwd(static_cast<const bf16_t*>(du) + o * H, t < T - 1 ? dh_rec : nullptr, gates + o * 4 * H,
                               c + o * H, t > 0 ? c + (o - B) * H : nullptr, B, H, dc, dz + o * 4 * H, s_));

@@ -221,6 +221,8 @@ SMALL_WORKLOADS: Dict[str, Workload] = {
     "transformer_enc_small": _single("transformer_enc_small", "transformer", "bf16", "none", 1, 4, 3, 2,
                                      (64, 2, 136, 40), 2e-3),
     "reslstm_small": _single("reslstm_small", "reslstm", "bf16", "ce", 3, 4, 5, 2, (48, 48, 6, 104), 5e-2),
+    # hidden size a multiple of 32 and batch <= 64: the fused recurrent steps
+    "reslstm_mid": _single("reslstm_mid", "reslstm", "bf16", "ce", 3, 4, 24, 2, (96, 96, 7, 136), 5e-2),
 }
 
 ALL_WORKLOADS: Dict[str, Workload] = {**WORKLOADS, **SMALL_WORKLOADS}

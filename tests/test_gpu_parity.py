@@ -38,7 +38,7 @@ def _gpu_trajectory(wl, steps=None):
 # same 20 steps) stays far below the bound; the ReLU-dominated reduced conv,
 # bottleneck and transformer stages amplify single mask decisions and are
 # covered step by step in test_gpu_stepwise.py.
-TRAJ = ["mlp3", "mlp3_small", "reslstm_small"]
+TRAJ = ["mlp3", "mlp3_small", "reslstm_small", "reslstm_mid"]
 
 
 @pytest.mark.parametrize("name", TRAJ)
