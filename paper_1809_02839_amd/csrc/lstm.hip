@@ -84,6 +84,16 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void lstm_step_fwd_kernel(const flo
   __shared__ float zs[16][17];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int u0 = blockIdx.x * FWD_UNITS, r0 = blockIdx.y * 16;
+  const long H4 = 4L * H;
+  // the cell's own operands are loaded first so their latency overlaps the contraction
+  const int crow = r0 + tid / FWD_UNITS, cuu = tid % FWD_UNITS, cu = u0 + cuu;
+  const bool cell = tid < 16 * FWD_UNITS && crow < B;
+  float zx[4] = {0.0f, 0.0f, 0.0f, 0.0f}, cp = 0.0f;
+  if (cell) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) zx[g] = zx_t[crow * H4 + g * H + cu];
+    if (c_prev) cp = c_prev[static_cast<long>(crow) * H + cu];
+  }
   if (h_prev) {
     // block column c = 4 unit + gate is the weight row gate * H + u0 + unit;
     // rows past B read row 0 (valid memory) and are never read back
@@ -93,25 +103,19 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void lstm_step_fwd_kernel(const flo
     const bf16_t* brow = Wh + static_cast<long>((col & 3) * H + u0 + (col >> 2)) * H + kq;
     reduce_tile<FWD_WAVES>(contract16<FWD_WAVES>(arow, brow, H, wave), red, zs, wave, lane, tid);
   }
-  const long H4 = 4L * H;
-  if (tid < 16 * FWD_UNITS) {
-    const int row = r0 + tid / FWD_UNITS, uu = tid % FWD_UNITS, u = u0 + uu;
-    if (row < B) {
-      const float* zr = zx_t + row * H4 + u;
-      float z[4];
+  if (cell) {
+    float z[4];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) z[g] = zr[g * H] + (h_prev ? zs[row - r0][4 * uu + g] : 0.0f);
-      const float i = sigmoidf(z[0]), f = sigmoidf(z[1]), gg = tanhf(z[2]), o = sigmoidf(z[3]);
-      const float cp = c_prev ? c_prev[static_cast<long>(row) * H + u] : 0.0f;
-      const float cn = fmaf(f, cp, i * gg);
-      float* gr = gates_t + row * H4 + u;
-      gr[0] = i;
-      gr[H] = f;
-      gr[2 * H] = gg;
-      gr[3 * H] = o;
-      c_t[static_cast<long>(row) * H + u] = cn;
-      h_t[static_cast<long>(row) * H + u] = f32_to_bf16(o * tanhf(cn));
-    }
+    for (int g = 0; g < 4; ++g) z[g] = zx[g] + (h_prev ? zs[crow - r0][4 * cuu + g] : 0.0f);
+    const float i = sigmoidf(z[0]), f = sigmoidf(z[1]), gg = tanhf(z[2]), o = sigmoidf(z[3]);
+    const float cn = fmaf(f, cp, i * gg);
+    float* gr = gates_t + crow * H4 + cu;
+    gr[0] = i;
+    gr[H] = f;
+    gr[2 * H] = gg;
+    gr[3 * H] = o;
+    c_t[static_cast<long>(crow) * H + cu] = cn;
+    h_t[static_cast<long>(crow) * H + cu] = f32_to_bf16(o * tanhf(cn));
   }
 }
 
@@ -125,6 +129,22 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void lstm_step_bwd_kernel(const bf1
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int u0 = blockIdx.x * BWD_UNITS, r0 = blockIdx.y * 16;
   const long H4 = 4L * H;
+  // the cell's own operands are loaded first so their latency overlaps the contraction
+  const int crow = r0 + tid / BWD_UNITS, cuu = tid % BWD_UNITS, cu = u0 + cuu;
+  const bool cell = tid < 16 * BWD_UNITS && crow < B;
+  const long t1 = static_cast<long>(crow) * H + cu;
+  float gi = 0.0f, gf = 0.0f, gg = 0.0f, go = 0.0f, ct = 0.0f, cpv = 0.0f, dcv = 0.0f, dho = 0.0f;
+  if (cell) {
+    const float* gr = gates_t + crow * H4 + cu;
+    gi = gr[0];
+    gf = gr[H];
+    gg = gr[2 * H];
+    go = gr[3 * H];
+    ct = c_t[t1];
+    if (c_prev) cpv = c_prev[t1];
+    dcv = dc[t1];
+    dho = bf16_to_f32(dh_out[t1]);
+  }
   if (dz_next) {
     // dh_rec[row][u0 + n] = sum_k dz_{t+1}[row][k] W_h[k][u0 + n] = sum_k dz[row][k] W_h^T[u0 + n][k]
     const int kq = 8 * (lane >> 4), row = r0 + (lane & 15);
@@ -132,24 +152,18 @@ __global__ __launch_bounds__(64 * BWD_WAVES) void lstm_step_bwd_kernel(const bf1
     const bf16_t* brow = WhT + static_cast<long>(u0 + (lane & 15)) * H4 + kq;
     reduce_tile<BWD_WAVES>(contract16<BWD_WAVES>(arow, brow, static_cast<int>(H4), wave), red, dhs, wave, lane, tid);
   }
-  if (tid < 16 * BWD_UNITS) {
-    const int row = r0 + tid / BWD_UNITS, uu = tid % BWD_UNITS, u = u0 + uu;
-    if (row < B) {
-      const long t1 = static_cast<long>(row) * H + u;
-      const float* gr = gates_t + row * H4 + u;
-      const float i = gr[0], f = gr[H], g = gr[2 * H], o = gr[3 * H];
-      const float dh = bf16_to_f32(dh_out[t1]) + (dz_next ? dhs[row - r0][uu] : 0.0f);
-      const float tc = tanhf(c_t[t1]);
-      const float d_o = dh * tc;
-      const float dct = dc[t1] + dh * o * (1.0f - tc * tc);
-      const float di = dct * g, dg = dct * i, df = dct * (c_prev ? c_prev[t1] : 0.0f);
-      dc[t1] = dct * f;
-      bf16_t* dr = dz_t + row * H4 + u;
-      dr[0] = f32_to_bf16(di * i * (1.0f - i));
-      dr[H] = f32_to_bf16(df * f * (1.0f - f));
-      dr[2 * H] = f32_to_bf16(dg * (1.0f - g * g));
-      dr[3 * H] = f32_to_bf16(d_o * o * (1.0f - o));
-    }
+  if (cell) {
+    const float dh = dho + (dz_next ? dhs[crow - r0][cuu] : 0.0f);
+    const float tc = tanhf(ct);
+    const float d_o = dh * tc;
+    const float dct = dcv + dh * go * (1.0f - tc * tc);
+    const float di = dct * gg, dg = dct * gi, df = dct * cpv;
+    dc[t1] = dct * gf;
+    bf16_t* dr = dz_t + crow * H4 + cu;
+    dr[0] = f32_to_bf16(di * gi * (1.0f - gi));
+    dr[H] = f32_to_bf16(df * gf * (1.0f - gf));
+    dr[2 * H] = f32_to_bf16(dg * (1.0f - gg * gg));
+    dr[3 * H] = f32_to_bf16(d_o * go * (1.0f - go));
   }
 }
 
