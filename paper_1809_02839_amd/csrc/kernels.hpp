@@ -88,6 +88,17 @@ hipError_t lstm_step_bwd(const bf16_t* dz_next, const bf16_t* WhT, const bf16_t*
                          const float* c_t, const float* c_prev, int B, int H, float* dc, bf16_t* dz_t, hipStream_t s);
 hipError_t transpose_bf16(const bf16_t* X, int R, int C, bf16_t* Y, hipStream_t s);   // R, C multiples of 32
 
+// Fused attention core for sequence length 128 and head dimension 64 (one
+// block per batch x head), on the packed qkv [B*S][3d] of a layer. Forward
+// writes ctx [B*S][d] and the softmax row statistics (max, 1/sum) as float32
+// [B*heads*S][2]; backward recomputes P from them and writes dQ, dK, dV into
+// dqkv [B*S][3d]. Other shapes use the batched GEMM path.
+bool attention_fused_supported(int seq, int head_dim, int d);
+hipError_t attention_fwd(const bf16_t* qkv, int batch, int heads, int d, float scale, float* stats, bf16_t* ctx,
+                         hipStream_t s);
+hipError_t attention_bwd(const bf16_t* qkv, const bf16_t* dctx, const float* stats, int batch, int heads, int d,
+                         float scale, bf16_t* dqkv, hipStream_t s);
+
 // Row chunking of the two-pass column reductions (column sums, layer-norm
 // parameter gradients) and the float32 workspace each pass needs.
 constexpr int COLSUM_ROWS = 64;   // rows summed per block in the first pass

@@ -258,9 +258,12 @@ void Stage::plan_buffers() {
       break;
     }
     case SPECTRAIN_KIND_TRANSFORMER: {
-      const long d = dm[0], H = dm[1], F = dm[2], S = dm[3], T = B * S, BHSS = B * H * S * S;
+      const long d = dm[0], H = dm[1], F = dm[2], S = dm[3], T = B * S;
+      const bool fused = attention_fused_supported(static_cast<int>(S), static_cast<int>(d / H), static_cast<int>(d));
+      // the fused attention keeps only softmax row statistics; the GEMM path P (f32, bf16) and the scores
+      const long BHSS = fused ? 0 : B * H * S * S;
       for (int l = 0; l < L; ++l) {
-        size_t s[13] = {static_cast<size_t>(T * 3 * d * 2), static_cast<size_t>(BHSS * 4),
+        size_t s[13] = {static_cast<size_t>(T * 3 * d * 2), static_cast<size_t>(fused ? B * H * S * 2 * 4 : BHSS * 4),
                         static_cast<size_t>(BHSS * 2),      static_cast<size_t>(T * d * 2),
                         static_cast<size_t>(T * d * 2),     static_cast<size_t>(T * 4),
                         static_cast<size_t>(T * 4),         static_cast<size_t>(T * d * 2),
@@ -699,8 +702,9 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
 
 // ======================================================= TRANSFORMER ====
 // Post-LN encoder layer; per layer stash ids 13*l + j:
-// 0 qkv, 1 P (f32), 2 P (bf16), 3 ctx, 4 r1, 5 mean1, 6 rstd1, 7 h, 8 f1,
-// 9 r2, 10 mean2, 11 rstd2, 12 layer output (l < L-1).
+// 0 qkv, 1 P (f32; with the fused attention core the softmax row statistics),
+// 2 P (bf16; unused with the fused core), 3 ctx, 4 r1, 5 mean1, 6 rstd1, 7 h,
+// 8 f1, 9 r2, 10 mean2, 11 rstd2, 12 layer output (l < L-1).
 void Stage::fwd_tfm(int slot, const void* x, void* y) {
   const int L = d_.num_layers, B = d_.batch, d = d_.dims[0], Hh = d_.dims[1], F = d_.dims[2], S = d_.dims[3];
   const int T = B * S, dh = d / Hh;
@@ -722,6 +726,9 @@ void Stage::fwd_tfm(int slot, const void* x, void* y) {
     g.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 1));
     g.epi.out_bf16 = qkv;
     gemm(g);
+    if (attention_fused_supported(S, dh, d)) {
+      LAUNCH("attention", 4.0 * B * Hh * S * S * dh, 0, attention_fwd(qkv, B, Hh, d, scale, P, ctx, s_));
+    } else {
     // scores[b, h] = Q K^T * scale
     Operand qa = opK(qkv, 3 * d), kb = opK(qkv + d, 3 * d);
     qa.bs1 = kb.bs1 = static_cast<long>(S) * 3 * d;
@@ -748,6 +755,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y) {
     pv.epi.bs2 = dh;
     pv.epi.out_bf16 = ctx;
     gemm(pv);
+    }
     GemmDesc go = gd(T, d, d, opK(ctx, d), opK(wf(p + 2), d), d);
     go.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 3));
     go.epi.res_bf16 = static_cast<const bf16_t*>(a);
@@ -828,7 +836,10 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     xo.epi.out_bf16 = dctx;
     gemm(xo);
 
-    // attention backward, batched over (b, h)
+    // attention backward: fused, or batched GEMMs over (b, h)
+    if (attention_fused_supported(S, dh, d)) {
+      LAUNCH("attention_bwd", 10.0 * B * Hh * S * S * dh, 0, attention_bwd(qkv, dctx, P, B, Hh, d, scale, dqkv, s_));
+    } else {
     const long sS = static_cast<long>(S) * S, sHSS = static_cast<long>(Hh) * S * S;
     const long sQ = static_cast<long>(S) * 3 * d, sO = static_cast<long>(S) * d;
     {  // dV = P^T dO
@@ -889,6 +900,7 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
       g.epi.alpha = scale;
       g.epi.out_bf16 = dqkv + d;
       gemm(g);
+    }
     }
     GemmDesc wq = gd(3 * d, d, T, opR(dqkv, 3 * d), opR(a, d), d);
     wq.epi.out_f32 = grad(p);

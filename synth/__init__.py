@@ -220,6 +220,9 @@ SMALL_WORKLOADS: Dict[str, Workload] = {
                                        (72, 24, 7, 5), 1e-3),
     "transformer_enc_small": _single("transformer_enc_small", "transformer", "bf16", "none", 1, 4, 3, 2,
                                      (64, 2, 136, 40), 2e-3),
+    # sequence 128 and head dimension 64: the fused attention core
+    "transformer_enc_mid": _single("transformer_enc_mid", "transformer", "bf16", "none", 1, 4, 2, 2,
+                                   (128, 2, 256, 128), 2e-3),
     "reslstm_small": _single("reslstm_small", "reslstm", "bf16", "ce", 3, 4, 5, 2, (48, 48, 6, 104), 5e-2),
     # hidden size a multiple of 32 and batch <= 64: the fused recurrent steps
     "reslstm_mid": _single("reslstm_mid", "reslstm", "bf16", "ce", 3, 4, 24, 2, (96, 96, 7, 136), 5e-2),

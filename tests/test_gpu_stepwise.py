@@ -15,7 +15,7 @@ torch = pytest.importorskip("torch")
 
 
 @pytest.mark.parametrize("name", ["mlp3_small", "vgg_conv_small", "resnet_bottleneck_small",
-                                  "transformer_enc_small", "reslstm_small", "reslstm_mid"])
+                                  "transformer_enc_small", "transformer_enc_mid", "reslstm_small", "reslstm_mid"])
 def test_stepwise_small(name):
     wl = synth.ALL_WORKLOADS[name]
     print(f"[stepwise] {name}", flush=True)
