@@ -633,13 +633,13 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   // Split K when the tiles cannot give every CU two resident blocks (two
   // 4-wave blocks per CU hide each other's barrier and load stalls) and K is
   // long: as many splits as keep all blocks resident at once, each with at
-  // least 8 K steps.
+  // least 12 K steps (shorter slices cost more in the reduction than they gain).
   constexpr long kTargetBlocks = 2 * 256;
   int splits = 1;
   const long tiles = static_cast<long>(a.tiles_total) * d.batch;
-  if (d.workspace && tiles < kTargetBlocks && d.K >= 2 * 8 * BK) {
+  if (d.workspace && tiles < kTargetBlocks && d.K >= 2 * 12 * BK) {
     splits = static_cast<int>(kTargetBlocks / tiles);   // all blocks resident in one round
-    splits = std::min(splits, d.K / (8 * BK));
+    splits = std::min(splits, d.K / (12 * BK));
     splits = std::min(splits, MAX_SPLITS);
     const long per = static_cast<long>(d.batch) * d.M * d.N * 4;
     while (splits > 1 && per * splits > static_cast<long>(d.workspace_bytes)) --splits;
