@@ -72,6 +72,8 @@ def prediction_rmse(spec, steps: int, s_values: Sequence[int] = (1, 2, 3), W0: O
     out = {s: {"t": [], "predicted": [], "stale": []} for s in s_values}
 
     def on_update(k, t, st):
+        if t % 10 == 0:
+            print(f"[rmse] update {t} of {steps}", file=sys.stderr, flush=True)
         W, _ = st.get_state()
         history[t] = W
         history.pop(t - smax - 1, None)
@@ -140,6 +142,7 @@ def policy_losses(workload, steps: int, policies: Sequence[str] = ("spectrain", 
         out = pipe.run(steps, draw)
         torch.cuda.synchronize()
         losses[policy] = [out["loss"][m].item() for m in range(steps)]
+        print(f"[policies] {policy}: {steps} mini-batches", file=sys.stderr, flush=True)
         pipe.destroy()
     return losses
 
