@@ -50,6 +50,21 @@ __global__ void mask_bf16_kernel(const bf16_t* src, const bf16_t* mask, bf16_t* 
   for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n; i += static_cast<long>(gridDim.x) * NT)
     dst[i] = bf16_to_f32(mask[i]) > 0.0f ? src[i] : static_cast<bf16_t>(0);
 }
+// 8 values per thread with 16-byte accesses (n % 8 == 0, 16-byte aligned).
+__global__ void mask_bf16x8_kernel(const uint4* src, const uint4* mask, uint4* dst, long n8) {
+  for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n8; i += static_cast<long>(gridDim.x) * NT) {
+    const uint4 a = src[i], m = mask[i];
+    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, mv[4] = {m.x, m.y, m.z, m.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = bf16_to_f32(static_cast<bf16_t>(mv[q] & 0xffff)) > 0.0f ? 0x0000ffffu : 0u;
+      const uint32_t hi = bf16_to_f32(static_cast<bf16_t>(mv[q] >> 16)) > 0.0f ? 0xffff0000u : 0u;
+      o[q] = av[q] & (lo | hi);
+    }
+    dst[i] = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
 __global__ void mask_f32_kernel(const float* src, const float* mask, float* dst, long n) {
   for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n; i += static_cast<long>(gridDim.x) * NT)
     dst[i] = mask[i] > 0.0f ? src[i] : 0.0f;
@@ -370,7 +385,11 @@ __global__ void fill_kernel(float* x, float v, long n) {
 
 hipError_t mask_relu_grad(const void* src, const void* mask, void* dst, long n, int dtype, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  if (dtype == 1)
+  auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  if (dtype == 1 && n % 8 == 0 && al16(src) && al16(mask) && al16(dst))
+    hipLaunchKernelGGL(mask_bf16x8_kernel, dim3(blocks_for(n / 8, 1)), dim3(NT), 0, s, static_cast<const uint4*>(src),
+                       static_cast<const uint4*>(mask), static_cast<uint4*>(dst), n / 8);
+  else if (dtype == 1)
     hipLaunchKernelGGL(mask_bf16_kernel, dim3(blocks_for(n, 4)), dim3(NT), 0, s, static_cast<const bf16_t*>(src),
                        static_cast<const bf16_t*>(mask), static_cast<bf16_t*>(dst), n);
   else

@@ -612,6 +612,23 @@ namespace {
 // Launch parameters of one GEMM: tile counts, the split of K and the device
 // view of both operands. Returns false (with err set) for a shape the kernel
 // cannot address; err stays hipSuccess for an empty problem.
+// Split K when the tiles cannot give every CU two resident blocks (two
+// 4-wave blocks per CU hide each other's barrier and load stalls) and K is
+// long: as many splits as keep all blocks resident at once, each with at
+// least 12 K steps (shorter slices cost more in the reduction than they gain),
+// and no more than the workspace holds.
+int split_rule(int M, int N, int K, int batch, size_t workspace_bytes) {
+  constexpr long kTargetBlocks = 2 * 256;
+  const long tiles = static_cast<long>((N + BN - 1) / BN) * ((M + BM - 1) / BM) * batch;
+  if (tiles >= kTargetBlocks || K < 2 * 12 * BK) return 1;
+  int splits = static_cast<int>(kTargetBlocks / tiles);   // all blocks resident in one round
+  splits = std::min(splits, K / (12 * BK));
+  splits = std::min(splits, MAX_SPLITS);
+  const long per = static_cast<long>(batch) * M * N * 4;
+  while (splits > 1 && per * splits > static_cast<long>(workspace_bytes)) --splits;
+  return std::max(splits, 1);
+}
+
 bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   err = hipSuccess;
   if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return false;
@@ -630,20 +647,7 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   a.zdiv = zdiv;
   a.tiles_n = (d.N + BN - 1) / BN;
   a.tiles_total = a.tiles_n * ((d.M + BM - 1) / BM);
-  // Split K when the tiles cannot give every CU two resident blocks (two
-  // 4-wave blocks per CU hide each other's barrier and load stalls) and K is
-  // long: as many splits as keep all blocks resident at once, each with at
-  // least 12 K steps (shorter slices cost more in the reduction than they gain).
-  constexpr long kTargetBlocks = 2 * 256;
-  int splits = 1;
-  const long tiles = static_cast<long>(a.tiles_total) * d.batch;
-  if (d.workspace && tiles < kTargetBlocks && d.K >= 2 * 12 * BK) {
-    splits = static_cast<int>(kTargetBlocks / tiles);   // all blocks resident in one round
-    splits = std::min(splits, d.K / (12 * BK));
-    splits = std::min(splits, MAX_SPLITS);
-    const long per = static_cast<long>(d.batch) * d.M * d.N * 4;
-    while (splits > 1 && per * splits > static_cast<long>(d.workspace_bytes)) --splits;
-  }
+  const int splits = d.workspace ? split_rule(d.M, d.N, d.K, d.batch, d.workspace_bytes) : 1;
   const int ksteps = (d.K + BK - 1) / BK;
   a.k_per_split = ((ksteps + splits - 1) / splits) * BK;
   a.splits = splits;
@@ -703,6 +707,11 @@ hipError_t launch_reduce(const KArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+int gemm_bf16_split_rule(int M, int N, int K, int batch, size_t workspace_bytes) {
+  if (M <= 0 || N <= 0 || K <= 0 || batch <= 0) return 1;
+  return split_rule(M, N, K, batch, workspace_bytes);
+}
 
 int gemm_bf16_splits(const GemmDesc& d) {
   KArgs a;

@@ -66,6 +66,8 @@ struct GemmDesc {
 enum { GEMM_MAIN = 1, GEMM_REDUCE = 2, GEMM_ALL = 3 };
 hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s, int phases = GEMM_ALL);
 int gemm_bf16_splits(const GemmDesc& d);   // K splits the launch will use (1 = none)
+// The same count from the shape alone, for a workspace of workspace_bytes.
+int gemm_bf16_split_rule(int M, int N, int K, int batch, size_t workspace_bytes);
 hipError_t gemm_f32(const GemmDesc& d, hipStream_t s);
 
 // ------------------------------------------------------- update/predict ----
@@ -76,6 +78,23 @@ hipError_t fused_update(float* W, float* v, const float* g, void* what_f, void* 
                         long n, float lr, float gamma, int s_f, int s_b, int* flag, hipStream_t s);
 hipError_t predict_slot(const float* W, const float* v, void* what, int what_dtype, long n, float lr, int s_pred,
                         hipStream_t s);
+
+// The same update with the gradient of some tensors still in split-K form:
+// segment i covers arena elements [off, off + n) whose gradient is the sum,
+// in split order, of `splits` float32 planes part[s * n + j] (the K-slice
+// partials of the filter-gradient GEMM, row-major like the tensor). Elements
+// outside every segment read g. Offsets and lengths are multiples of 8;
+// segments are sorted and disjoint. The sum is the one the split-K reduction
+// forms, so W, v and both slots are bitwise those of reduce-then-update.
+constexpr int UPDATE_MAX_SEGMENTS = 24;
+struct UpdateSegment {
+  long off = 0, n = 0;
+  const float* part = nullptr;
+  int splits = 0;
+};
+hipError_t fused_update_partials(float* W, float* v, const float* g, const UpdateSegment* segs, int nsegs,
+                                 void* what_f, void* what_b, int what_dtype, long n, float lr, float gamma, int s_f,
+                                 int s_b, int* flag, hipStream_t s);
 
 // Fused residual-LSTM recurrence steps (supported for B <= 64 and H a
 // multiple of 32): forward z_t = zx_t + h_{t-1} W_h^T and the cell in one

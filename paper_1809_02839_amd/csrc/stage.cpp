@@ -147,7 +147,7 @@ void Stage::build_layout() {
 const void* Stage::wf(int i) const { return static_cast<const char*>(what_[0]) + tensors_[i].off * esz_; }
 const void* Stage::wb(int i) const { return static_cast<const char*>(bwd_weights_) + tensors_[i].off * esz_; }
 
-void Stage::gemm(const GemmDesc& d) {
+void Stage::gemm(const GemmDesc& d, bool defer) {
   const char* name = "gemm";
   const int ma = d.A.mode, mb = d.B.mode;
   if (ma == OP_K_CONV_FWD) name = "conv3x3_fwd";
@@ -166,6 +166,28 @@ void Stage::gemm(const GemmDesc& d) {
   if (!dt_) {
     LAUNCH(name, flops, 0, gemm_f32(dd, s_));
     return;
+  }
+  if (defer) {
+    const Epilogue& e = d.epi;
+    const long mn = static_cast<long>(d.M) * d.N;
+    const long off = e.out_f32 ? static_cast<long>(e.out_f32 - g_) : -1;
+    const bool plain = d.batch == 1 && e.out_f32 && !e.out_bf16 && !e.bias && !e.bias_bf16 && !e.res_f32 &&
+                       !e.res_bf16 && !e.mask && e.alpha == 1.0f && !e.relu && !e.accumulate && e.ldc == d.N;
+    const int splits = gemm_bf16_split_rule(d.M, d.N, d.K, d.batch, gemm_ws_bytes_);
+    if (plain && splits > 1 && off >= 0 && off + mn <= n_arena_ && off % 8 == 0 && mn % 8 == 0 &&
+        defer_used_ + splits * mn <= defer_cap_ && defer_segs_.size() < static_cast<size_t>(UPDATE_MAX_SEGMENTS)) {
+      dd.workspace = defer_ + defer_used_;
+      dd.workspace_bytes = static_cast<size_t>(splits * mn) * 4;
+      LAUNCH(name, flops, 0, gemm_bf16(dd, s_, GEMM_MAIN));
+      UpdateSegment sg;
+      sg.off = off;
+      sg.n = mn;
+      sg.part = dd.workspace;
+      sg.splits = splits;
+      defer_segs_.push_back(sg);
+      defer_used_ += splits * mn;
+      return;
+    }
   }
   LAUNCH(name, flops, 0, gemm_bf16(dd, s_, GEMM_MAIN));
   const int splits = gemm_bf16_splits(dd);
@@ -229,6 +251,7 @@ void Stage::plan_buffers() {
   std::vector<size_t> st, ws;   // byte sizes, indexed by buffer id
   auto partial_floats = [](long rows, long cols) { return column_sum_ws_floats(rows, cols); };
   long partial = 0;
+  gemm_ws_bytes_ = dt_ ? (64u << 20) : 0;
   switch (d_.kind) {
     case SPECTRAIN_KIND_FC: {
       const long C = dm[1], hid = dm[2], maxw = std::max<long>(std::max<long>(dm[0], dm[1]), dm[2]);
@@ -244,6 +267,11 @@ void Stage::plan_buffers() {
       for (int l = 1; l < L; ++l) st.push_back(P * dm[1] * esz_);
       const long cmax = std::max(dm[0], dm[1]);
       ws = {static_cast<size_t>(P * cmax * esz_), static_cast<size_t>(P * cmax * esz_)};
+      for (int l = 0; l < L && dt_; ++l) {   // filter-gradient partials, reduced by the update
+        const int C = l == 0 ? dm[0] : dm[1];
+        defer_cap_ += static_cast<long>(gemm_bf16_split_rule(dm[1], 9 * C, static_cast<int>(P), 1, gemm_ws_bytes_)) *
+                      dm[1] * 9 * C;
+      }
       break;
     }
     case SPECTRAIN_KIND_BOTTLENECK: {
@@ -300,8 +328,12 @@ void Stage::plan_buffers() {
     }
   }
   ws.push_back(static_cast<size_t>(std::max<long>(partial, 1) * 4));  // column-sum partials
-  gemm_ws_bytes_ = dt_ ? (64u << 20) : 0;
   ws.push_back(std::max<size_t>(gemm_ws_bytes_, 1));                   // split-K partials: last id
+  if (defer_cap_ > 0) {
+    const size_t o = defer_block_.add(static_cast<size_t>(defer_cap_) * 4);
+    defer_block_.allocate();
+    defer_ = defer_block_.at<float>(o);
+  }
   DeviceBlock probe;
   for (size_t b : st) stash_off_.push_back(probe.add(std::max<size_t>(b, 1)));
   for (size_t b : ws) ws_off_.push_back(ws_block_.add(std::max<size_t>(b, 1)));
@@ -478,9 +510,20 @@ void Stage::predict(int s, int slot) {
 
 void Stage::update(int s_f, int s_b) {
   if (!g_pending_) throw StageError(SPECTRAIN_ESTATE, "update without a gradient from a backward pass");
-  const double bytes = static_cast<double>(n_params_) * (12 + 8 + (s_f >= 0) * esz_ + (s_b >= 0) * esz_);
-  LAUNCH("fused_update", 0, bytes,
-         fused_update(W_, v_, g_, what_[0], what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_dev_, s_));
+  double bytes = static_cast<double>(n_params_) * (12 + 8 + (s_f >= 0) * esz_ + (s_b >= 0) * esz_);
+  if (defer_segs_.empty()) {
+    LAUNCH("fused_update", 0, bytes,
+           fused_update(W_, v_, g_, what_[0], what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_dev_, s_));
+  } else {
+    std::sort(defer_segs_.begin(), defer_segs_.end(),
+              [](const UpdateSegment& a, const UpdateSegment& b) { return a.off < b.off; });
+    for (const UpdateSegment& sg : defer_segs_) bytes += 4.0 * (sg.splits - 1) * sg.n;   // planes instead of g
+    LAUNCH("fused_update", 0, bytes,
+           fused_update_partials(W_, v_, g_, defer_segs_.data(), static_cast<int>(defer_segs_.size()), what_[0],
+                                 what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_dev_, s_));
+  }
+  defer_segs_.clear();
+  defer_used_ = 0;
   g_pending_ = false;
 }
 
@@ -518,6 +561,8 @@ void Stage::backward(int64_t mb, const void* dy, void* dx) {
   if (g_pending_) throw StageError(SPECTRAIN_ESTATE, "the previous gradient has not been applied by an update");
   if (d_.head != SPECTRAIN_HEAD_CE && !dy) fail("dy_dev is NULL");
   bwd_weights_ = d_.weight_policy == SPECTRAIN_POLICY_STASH ? wstash_.at<char>(wstash_off_[slot]) : what_[1];
+  defer_segs_.clear();
+  defer_used_ = 0;
   switch (d_.kind) {
     case SPECTRAIN_KIND_FC: bwd_fc(slot, dy, dx); break;
     case SPECTRAIN_KIND_CONV3X3: bwd_conv(slot, dy, dx); break;
@@ -617,7 +662,7 @@ void Stage::bwd_conv(int slot, const void* dy, void* dx) {
     const int C = l == 0 ? Cin : Cout;
     GemmDesc gw = gd(Cout, 9 * C, P, opR(dz, Cout), opConv(OP_R_CONV_WGRAD, act(l), B, H, W, C), 9 * C);
     gw.epi.out_f32 = grad(l);
-    gemm(gw);
+    gemm(gw, true);
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
     GemmDesc gx = gd(P, C, 9 * Cout, opConv(OP_K_CONV_DGRAD, dz, B, H, W, Cout),

@@ -86,7 +86,10 @@ class Stage {
   T* stash(int slot, int buf) const { return slot_blocks_[slot].at<T>(stash_off_[buf]); }
   template <typename T>
   T* ws(int buf) const { return ws_block_.at<T>(ws_off_[buf]); }
-  void gemm(const GemmDesc& d);
+  // defer: the GEMM is the only writer of a gradient tensor (plain float32
+  // store into g); when it splits K, its partials stay in the deferred buffer
+  // and the update sums them instead of a separate reduction pass.
+  void gemm(const GemmDesc& d, bool defer = false);
 
   // Launch wrapper: checks the launch status and, while profiling, brackets
   // the launch with events on the stage's stream.
@@ -154,6 +157,10 @@ class Stage {
   std::vector<size_t> ws_off_;
   size_t gemm_ws_bytes_ = 0;
   bool g_pending_ = false;
+  DeviceBlock defer_block_;              // split-K partials of gradients the update reduces
+  float* defer_ = nullptr;
+  long defer_cap_ = 0, defer_used_ = 0;  // floats
+  std::vector<UpdateSegment> defer_segs_;
 
   struct ProfRec {
     int family;

@@ -216,6 +216,8 @@ WORKLOADS: Dict[str, Workload] = {
 SMALL_WORKLOADS: Dict[str, Workload] = {
     "mlp3_small": _mlp3(batch=7, widths=(37, 50, 21, 10), lr=0.05),
     "vgg_conv_small": _single("vgg_conv_small", "conv3x3", "bf16", "none", 1, 4, 3, 3, (24, 40, 7, 9), 1e-3),
+    # batch 32 at 7x9: K = 2016 positions, so the filter gradients split K
+    "vgg_conv_mid": _single("vgg_conv_mid", "conv3x3", "bf16", "none", 1, 4, 32, 3, (40, 72, 7, 9), 1e-3),
     "resnet_bottleneck_small": _single("resnet_bottleneck_small", "bottleneck", "bf16", "none", 2, 4, 2, 2,
                                        (72, 24, 7, 5), 1e-3),
     "transformer_enc_small": _single("transformer_enc_small", "transformer", "bf16", "none", 1, 4, 3, 2,

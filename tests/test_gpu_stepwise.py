@@ -14,7 +14,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 
-@pytest.mark.parametrize("name", ["mlp3_small", "vgg_conv_small", "resnet_bottleneck_small",
+@pytest.mark.parametrize("name", ["mlp3_small", "vgg_conv_small", "vgg_conv_mid", "resnet_bottleneck_small",
                                   "transformer_enc_small", "transformer_enc_mid", "reslstm_small", "reslstm_mid"])
 def test_stepwise_small(name):
     wl = synth.ALL_WORKLOADS[name]
@@ -43,7 +43,7 @@ def _with_policy(wl, policy):
 
 
 @pytest.mark.parametrize("policy", ["vanilla", "stash"])
-@pytest.mark.parametrize("name", ["mlp3_small", "vgg_conv_small", "resnet_bottleneck_small",
+@pytest.mark.parametrize("name", ["mlp3_small", "vgg_conv_small", "vgg_conv_mid", "resnet_bottleneck_small",
                                   "transformer_enc_small", "reslstm_small"])
 def test_stepwise_small_policies(name, policy):
     """The Vanilla and weight-stashing pipelines of Section 4.2 on the same
