@@ -82,6 +82,7 @@ __global__ void colsum_partial_bf16x8_kernel(const bf16_t* X, long rows, int col
   const long r0 = static_cast<long>(blockIdx.y) * RCH;
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   if (col < cols) {
+#pragma unroll 8
     for (long r = r0 + rl; r < r0 + RCH && r < rows; r += 8) {
       const uint4 v = *reinterpret_cast<const uint4*>(X + r * ld + col);
       const uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -111,6 +112,7 @@ __global__ void colsum_partial_kernel(const T* X, long rows, int cols, long ld, 
   const long r0 = static_cast<long>(blockIdx.y) * RCH;
   float s = 0.0f;
   if (col < cols) {
+#pragma unroll 8
     for (long r = r0 + ty; r < r0 + RCH && r < rows; r += 4) {
       if constexpr (sizeof(T) == 2) s += bf16_to_f32(X[r * ld + col]);
       else s += X[r * ld + col];
@@ -129,8 +131,11 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* partial,
   const int cx = threadIdx.x & 15, cy = threadIdx.x >> 4;
   const int col = blockIdx.x * 16 + cx;
   float s = 0.0f;
-  if (col < cols)
+  if (col < cols) {
+    // eight loads in flight per thread; the sum keeps its sequential order
+#pragma unroll 8
     for (int c = cy; c < nchunks; c += 16) s += partial[static_cast<long>(c) * cols + col];
+  }
   sh[cy][cx] = s;
   __syncthreads();
   if (cy == 0 && col < cols) {
@@ -254,14 +259,29 @@ __global__ __launch_bounds__(NT) void layernorm_bwd_kernel(const bf16_t* dy, con
   ld_row<VPL>(gamma + lane * VPL, gm);
 #pragma unroll
   for (int j = 0; j < VPL; ++j) pg[j] = pb[j] = 0.0f;
-  for (int rr = w; rr < LNB_ROWS; rr += 4) {
-    const int row = blockIdx.x * LNB_ROWS + rr;
+  // wave w takes rows w, w + 4, ...: all of its rows are loaded before any
+  // is reduced, so the loads overlap the cross-lane sums
+  constexpr int RPW = LNB_ROWS / 4;
+  float dq[RPW][VPL], xq[RPW][VPL], muq[RPW], rsq[RPW];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    const int row = blockIdx.x * LNB_ROWS + w + 4 * q;
+    if (row < R) {
+      const long base = static_cast<long>(row) * D + lane * VPL;
+      ld_row<VPL>(dy + base, dq[q]);
+      ld_row<VPL>(r + base, xq[q]);
+      muq[q] = mean[row];
+      rsq[q] = rstd[row];
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    const int row = blockIdx.x * LNB_ROWS + w + 4 * q;
     if (row >= R) break;
     const long base = static_cast<long>(row) * D + lane * VPL;
-    const float mu = mean[row], rs = rstd[row];
-    float d[VPL], xh[VPL];
-    ld_row<VPL>(dy + base, d);
-    ld_row<VPL>(r + base, xh);
+    const float mu = muq[q], rs = rsq[q];
+    float(&d)[VPL] = dq[q];
+    float(&xh)[VPL] = xq[q];
     float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
     for (int j = 0; j < VPL; ++j) {

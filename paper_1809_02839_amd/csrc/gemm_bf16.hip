@@ -347,6 +347,62 @@ __device__ __forceinline__ void epilogue4(const EpiDev& e, long idx, int col, fl
   }
 }
 
+// Stores a block's 128 x 128 accumulator tile: float32 partials of its K
+// split, or the epilogue into the outputs.
+__device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2][2], int row0, int col0, int wm,
+                                           int wn, int lane, int split, int z, int z1, int z2) {
+  // With B as the first MFMA operand, lane l holds row (l % 32) and columns
+  // 8 (r / 4) + 4 (l / 32) + r % 4 of each 32 x 32 tile: four consecutive
+  // columns per register group.
+  if (args.splits > 1) {
+    float* part = args.partial + (static_cast<long>(split) * args.batch + z) * args.M * args.N;
+    const bool vec = (args.N & 3) == 0;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int row = row0 + wm * 64 + i * 32 + (lane & 31);
+        if (row >= args.M) continue;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int col = col0 + wn * 64 + j * 32 + 8 * g + 4 * (lane >> 5);
+          float* o = part + static_cast<long>(row) * args.N + col;
+          if (vec && col + 3 < args.N) {
+            *reinterpret_cast<float4*>(o) =
+                make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              if (col + q < args.N) o[q] = acc[i][j][4 * g + q];
+          }
+        }
+      }
+    return;
+  }
+  const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int row = row0 + wm * 64 + i * 32 + (lane & 31);
+      if (row >= args.M) continue;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int col = col0 + wn * 64 + j * 32 + 8 * g + 4 * (lane >> 5);
+        const long idx = coff + static_cast<long>(row) * args.e.ldc + col;
+        const float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+        if (args.vec_epi && col + 3 < args.N) {
+          epilogue4(args.e, idx, col, v);
+        } else {
+          if (col < args.N) epilogue(args.e, idx, col, v.x);
+          if (col + 1 < args.N) epilogue(args.e, idx + 1, col + 1, v.y);
+          if (col + 2 < args.N) epilogue(args.e, idx + 2, col + 2, v.z);
+          if (col + 3 < args.N) epilogue(args.e, idx + 3, col + 3, v.w);
+        }
+      }
+    }
+}
+
 template <int MA, int MB, bool TAPK>
 __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TILE_ELEMS];  // [buffer][A|B]
@@ -447,56 +503,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
     if (kt < nk) compute(lds[0][0], lds[0][1]);   // odd step count: the last step is in buffer 0
   }
 
-  // With B as the first MFMA operand, lane l holds row (l % 32) and columns
-  // 8 (r / 4) + 4 (l / 32) + r % 4 of each 32 x 32 tile: four consecutive
-  // columns per register group.
-  if (args.splits > 1) {
-    float* part = args.partial + (static_cast<long>(split) * args.batch + z) * args.M * args.N;
-    const bool vec = (args.N & 3) == 0;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int row = row0 + wm * 64 + i * 32 + (lane & 31);
-        if (row >= args.M) continue;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int col = col0 + wn * 64 + j * 32 + 8 * g + 4 * (lane >> 5);
-          float* o = part + static_cast<long>(row) * args.N + col;
-          if (vec && col + 3 < args.N) {
-            *reinterpret_cast<float4*>(o) =
-                make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
-          } else {
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              if (col + q < args.N) o[q] = acc[i][j][4 * g + q];
-          }
-        }
-      }
-    return;
-  }
-  const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int row = row0 + wm * 64 + i * 32 + (lane & 31);
-      if (row >= args.M) continue;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int col = col0 + wn * 64 + j * 32 + 8 * g + 4 * (lane >> 5);
-        const long idx = coff + static_cast<long>(row) * args.e.ldc + col;
-        const float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
-        if (args.vec_epi && col + 3 < args.N) {
-          epilogue4(args.e, idx, col, v);
-        } else {
-          if (col < args.N) epilogue(args.e, idx, col, v.x);
-          if (col + 1 < args.N) epilogue(args.e, idx + 1, col + 1, v.y);
-          if (col + 2 < args.N) epilogue(args.e, idx + 2, col + 2, v.z);
-          if (col + 3 < args.N) epilogue(args.e, idx + 3, col + 3, v.w);
-        }
-      }
-    }
+  write_tile(args, acc, row0, col0, wm, wn, lane, split, z, z1, z2);
 }
 
 // Sum the split partials in split order and apply the epilogue. Four
