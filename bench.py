@@ -39,6 +39,12 @@ DESCRIPTIONS = {
     "resnet_bottleneck": "ResNet-152-style stage: 8 bottlenecks 1024->256->256->1024, 14x14 maps, identity skip",
     "transformer_enc": "Transformer encoder stage: 3 post-LN layers, d=512, 8 heads, FFN 2048, seq 128",
     "reslstm": "Residual LSTM stage: 2 layers, input=hidden=1024, T=35, vocab-10000 softmax-CE head",
+    "vgg_conv_pipe": "4-stage pipeline of VGG-16-style conv stages (16 conv3x3 layers, 8x8 maps, 512 channels)",
+    "resnet_bottleneck_pipe": "4-stage pipeline of ResNet-152-style stages (32 bottlenecks, 14x14 maps)",
+    "transformer_enc_pipe": "4-stage pipeline of transformer encoder stages (12 layers) with a 32000-token "
+                            "softmax-CE head on the last stage",
+    "reslstm_pipe": "4-stage pipeline of residual LSTM stages (8 layers, hidden 1024, T=35) with a "
+                    "10000-token softmax-CE head on the last stage",
 }
 
 
@@ -127,6 +133,114 @@ class StageLoop:
             self.next_b += 1
 
 
+class PipeLoop:
+    """All N stages of a pipeline workload on one GPU, driven in the
+    one-forward-one-backward task order (every stage's forward, backward and
+    update of each mini-batch). Stage 0 inputs, last-stage labels or upstream
+    gradients, and every stage output and input gradient live in device rings
+    sized to the mini-batches a stage can hold in flight."""
+
+    def __init__(self, specs, torch, native, stream, ring=8):
+        import synth
+        self.torch, self.specs, self.stream = torch, list(specs), stream
+        dev = torch.device("cuda")
+        dt = torch.bfloat16
+        self.N = len(self.specs)
+        self.ring = ring
+        self.st, self.sf, self.sb = [], [], []
+        for spec in self.specs:
+            st = native.Stage(native.desc_from_spec(spec), synth.initial_params(spec), stream)
+            sf, sb = native.policy_versions(spec.policy, spec.stage_index, spec.num_stages)
+            self.st.append(st)
+            self.sf.append(sf)
+            self.sb.append(sb)
+        first, last = self.specs[0], self.specs[-1]
+        half = ring // 2
+        depth = self.N + 1    # outputs and input gradients kept per stage (more than any stage holds in flight)
+        self.depth = depth
+        with torch.cuda.stream(stream):
+            for k, st in enumerate(self.st):
+                st.predict(self.sf[k], 0)
+                st.predict(self.sb[k], 1)
+            self.x = [torch.from_numpy(synth.stage_input(first, m % half)).to(dev).to(dt) for m in range(ring)]
+            if last.head == "ce":
+                self.lab = [torch.from_numpy(synth.labels(last, m % half)).to(dev) for m in range(ring)]
+                self.loss = [torch.zeros(1, device=dev) for _ in range(ring)]
+                self.dy = None
+            else:
+                self.dy = [torch.from_numpy(synth.upstream_grad(last, m % half) * (1 if m < half else -1)).to(dev)
+                           .to(dt) for m in range(ring)]
+            self.y = [[torch.empty(sp.output_shape(), device=dev, dtype=dt) for _ in range(depth)]
+                      if k < self.N - 1 or sp.head != "ce" else None for k, sp in enumerate(self.specs)]
+            self.dx = [[torch.empty(sp.input_shape(), device=dev, dtype=dt) for _ in range(depth)] if k > 0 else None
+                       for k, sp in enumerate(self.specs)]
+            self.dx0 = torch.empty(first.input_shape(), device=dev, dtype=dt)
+        self.m0 = 0
+        stream.synchronize()
+
+    def steps(self, n):
+        """n mini-batches through the whole pipeline (fill and drain included)."""
+        from paper_1809_02839_amd.pipeline import pipeline_task_order
+        N, d = self.N, self.depth
+        for k, kind, i in pipeline_task_order(N, n):
+            m = self.m0 + i
+            st = self.st[k]
+            if kind == "F":
+                x = self.x[m % self.ring] if k == 0 else self.y[k - 1][m % d]
+                if self.y[k] is None:
+                    st.forward(m, x, None, self.lab[m % self.ring], self.loss[m % self.ring])
+                else:
+                    st.forward(m, x, self.y[k][m % d])
+            else:
+                if k < N - 1:
+                    dy = self.dx[k + 1][m % d]
+                else:
+                    dy = None if self.dy is None else self.dy[m % self.ring]
+                dx = self.dx[k][m % d] if k > 0 else self.dx0
+                st.backward(m, dy, dx)
+                st.update(self.sf[k], self.sb[k])
+        self.m0 += n
+
+    def profile(self, on):
+        for st in self.st:
+            st.profile(on)
+
+    def profile_read(self):
+        total = {}
+        for st in self.st:
+            for k, v in st.profile_read().items():
+                t = total.setdefault(k, {"launches": 0, "ms_total": 0.0, "flops_total": 0.0, "bytes_total": 0.0})
+                for f in t:
+                    t[f] += v[f]
+        return total
+
+    def destroy(self):
+        for st in self.st:
+            st.destroy()
+
+
+def cpu_baseline_pipeline(specs, n_steps):
+    """The oracle as it stands on the host: n_steps mini-batches through all
+    stages of the pipeline workload (each stage's forward, backward, update)."""
+    import numpy as np
+    import synth
+    from oracle import trajectory
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    wl = synth.Workload("sample", tuple(specs), n_steps)
+    t0 = time.perf_counter()
+    trajectory.run(wl)
+    dt = time.perf_counter() - t0
+    per_step = dt / n_steps
+    _ = np
+    return {"value": specs[0].batch / per_step, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n_steps} full-size mini-batches through all {len(specs)} stages (forward, backward, "
+                      f"update each), float64 NumPy, {per_step:.2f} s per mini-batch"}
+
+
 def cpu_baseline(spec, n_steps):
     """The oracle as it stands, timed on the host: n_steps (forward, backward,
     update) of the same stage at full size."""
@@ -187,7 +301,10 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
-    spec = dataclasses.replace(synth.WORKLOADS[args.workload].stages[0], policy=args.policy)
+    wl = synth.ALL_WORKLOADS[args.workload]
+    specs = [dataclasses.replace(sp, policy=args.policy) for sp in wl.stages]
+    spec = specs[0]
+    pipeline = len(specs) > 1
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib << 18   # float32 elements
         src = torch.ones(n, device="cuda")
@@ -197,7 +314,7 @@ def main():
         log(f"[bench] calibration kernel (neg): {n * 4} bytes read, {n * 4} bytes written")
         del src, dst
     stream = torch.cuda.Stream()
-    loop = StageLoop(spec, torch, native, stream)
+    loop = PipeLoop(specs, torch, native, stream) if pipeline else StageLoop(spec, torch, native, stream)
 
     loop.steps(args.warmup)
     torch.cuda.synchronize()
@@ -213,10 +330,16 @@ def main():
     log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {value:.0f} samples/s")
 
     # per-kernel pass (events around every launch, separate from the timed region)
-    loop.st.profile(True)
-    loop.steps(args.profile_steps)
-    prof = loop.st.profile_read()
-    loop.st.profile(False)
+    if pipeline:
+        loop.profile(True)
+        loop.steps(args.profile_steps)
+        prof = loop.profile_read()
+        loop.profile(False)
+    else:
+        loop.st.profile(True)
+        loop.steps(args.profile_steps)
+        prof = loop.st.profile_read()
+        loop.st.profile(False)
     torch.cuda.synchronize()
     fam_ms = {k: v["ms_total"] / args.profile_steps for k, v in prof.items()}
     for k, v in prof.items():
@@ -250,7 +373,8 @@ def main():
     cpu = None
     if not args.no_cpu:
         log(f"[bench] timing the CPU oracle on {args.cpu_steps} steps ...")
-        cpu = cpu_baseline(spec, args.cpu_steps)
+        cpu = (cpu_baseline_pipeline(specs, max(1, args.cpu_steps // 4)) if pipeline
+               else cpu_baseline(spec, args.cpu_steps))
         log(f"[bench] oracle: {cpu['value']:.2f} samples/s on {cpu['cores']} threads")
 
     out = {
@@ -268,8 +392,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: {DESCRIPTIONS[args.workload]}", "policy": args.policy,
                    "batch": spec.batch,
-                   "stage_index": spec.stage_index, "num_stages": spec.num_stages,
-                   "s_forward": loop.sf, "s_backward": loop.sb, "params": synth.num_params(spec)},
+                   "stage_index": None if pipeline else spec.stage_index, "num_stages": spec.num_stages,
+                   "s_forward": loop.sf, "s_backward": loop.sb,
+                   "params": sum(synth.num_params(sp) for sp in specs)},
         "mfma_util_pct": round(100.0 * gemm_flops / (gemm_ms / 1e3) / 1e12 / peak_mfma, 2) if gemm_ms else None,
         "mfma_util_pct_of_step": round(100.0 * gemm_flops / args.profile_steps / (ms_step / 1e3) / 1e12 / peak_mfma, 2),
         "predict_update_GBps": round(upd_gbps, 1) if upd_gbps else None,
@@ -278,7 +403,10 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
-    loop.st.destroy()
+    if pipeline:
+        loop.destroy()
+    else:
+        loop.st.destroy()
 
 
 if __name__ == "__main__":

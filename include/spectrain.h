@@ -33,17 +33,22 @@
  *   FC          weight [out, in] row-major, bias [out]
  *   CONV3X3     filter [C_out, 3, 3, C_in]                  (no bias)
  *   BOTTLENECK  conv1 [C_mid,1,1,C], conv2 [C_mid,3,3,C_mid], conv3 [C,1,1,C_mid]
+ *               (both: then, with a CE head, head.weight [classes, channels of the
+ *               stage output], head.bias [classes])
  *   TRANSFORMER qkv.weight [3d, d], qkv.bias [3d], out.weight [d, d], out.bias [d],
  *               ln1.weight [d], ln1.bias [d], ffn1.weight [F, d], ffn1.bias [F],
- *               ffn2.weight [d, F], ffn2.bias [d], ln2.weight [d], ln2.bias [d]
+ *               ffn2.weight [d, F], ffn2.bias [d], ln2.weight [d], ln2.bias [d];
+ *               then, with a CE head, vocab.weight [V, d], vocab.bias [V]
  *   RESLSTM     weight_x [4H, I], weight_h [4H, H], bias [4H], gate blocks (i, f, g, o);
  *               then, with a CE head, vocab.weight [V, H], vocab.bias [V]
  *
  * Activation layouts (compute dtype; bf16 is stored as raw 16-bit bf16):
  *   FC [B, features]; CONV3X3 and BOTTLENECK NHWC [B, H, W, C];
  *   TRANSFORMER [B, S, d]; RESLSTM time-major [T, B, H]; labels int32
- *   [B] (FC) or [T, B] (RESLSTM) with values in [0, classes); a label outside
- *   that range makes the reported loss NaN.
+ *   [B] (FC, CONV3X3, BOTTLENECK), [B, S] (TRANSFORMER, one target per token)
+ *   or [T, B] (RESLSTM)
+ *   with values in [0, classes); a label outside that range makes the
+ *   reported loss NaN.
  */
 #ifndef SPECTRAIN_H
 #define SPECTRAIN_H
@@ -73,15 +78,17 @@ typedef enum { SPECTRAIN_FP32 = 0, SPECTRAIN_BF16 = 1 } spectrain_dtype;
 
 typedef enum {
   SPECTRAIN_KIND_FC = 0,           /* dims: in, out, hidden; widths in, hidden x (L-1), out */
-  SPECTRAIN_KIND_CONV3X3 = 1,      /* dims: C_in, C_out, H, W; 3x3 stride 1 pad 1, ReLU */
-  SPECTRAIN_KIND_BOTTLENECK = 2,   /* dims: C, C_mid, H, W; 1x1-3x3-1x1, identity skip, ReLU */
-  SPECTRAIN_KIND_TRANSFORMER = 3,  /* dims: d_model, heads, ffn, seq; post-LN encoder layer */
+  SPECTRAIN_KIND_CONV3X3 = 1,      /* dims: C_in, C_out, H, W[, classes]; 3x3 stride 1 pad 1, ReLU */
+  SPECTRAIN_KIND_BOTTLENECK = 2,   /* dims: C, C_mid, H, W[, classes]; 1x1-3x3-1x1, identity skip, ReLU */
+  SPECTRAIN_KIND_TRANSFORMER = 3,  /* dims: d_model, heads, ffn, seq[, vocab with a CE head]; post-LN encoder layer */
   SPECTRAIN_KIND_RESLSTM = 4       /* dims: input, hidden, T, vocab; residual LSTM layers */
 } spectrain_kind;
 
 typedef enum {
   SPECTRAIN_HEAD_NONE = 0,  /* the caller passes dL/dY to backward */
-  SPECTRAIN_HEAD_CE = 1     /* mean softmax cross-entropy over rows; caller passes int32 labels */
+  SPECTRAIN_HEAD_CE = 1     /* mean softmax cross-entropy over rows; caller passes int32 labels.
+                               CONV3X3 and BOTTLENECK score the global average over H x W of the
+                               stage output with a linear classifier (an even number of classes) */
 } spectrain_head;
 
 /* Which weights the backward pass of a mini-batch uses (Section 4.2 compares
@@ -100,7 +107,7 @@ typedef struct {
   uint32_t abi_version;     /* SPECTRAIN_ABI_VERSION */
   int32_t kind;             /* spectrain_kind */
   int32_t dtype;            /* spectrain_dtype: operand/activation format; W, v, g are float32 */
-  int32_t head;             /* spectrain_head: CE allowed for FC and RESLSTM only */
+  int32_t head;             /* spectrain_head */
   int32_t stage_index;      /* k, 0-based, 0 <= k < num_stages */
   int32_t num_stages;       /* N >= 1 */
   int32_t batch;            /* mini-batch size B >= 1 */

@@ -109,12 +109,37 @@ def _fc_bwd(spec, P, st, dy, q):
     return dx, grads
 
 
+# ---------------------------------------------- classifier of conv stages ----
+
+def _pool_head_fwd(P, y, labels, q, st):
+    """Global average pool of the NHWC output over H x W, a linear layer to
+    the classes and the mean softmax cross-entropy over the batch."""
+    pooled = q(y.mean(axis=(1, 2)))
+    logits = Lr.linear(pooled, P["head.weight"], P["head.bias"])
+    loss, dlogits = Lr.softmax_cross_entropy(logits, np.asarray(labels).reshape(-1))
+    st["pooled"] = pooled
+    st["dlogits"] = q(dlogits)
+    return logits, loss, st
+
+
+def _pool_head_bwd(P, st, y_shape, q, grads):
+    """Head gradients and dL/dY: the pooled gradient spread evenly over H x W."""
+    dl = st["dlogits"]
+    grads["head.weight"] = dl.T @ st["pooled"]
+    grads["head.bias"] = dl.sum(axis=0)
+    dpool = q(dl @ P["head.weight"])
+    B, H, W, C = y_shape
+    return np.broadcast_to(q(dpool / (H * W))[:, None, None, :], y_shape)
+
+
 # ------------------------------------------------------------- conv3x3 ----
 
 def _conv_fwd(spec, P, x, labels, q):
     acts = [x]
     for l in range(spec.num_layers):
         acts.append(q(Lr.relu(Lr.conv3x3_forward(acts[-1], P[f"conv{l}.weight"]))))
+    if spec.head == "ce":
+        return _pool_head_fwd(P, acts[-1], labels, q, {"acts": acts})
     return acts[-1], None, {"acts": acts}
 
 
@@ -122,6 +147,8 @@ def _conv_bwd(spec, P, st, dy, q):
     acts = st["acts"]
     L = spec.num_layers
     grads = {}
+    if spec.head == "ce":
+        dy = _pool_head_bwd(P, st, acts[L].shape, q, grads)
     dz = dy * Lr.relu_mask(acts[L])
     dx = None
     for l in range(L - 1, -1, -1):
@@ -149,12 +176,16 @@ def _bneck_fwd(spec, P, x, labels, q):
         y = q(Lr.relu(a + Lr.conv1x1_forward(t2, P[p + "conv3.weight"])))
         blocks.append({"x": a, "t1": t1, "t2": t2, "y": y})
         a = y
+    if spec.head == "ce":
+        return _pool_head_fwd(P, a, labels, q, {"blocks": blocks})
     return a, None, {"blocks": blocks}
 
 
 def _bneck_bwd(spec, P, st, dy, q):
     grads = {}
     blocks = st["blocks"]
+    if spec.head == "ce":
+        dy = _pool_head_bwd(P, st, blocks[-1]["y"].shape, q, grads)
     g = dy   # gradient w.r.t. the current block's output y
     for l in range(spec.num_layers - 1, -1, -1):
         p = f"block{l}."
@@ -174,8 +205,9 @@ def _bneck_bwd(spec, P, st, dy, q):
 def _tfm_fwd(spec, P, x, labels, q):
     """Post-LN encoder layer: h = LN1(x + W_o MHA(x) + b_o),
     y = LN2(h + W_2 relu(W_1 h + b_1) + b_2); softmax scale 1/sqrt(d_head),
-    no mask, no dropout."""
-    dm, H, _, S = spec.dims
+    no mask, no dropout. A CE head projects every token to the vocabulary and
+    averages the per-token loss (the target-token head of the last stage)."""
+    dm, H, _, S = spec.dims[:4]
     B = spec.batch
     a = x.reshape(B * S, dm)
     layers = []
@@ -195,7 +227,15 @@ def _tfm_fwd(spec, P, x, labels, q):
         y, _, _ = Lr.layernorm_forward(r2, P[p + "ln2.weight"], P[p + "ln2.bias"], LN_EPS)
         layers.append({"a": a, "qkv": qkv, "ctx": ctx, "r1": r1, "h": h, "f1": f1, "r2": r2})
         a = q(y)
-    return a.reshape(B, S, dm), None, {"layers": layers}
+    st = {"layers": layers}
+    if spec.head == "ce":
+        # vocabulary projection of every token and the mean token cross-entropy
+        logits = Lr.linear(a, P["vocab.weight"], P["vocab.bias"])
+        loss, dlogits = Lr.softmax_cross_entropy(logits, np.asarray(labels).reshape(B * S))
+        st["out"] = a
+        st["dlogits"] = q(dlogits)
+        return logits, loss, st
+    return a.reshape(B, S, dm), None, st
 
 
 def _attention_backward(dctx, qkv, B, S, H, q):
@@ -215,10 +255,16 @@ def _attention_backward(dctx, qkv, B, S, H, q):
 
 
 def _tfm_bwd(spec, P, st, dy, q):
-    dm, H, _, S = spec.dims
+    dm, H, _, S = spec.dims[:4]
     B = spec.batch
     grads = {}
-    g = dy.reshape(B * S, dm)
+    if spec.head == "ce":
+        dl = st["dlogits"]
+        grads["vocab.weight"] = dl.T @ st["out"]
+        grads["vocab.bias"] = dl.sum(axis=0)
+        g = q(dl @ P["vocab.weight"])
+    else:
+        g = dy.reshape(B * S, dm)
     for l in range(spec.num_layers - 1, -1, -1):
         p = f"layer{l}."
         c = st["layers"][l]

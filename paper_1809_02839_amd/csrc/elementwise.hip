@@ -70,6 +70,47 @@ __global__ void mask_f32_kernel(const float* src, const float* mask, float* dst,
     dst[i] = mask[i] > 0.0f ? src[i] : 0.0f;
 }
 
+// ------------------------------------------------- global average pool ----
+// out[b][c] = bf16(sum over hw of x[b][hw][c] / HW) for an NHWC tensor; one
+// thread per (b, c) sums its H x W values in order (columns of a block are
+// consecutive channels, so every load of a wave is contiguous).
+__global__ void avgpool_bf16_kernel(const bf16_t* x, int HW, int C, bf16_t* out) {
+  const int c = blockIdx.x * NT + threadIdx.x, b = blockIdx.y;
+  if (c >= C) return;
+  const bf16_t* p = x + static_cast<long>(b) * HW * C + c;
+  float s = 0.0f;
+#pragma unroll 8
+  for (int i = 0; i < HW; ++i) s += bf16_to_f32(p[static_cast<long>(i) * C]);
+  out[static_cast<long>(b) * C + c] = f32_to_bf16(__fdiv_rn(s, static_cast<float>(HW)));
+}
+
+// Backward of the pool through the ReLU of the pooled activations:
+// dx[b][hw][c] = y[b][hw][c] > 0 ? bf16(dpool[b][c] / HW) : 0, eight channels
+// per thread (C % 8 == 0).
+__global__ void avgpool_bwd_mask_kernel(const bf16_t* dpool, const bf16_t* y, long n8, int HW, int C,
+                                        bf16_t* dx) {
+  const int c8 = C / 8;
+  const float hw_f = static_cast<float>(HW);
+  for (long i = static_cast<long>(blockIdx.x) * NT + threadIdx.x; i < n8; i += static_cast<long>(gridDim.x) * NT) {
+    const long pix = i / c8;
+    const int cg = static_cast<int>(i - pix * c8);
+    const long b = pix / HW;
+    const uint4 g = *reinterpret_cast<const uint4*>(dpool + b * C + cg * 8);
+    const uint4 m = reinterpret_cast<const uint4*>(y)[i];
+    const uint32_t gv[4] = {g.x, g.y, g.z, g.w}, mv[4] = {m.x, m.y, m.z, m.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = f32_to_bf16(__fdiv_rn(bf16_to_f32(static_cast<bf16_t>(gv[q] & 0xffff)), hw_f));
+      const uint32_t hi = f32_to_bf16(__fdiv_rn(bf16_to_f32(static_cast<bf16_t>(gv[q] >> 16)), hw_f));
+      const bool plo = bf16_to_f32(static_cast<bf16_t>(mv[q] & 0xffff)) > 0.0f;
+      const bool phi = bf16_to_f32(static_cast<bf16_t>(mv[q] >> 16)) > 0.0f;
+      o[q] = (plo ? lo : 0u) | (phi ? hi << 16 : 0u);
+    }
+    reinterpret_cast<uint4*>(dx)[i] = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
 // --------------------------------------------------------- column sums ----
 // Pass 1: block (cb, rb) sums rows [rb*RCH, (rb+1)*RCH) of its columns into
 // partial[rb][col]. bf16 inputs with cols % 8 == 0 use 16-byte loads: 32
@@ -415,6 +456,21 @@ hipError_t mask_relu_grad(const void* src, const void* mask, void* dst, long n, 
   else
     hipLaunchKernelGGL(mask_f32_kernel, dim3(blocks_for(n, 4)), dim3(NT), 0, s, static_cast<const float*>(src),
                        static_cast<const float*>(mask), static_cast<float*>(dst), n);
+  return hipGetLastError();
+}
+
+hipError_t avgpool_fwd(const bf16_t* x, int B, int HW, int C, bf16_t* out, hipStream_t s) {
+  if (B <= 0 || C <= 0) return hipSuccess;
+  if (HW <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(avgpool_bf16_kernel, dim3((C + NT - 1) / NT, B), dim3(NT), 0, s, x, HW, C, out);
+  return hipGetLastError();
+}
+
+hipError_t avgpool_bwd_mask(const bf16_t* dpool, const bf16_t* y, int B, int HW, int C, bf16_t* dx, hipStream_t s) {
+  if (C % 8 || HW <= 0) return hipErrorInvalidValue;
+  const long n8 = static_cast<long>(B) * HW * (C / 8);
+  if (n8 <= 0) return hipSuccess;
+  hipLaunchKernelGGL(avgpool_bwd_mask_kernel, dim3(blocks_for(n8, 1)), dim3(NT), 0, s, dpool, y, n8, HW, C, dx);
   return hipGetLastError();
 }
 

@@ -70,6 +70,12 @@ int gemm_bf16_splits(const GemmDesc& d);   // K splits the launch will use (1 = 
 int gemm_bf16_split_rule(int M, int N, int K, int batch, size_t workspace_bytes);
 hipError_t gemm_f32(const GemmDesc& d, hipStream_t s);
 
+// Global average pool of an NHWC bf16 tensor [B, HW, C] -> [B, C] (bf16 of the
+// float32 mean), and its backward through the ReLU of the pooled tensor y:
+// dx = y > 0 ? bf16(dpool / HW) : 0 (C % 8 == 0, 16-byte aligned tensors).
+hipError_t avgpool_fwd(const bf16_t* x, int B, int HW, int C, bf16_t* out, hipStream_t s);
+hipError_t avgpool_bwd_mask(const bf16_t* dpool, const bf16_t* y, int B, int HW, int C, bf16_t* dx, hipStream_t s);
+
 // ------------------------------------------------------- update/predict ----
 // Fused Eq. 1 + momentum update + Eq. 4 for two slots over n float32 values.
 // what_dtype: 0 float32, 1 bf16. s < 0 skips a slot. flag is set to 1 when a

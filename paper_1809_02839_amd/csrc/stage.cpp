@@ -102,6 +102,10 @@ void Stage::build_layout() {
     }
     case SPECTRAIN_KIND_CONV3X3:
       for (int l = 0; l < L; ++l) sizes.push_back(static_cast<long>(dm[1]) * 9 * (l == 0 ? dm[0] : dm[1]));
+      if (d_.head == SPECTRAIN_HEAD_CE) {   // classifier [classes, C_out] and its bias
+        sizes.push_back(static_cast<long>(dm[4]) * dm[1]);
+        sizes.push_back(dm[4]);
+      }
       break;
     case SPECTRAIN_KIND_BOTTLENECK:
       for (int l = 0; l < L; ++l) {
@@ -109,12 +113,20 @@ void Stage::build_layout() {
         sizes.push_back(static_cast<long>(dm[1]) * 9 * dm[1]);
         sizes.push_back(static_cast<long>(dm[0]) * dm[1]);
       }
+      if (d_.head == SPECTRAIN_HEAD_CE) {   // classifier [classes, C] and its bias
+        sizes.push_back(static_cast<long>(dm[4]) * dm[0]);
+        sizes.push_back(dm[4]);
+      }
       break;
     case SPECTRAIN_KIND_TRANSFORMER: {
       const long d = dm[0], F = dm[2];
       for (int l = 0; l < L; ++l) {
         long s[12] = {3 * d * d, 3 * d, d * d, d, d, d, F * d, F, d * F, d, d, d};
         sizes.insert(sizes.end(), s, s + 12);
+      }
+      if (d_.head == SPECTRAIN_HEAD_CE) {   // vocabulary projection [V, d] and its bias
+        sizes.push_back(static_cast<long>(dm[4]) * d);
+        sizes.push_back(dm[4]);
       }
       break;
     }
@@ -265,8 +277,16 @@ void Stage::plan_buffers() {
     case SPECTRAIN_KIND_CONV3X3: {
       const long P = B * dm[2] * dm[3];
       for (int l = 1; l < L; ++l) st.push_back(P * dm[1] * esz_);
+      const bool ce = d_.head == SPECTRAIN_HEAD_CE;
+      const long V = ce ? dm[4] : 0;
+      st.push_back(ce ? P * dm[1] * esz_ : 0);   // id L-1: last output (the pooled tensor)
+      st.push_back(ce ? B * dm[1] * 2 : 0);      // id L: pooled [B, C_out]
+      st.push_back(B * V * 2);                   // id L+1: class-score gradient
       const long cmax = std::max(dm[0], dm[1]);
-      ws = {static_cast<size_t>(P * cmax * esz_), static_cast<size_t>(P * cmax * esz_)};
+      ws = {static_cast<size_t>(P * cmax * esz_), static_cast<size_t>(P * cmax * esz_),
+            static_cast<size_t>(B * V * 4), static_cast<size_t>(ce ? B * 4 : 0),
+            static_cast<size_t>(ce ? B * dm[1] * 2 : 0)};
+      partial = partial_floats(B, V);
       for (int l = 0; l < L && dt_; ++l) {   // filter-gradient partials, reduced by the update
         const int C = l == 0 ? dm[0] : dm[1];
         defer_cap_ += static_cast<long>(gemm_bf16_split_rule(dm[1], 9 * C, static_cast<int>(P), 1, gemm_ws_bytes_)) *
@@ -276,17 +296,25 @@ void Stage::plan_buffers() {
     }
     case SPECTRAIN_KIND_BOTTLENECK: {
       const long P = B * dm[2] * dm[3], C = dm[0], Cm = dm[1];
+      const bool ce = d_.head == SPECTRAIN_HEAD_CE;
+      const long V = ce ? dm[4] : 0;
       for (int l = 0; l < L; ++l) {
         st.push_back(P * Cm * esz_);
         st.push_back(P * Cm * esz_);
-        st.push_back(l < L - 1 ? P * C * esz_ : 0);
+        st.push_back(l < L - 1 || ce ? P * C * esz_ : 0);
       }
+      st.push_back(ce ? B * C * 2 : 0);   // id 3L: pooled [B, C]
+      st.push_back(B * V * 2);   // id 3L+1: class-score gradient
       ws = {static_cast<size_t>(P * C * esz_), static_cast<size_t>(P * C * esz_), static_cast<size_t>(P * Cm * esz_),
-            static_cast<size_t>(P * Cm * esz_)};
+            static_cast<size_t>(P * Cm * esz_), static_cast<size_t>(B * V * 4), static_cast<size_t>(ce ? B * 4 : 0),
+            static_cast<size_t>(ce ? B * C * 2 : 0)};
+      partial = partial_floats(B, V);
       break;
     }
     case SPECTRAIN_KIND_TRANSFORMER: {
       const long d = dm[0], H = dm[1], F = dm[2], S = dm[3], T = B * S;
+      const bool ce = d_.head == SPECTRAIN_HEAD_CE;
+      const long V = ce ? dm[4] : 0;
       const bool fused = attention_fused_supported(static_cast<int>(S), static_cast<int>(d / H), static_cast<int>(d));
       // the fused attention keeps only softmax row statistics; the GEMM path P (f32, bf16) and the scores
       const long BHSS = fused ? 0 : B * H * S * S;
@@ -297,14 +325,17 @@ void Stage::plan_buffers() {
                         static_cast<size_t>(T * 4),         static_cast<size_t>(T * d * 2),
                         static_cast<size_t>(T * F * 2),     static_cast<size_t>(T * d * 2),
                         static_cast<size_t>(T * 4),         static_cast<size_t>(T * 4),
-                        static_cast<size_t>(l < L - 1 ? T * d * 2 : 0)};
+                        static_cast<size_t>(l < L - 1 || ce ? T * d * 2 : 0)};
         st.insert(st.end(), s, s + 13);
       }
+      st.push_back(ce ? T * V * 2 : 0);   // dlogits (bf16) at id 13 L
       ws = {static_cast<size_t>(BHSS * 4), static_cast<size_t>(BHSS * 2), static_cast<size_t>(T * d * 2),
             static_cast<size_t>(T * d * 2), static_cast<size_t>(T * d * 2), static_cast<size_t>(T * F * 2),
             static_cast<size_t>(T * d * 2), static_cast<size_t>(T * d * 2), static_cast<size_t>(T * d * 2),
-            static_cast<size_t>(T * 3 * d * 2)};
+            static_cast<size_t>(T * 3 * d * 2), static_cast<size_t>(ce ? T * V * 4 : 0),
+            static_cast<size_t>(ce ? T * 4 : 0)};
       partial = std::max(partial_floats(T, 3 * d), partial_floats(T, F));
+      if (ce) partial = std::max(partial, partial_floats(T, V));
       partial = std::max(partial, layernorm_bwd_ws_floats(T, d));
       break;
     }
@@ -358,8 +389,9 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
     fail("weight_policy must be PREDICT or STASH");
   if (d.dtype != SPECTRAIN_FP32 && d.dtype != SPECTRAIN_BF16) fail("unknown dtype");
   if (d.head != SPECTRAIN_HEAD_NONE && d.head != SPECTRAIN_HEAD_CE) fail("unknown head");
-  if (d.head == SPECTRAIN_HEAD_CE && d.kind != SPECTRAIN_KIND_FC && d.kind != SPECTRAIN_KIND_RESLSTM)
-    fail("a CE head exists for FC and RESLSTM stages only");
+  if (d.head == SPECTRAIN_HEAD_CE && d.kind != SPECTRAIN_KIND_FC && d.kind != SPECTRAIN_KIND_RESLSTM &&
+      d.kind != SPECTRAIN_KIND_TRANSFORMER && d.kind != SPECTRAIN_KIND_CONV3X3 && d.kind != SPECTRAIN_KIND_BOTTLENECK)
+    fail("unknown stage kind for a CE head");
   dt_ = d.dtype == SPECTRAIN_BF16 ? 1 : 0;
   esz_ = dt_ ? 2 : 4;
   const int* dm = d.dims;
@@ -385,6 +417,10 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
       if (!dt_) fail("convolution stages run in bf16 only");
       mult8(dm[0], "channels");
       mult8(dm[1], "channels");
+      if (d.head == SPECTRAIN_HEAD_CE) {
+        need(5);
+        if (dm[4] % 2) fail("classes must be even (rows of the class-score gradient are 4-byte aligned)");
+      }
       break;
     case SPECTRAIN_KIND_TRANSFORMER:
       need(4);
@@ -395,6 +431,10 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
       mult8(dm[0] / dm[1], "head dimension");
       mult8(dm[2], "ffn");
       mult8(dm[3], "seq");
+      if (d.head == SPECTRAIN_HEAD_CE) {
+        need(5);
+        mult8(dm[4], "vocab");
+      }
       break;
     case SPECTRAIN_KIND_RESLSTM:
       need(3);
@@ -545,9 +585,9 @@ void Stage::forward(int64_t mb, const void* x, void* y, const int32_t* labels, f
               "stash weights");
   switch (d_.kind) {
     case SPECTRAIN_KIND_FC: fwd_fc(free_slot, x, y, labels, loss); break;
-    case SPECTRAIN_KIND_CONV3X3: fwd_conv(free_slot, x, y); break;
-    case SPECTRAIN_KIND_BOTTLENECK: fwd_bneck(free_slot, x, y); break;
-    case SPECTRAIN_KIND_TRANSFORMER: fwd_tfm(free_slot, x, y); break;
+    case SPECTRAIN_KIND_CONV3X3: fwd_conv(free_slot, x, y, labels, loss); break;
+    case SPECTRAIN_KIND_BOTTLENECK: fwd_bneck(free_slot, x, y, labels, loss); break;
+    case SPECTRAIN_KIND_TRANSFORMER: fwd_tfm(free_slot, x, y, labels, loss); break;
     case SPECTRAIN_KIND_RESLSTM: fwd_lstm(free_slot, x, y, labels, loss); break;
   }
   slots_[free_slot] = Slot{true, mb, x, y};
@@ -635,27 +675,69 @@ void Stage::bwd_fc(int slot, const void* dy, void* dx) {
 }
 
 // ========================================================== CONV 3x3 ====
-void Stage::fwd_conv(int slot, const void* x, void* y) {
+void Stage::fwd_conv(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
   const int L = d_.num_layers, B = d_.batch, Cin = d_.dims[0], Cout = d_.dims[1], H = d_.dims[2], W = d_.dims[3];
   const int P = B * H * W;
+  const bool ce = d_.head == SPECTRAIN_HEAD_CE;
   const void* a = x;
   for (int l = 0; l < L; ++l) {
     const int C = l == 0 ? Cin : Cout;
-    void* out = l == L - 1 ? y : stash<void>(slot, l);
+    void* out = l == L - 1 && !ce ? y : stash<void>(slot, l);
     GemmDesc g = gd(P, Cout, 9 * C, opConv(OP_K_CONV_FWD, a, B, H, W, C), opK(wf(l), 9 * C), Cout);
     g.epi.relu = 1;
     g.epi.out_bf16 = static_cast<bf16_t*>(out);
     gemm(g);
     a = out;
   }
+  if (ce) pool_head_fwd(slot, a, H * W, Cout, L, L, L + 1, 2, labels, loss);
+}
+
+// Classifier of a conv stage with a CE head (global average pool over H x W,
+// linear to the classes, mean softmax cross-entropy over the batch). yl is the
+// stage's last output [B, HW, C]; tensor t is the classifier weight (t + 1 its
+// bias); the pooled tensor and the class-score gradient go to stash ids
+// id_pool, id_dl; workspace ids wsl, wsl + 1, wsl + 2 hold the float32 scores,
+// the per-sample losses and the pooled gradient.
+void Stage::pool_head_fwd(int slot, const void* yl, int HW, int C, int t, int id_pool, int id_dl, int wsl,
+                          const int32_t* labels, float* loss) {
+  const int B = d_.batch, V = d_.dims[4];
+  bf16_t* pooled = stash<bf16_t>(slot, id_pool);
+  LAUNCH("avgpool", 0, 2.0 * B * C * (HW + 1),
+         avgpool_fwd(static_cast<const bf16_t*>(yl), B, HW, C, pooled, s_));
+  GemmDesc g = gd(B, V, C, opK(pooled, C), opK(wf(t), C), V);
+  g.epi.bias_bf16 = static_cast<const bf16_t*>(wf(t + 1));
+  g.epi.out_f32 = ws<float>(wsl);
+  gemm(g);
+  LAUNCH("softmax_ce", 0, 0, softmax_ce(ws<float>(wsl), labels, B, V, stash<void>(slot, id_dl), 1, loss,
+                                        ws<float>(wsl + 1), s_));
+}
+
+void Stage::pool_head_bwd(int slot, const void* yl, int HW, int C, int t, int id_pool, int id_dl, int wsl, void* dz) {
+  const int B = d_.batch, V = d_.dims[4];
+  const bf16_t* dl = stash<bf16_t>(slot, id_dl);
+  const bf16_t* pooled = stash<bf16_t>(slot, id_pool);
+  GemmDesc gw = gd(V, C, B, opR(dl, V), opR(pooled, C), C);
+  gw.epi.out_f32 = grad(t);
+  gemm(gw);
+  LAUNCH("bias_grad", 0, 0,
+         column_sum(dl, 1, B, V, V, grad(t + 1), 0, ws<float>(static_cast<int>(ws_off_.size()) - 2), s_));
+  bf16_t* dpool = ws<bf16_t>(wsl + 2);
+  GemmDesc gx = gd(B, C, V, opK(dl, V), opR(wb(t), C), C);
+  gx.epi.out_bf16 = dpool;
+  gemm(gx);
+  LAUNCH("avgpool_bwd", 0, 2.0 * B * C * (2 * HW + 1),
+         avgpool_bwd_mask(dpool, static_cast<const bf16_t*>(yl), B, HW, C, static_cast<bf16_t*>(dz), s_));
 }
 
 void Stage::bwd_conv(int slot, const void* dy, void* dx) {
   const int L = d_.num_layers, B = d_.batch, Cin = d_.dims[0], Cout = d_.dims[1], H = d_.dims[2], W = d_.dims[3];
   const int P = B * H * W;
   const Slot& sl = slots_[slot];
-  auto act = [&](int l) -> const void* { return l == 0 ? sl.x : (l == L ? sl.y : stash<void>(slot, l - 1)); };
-  LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * Cout, 1, s_));
+  auto act = [&](int l) -> const void* { return l == 0 ? sl.x : stash<void>(slot, l - 1); };
+  if (d_.head == SPECTRAIN_HEAD_CE)
+    pool_head_bwd(slot, stash<void>(slot, L - 1), H * W, Cout, L, L, L + 1, 2, ws<void>(0));
+  else
+    LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * Cout, 1, s_));
   const void* dz = ws<void>(0);
   int pp = 1;
   for (int l = L - 1; l >= 0; --l) {
@@ -677,14 +759,15 @@ void Stage::bwd_conv(int slot, const void* dy, void* dx) {
 
 // ======================================================== BOTTLENECK ====
 // y = relu(x + conv1x1_3(relu(conv3x3_2(relu(conv1x1_1(x)))))).
-void Stage::fwd_bneck(int slot, const void* x, void* y) {
+void Stage::fwd_bneck(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
   const int L = d_.num_layers, B = d_.batch, C = d_.dims[0], Cm = d_.dims[1], H = d_.dims[2], W = d_.dims[3];
   const int P = B * H * W;
+  const bool ce = d_.head == SPECTRAIN_HEAD_CE;
   const void* a = x;
   for (int l = 0; l < L; ++l) {
     bf16_t* t1 = stash<bf16_t>(slot, 3 * l);
     bf16_t* t2 = stash<bf16_t>(slot, 3 * l + 1);
-    void* out = l == L - 1 ? y : stash<void>(slot, 3 * l + 2);
+    void* out = l == L - 1 && !ce ? y : stash<void>(slot, 3 * l + 2);
     GemmDesc g1 = gd(P, Cm, C, opK(a, C), opK(wf(3 * l), C), Cm);
     g1.epi.relu = 1;
     g1.epi.out_bf16 = t1;
@@ -700,6 +783,7 @@ void Stage::fwd_bneck(int slot, const void* x, void* y) {
     gemm(g3);
     a = out;
   }
+  if (ce) pool_head_fwd(slot, a, H * W, C, 3 * L, 3 * L, 3 * L + 1, 4, labels, loss);
 }
 
 void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
@@ -708,7 +792,10 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
   const Slot& sl = slots_[slot];
   auto xin = [&](int l) -> const void* { return l == 0 ? sl.x : stash<void>(slot, 3 * (l - 1) + 2); };
   // dr: gradient at the block's pre-ReLU output (after the output mask)
-  LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * C, 1, s_));
+  if (d_.head == SPECTRAIN_HEAD_CE)
+    pool_head_bwd(slot, stash<void>(slot, 3 * (L - 1) + 2), H * W, C, 3 * L, 3 * L, 3 * L + 1, 4, ws<void>(0));
+  else
+    LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * C, 1, s_));
   int cur = 0;
   bf16_t* dt2 = ws<bf16_t>(2);
   bf16_t* dt1 = ws<bf16_t>(3);
@@ -750,9 +837,10 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
 // 0 qkv, 1 P (f32; with the fused attention core the softmax row statistics),
 // 2 P (bf16; unused with the fused core), 3 ctx, 4 r1, 5 mean1, 6 rstd1, 7 h,
 // 8 f1, 9 r2, 10 mean2, 11 rstd2, 12 layer output (l < L-1).
-void Stage::fwd_tfm(int slot, const void* x, void* y) {
+void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
   const int L = d_.num_layers, B = d_.batch, d = d_.dims[0], Hh = d_.dims[1], F = d_.dims[2], S = d_.dims[3];
   const int T = B * S, dh = d / Hh;
+  const bool ce = d_.head == SPECTRAIN_HEAD_CE;
   const float scale = 1.0f / std::sqrt(static_cast<float>(dh));
   const void* a = x;
   for (int l = 0; l < L; ++l) {
@@ -765,7 +853,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y) {
     bf16_t* h = stash<bf16_t>(slot, q + 7);
     bf16_t* f1 = stash<bf16_t>(slot, q + 8);
     bf16_t* r2 = stash<bf16_t>(slot, q + 9);
-    void* out = l == L - 1 ? y : stash<void>(slot, q + 12);
+    void* out = l == L - 1 && !ce ? y : stash<void>(slot, q + 12);
 
     GemmDesc g = gd(T, 3 * d, d, opK(a, d), opK(wf(p), d), 3 * d);
     g.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 1));
@@ -823,6 +911,15 @@ void Stage::fwd_tfm(int slot, const void* x, void* y) {
                             s_));
     a = out;
   }
+  if (ce) {   // logits of every token (float32), mean token cross-entropy, dlogits (bf16) for the backward
+    const int V = d_.dims[4];
+    GemmDesc gv = gd(T, V, d, opK(a, d), opK(wf(12 * L), d), V);
+    gv.epi.bias_bf16 = static_cast<const bf16_t*>(wf(12 * L + 1));
+    gv.epi.out_f32 = ws<float>(10);
+    gemm(gv);
+    LAUNCH("softmax_ce", 0, 0, softmax_ce(ws<float>(10), labels, T, V, stash<void>(slot, 13 * L), 1, loss,
+                                          ws<float>(11), s_));
+  }
 }
 
 // workspace ids: 0 scores/dP (f32), 1 dS, 2/3 layer-output gradient ping-pong,
@@ -832,9 +929,23 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
   const int T = B * S, dh = d / Hh;
   const float scale = 1.0f / std::sqrt(static_cast<float>(dh));
   const Slot& sl = slots_[slot];
-  float* part = ws<float>(10);
+  float* part = ws<float>(12);
   const void* gy = dy;
   int pp = 2;
+  if (d_.head == SPECTRAIN_HEAD_CE) {   // vocabulary head: its gradients and dY of the last layer
+    const int V = d_.dims[4];
+    const bf16_t* dl = stash<bf16_t>(slot, 13 * L);
+    const void* yL = stash<void>(slot, 13 * (L - 1) + 12);
+    GemmDesc gw = gd(V, d, T, opR(dl, V), opR(yL, d), d);
+    gw.epi.out_f32 = grad(12 * L);
+    gemm(gw);
+    LAUNCH("bias_grad", 0, 0, column_sum(dl, 1, T, V, V, grad(12 * L + 1), 0, part, s_));
+    GemmDesc gx = gd(T, d, V, opK(dl, V), opR(wb(12 * L), d), d);
+    gx.epi.out_bf16 = ws<bf16_t>(2);
+    gemm(gx);
+    gy = ws<void>(2);
+    pp = 3;
+  }
   for (int l = L - 1; l >= 0; --l) {
     const int p = 12 * l, q = 13 * l;
     const void* a = l == 0 ? sl.x : stash<void>(slot, 13 * (l - 1) + 12);

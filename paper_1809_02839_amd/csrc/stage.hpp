@@ -122,11 +122,14 @@ class Stage {
   // ---- per kind
   void fwd_fc(int slot, const void* x, void* y, const int32_t* labels, float* loss);
   void bwd_fc(int slot, const void* dy, void* dx);
-  void fwd_conv(int slot, const void* x, void* y);
+  void fwd_conv(int slot, const void* x, void* y, const int32_t* labels, float* loss);
   void bwd_conv(int slot, const void* dy, void* dx);
-  void fwd_bneck(int slot, const void* x, void* y);
+  void fwd_bneck(int slot, const void* x, void* y, const int32_t* labels, float* loss);
+  void pool_head_fwd(int slot, const void* yl, int HW, int C, int t, int id_pool, int id_dl, int wsl,
+                     const int32_t* labels, float* loss);
+  void pool_head_bwd(int slot, const void* yl, int HW, int C, int t, int id_pool, int id_dl, int wsl, void* dz);
   void bwd_bneck(int slot, const void* dy, void* dx);
-  void fwd_tfm(int slot, const void* x, void* y);
+  void fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, float* loss);
   void bwd_tfm(int slot, const void* dy, void* dx);
   void fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, float* loss);
   void bwd_lstm(int slot, const void* dy, void* dx);

@@ -32,9 +32,10 @@ class StageSpec:
 
     dims meaning per kind:
       fc:          (in_features, out_features, hidden)   widths in, hidden*(L-1), out
-      conv3x3:     (C_in, C_out, H, W)                    L layers, first C_in->C_out
-      bottleneck:  (C, C_mid, H, W)                       L blocks
-      transformer: (d_model, heads, ffn, seq)             L encoder layers
+      conv3x3:     (C_in, C_out, H, W[, classes])         L layers, first C_in->C_out
+      bottleneck:  (C, C_mid, H, W[, classes])            L blocks
+                   (a CE head on a conv stage: global average pool, linear to classes)
+      transformer: (d_model, heads, ffn, seq[, vocab])    L encoder layers, vocab used by a CE head
       reslstm:     (input, hidden, T, vocab)              L layers, vocab used by a CE head
     """
 
@@ -52,6 +53,9 @@ class StageSpec:
     # "vanilla" (the latest weights at every pass) or "stash" (the backward
     # reuses the weights of its own forward)
     policy: str = "spectrain"
+    # bottleneck: start every block's last convolution at zero, so each block
+    # is the identity at initialisation (whole stacks without normalisation)
+    zero_residual: bool = False
 
     # ----- shapes -------------------------------------------------------
     def fc_widths(self) -> List[int]:
@@ -88,8 +92,10 @@ class StageSpec:
         raise ValueError(self.kind)
 
     def label_shape(self) -> Tuple[int, ...]:
-        if self.kind == "fc":
+        if self.kind in ("fc", "conv3x3", "bottleneck"):
             return (self.batch,)
+        if self.kind == "transformer":
+            return (self.batch, self.dims[3])              # one target per token
         if self.kind == "reslstm":
             return (self.dims[2], self.batch)
         raise ValueError(f"{self.kind} has no loss head")
@@ -97,6 +103,8 @@ class StageSpec:
     def num_classes(self) -> int:
         if self.kind == "fc":
             return self.dims[1]
+        if self.kind in ("conv3x3", "bottleneck", "transformer"):
+            return self.dims[4]
         if self.kind == "reslstm":
             return self.dims[3]
         raise ValueError(self.kind)
@@ -128,12 +136,18 @@ def param_layout(spec: StageSpec) -> List[Tuple[str, Tuple[int, ...], str]]:
         cin, cout = d[0], d[1]
         for l in range(L):
             out.append((f"conv{l}.weight", (cout, 3, 3, cin if l == 0 else cout), "he"))
+        if spec.head == "ce":
+            out.append(("head.weight", (d[4], cout), "he"))
+            out.append(("head.bias", (d[4],), "zeros"))
     elif spec.kind == "bottleneck":
         c, cm = d[0], d[1]
         for l in range(L):
             out.append((f"block{l}.conv1.weight", (cm, 1, 1, c), "he"))
             out.append((f"block{l}.conv2.weight", (cm, 3, 3, cm), "he"))
-            out.append((f"block{l}.conv3.weight", (c, 1, 1, cm), "he"))
+            out.append((f"block{l}.conv3.weight", (c, 1, 1, cm), "zeros" if spec.zero_residual else "he"))
+        if spec.head == "ce":
+            out.append(("head.weight", (d[4], c), "he"))
+            out.append(("head.bias", (d[4],), "zeros"))
     elif spec.kind == "transformer":
         dm, ffn = d[0], d[2]
         for l in range(L):
@@ -152,6 +166,9 @@ def param_layout(spec: StageSpec) -> List[Tuple[str, Tuple[int, ...], str]]:
                 (p + "ln2.weight", (dm,), "ones"),
                 (p + "ln2.bias", (dm,), "zeros"),
             ]
+        if spec.head == "ce":
+            out.append(("vocab.weight", (d[4], dm), "he"))
+            out.append(("vocab.bias", (d[4],), "zeros"))
     elif spec.kind == "reslstm":
         inp, hid, _, vocab = d
         for l in range(L):
@@ -195,6 +212,22 @@ def _single(name, kind, dtype, head, k, N, batch, L, dims, lr, steps=20) -> Work
     return Workload(name, (StageSpec(kind, dtype, head, k, N, batch, L, tuple(dims), lr, 0.9),), steps)
 
 
+def _pipeline(name, kind, N, batch, L, dims, lr, first_dims=None, last_head="none", last_dims=None,
+              steps=20, zero_residual=False) -> Workload:
+    """All N stages of one model, each a stage of the same kind and shape
+    (stage 0 may differ in its input width, the last stage may carry the loss
+    head); a last stage without a head takes the synthetic upstream gradient."""
+    specs = []
+    for k in range(N):
+        d = first_dims if (k == 0 and first_dims) else dims
+        head = "none"
+        if k == N - 1:
+            head = last_head
+            d = last_dims or d
+        specs.append(StageSpec(kind, "bf16", head, k, N, batch, L, tuple(d), lr, 0.9, zero_residual=zero_residual))
+    return Workload(name, tuple(specs), steps)
+
+
 # Full-size workloads: the five stage configurations of the benchmark.
 # Learning rates follow Section 4.1 for VGG16 (2e-3), the Transformer (5e-5)
 # and the residual LSTM (5e-3); momentum 0.9 for all. The bottleneck stage
@@ -230,7 +263,49 @@ SMALL_WORKLOADS: Dict[str, Workload] = {
     "reslstm_mid": _single("reslstm_mid", "reslstm", "bf16", "ce", 3, 4, 24, 2, (96, 96, 7, 136), 5e-2),
 }
 
-ALL_WORKLOADS: Dict[str, Workload] = {**WORKLOADS, **SMALL_WORKLOADS}
+# Whole 4-stage pipelines of the four bf16 models, every stage simulated in the
+# one-forward-one-backward order on one GPU: the benchmark stage shapes
+# chained, the last stage with its loss head (the conv models classify the
+# average-pooled output into 10 classes, the transformer projects to its
+# 32000-token vocabulary, the residual LSTM to 10000; the VGG stage 0 takes
+# 256 channels to 512).
+PIPELINE_WORKLOADS: Dict[str, Workload] = {
+    "vgg_conv_pipe": _pipeline("vgg_conv_pipe", "conv3x3", 4, 128, 4, (512, 512, 8, 8), 2e-3,
+                               first_dims=(256, 512, 8, 8), last_head="ce", last_dims=(512, 512, 8, 8, 10)),
+    "resnet_bottleneck_pipe": _pipeline("resnet_bottleneck_pipe", "bottleneck", 4, 64, 8, (1024, 256, 14, 14), 1e-5,
+                                        zero_residual=True, last_head="ce", last_dims=(1024, 256, 14, 14, 10)),
+    "transformer_enc_pipe": _pipeline("transformer_enc_pipe", "transformer", 4, 64, 3, (512, 8, 2048, 128), 5e-5,
+                                      last_head="ce", last_dims=(512, 8, 2048, 128, 32000)),
+    "reslstm_pipe": _pipeline("reslstm_pipe", "reslstm", 4, 64, 2, (1024, 1024, 35, 10000), 5e-3, last_head="ce"),
+}
+
+SMALL_PIPELINE_WORKLOADS: Dict[str, Workload] = {
+    "vgg_conv_small_pipe": _pipeline("vgg_conv_small_pipe", "conv3x3", 4, 3, 2, (40, 40, 7, 9), 1e-3,
+                                     first_dims=(24, 40, 7, 9), last_head="ce", last_dims=(40, 40, 7, 9, 10)),
+    "resnet_bottleneck_small_pipe": _pipeline("resnet_bottleneck_small_pipe", "bottleneck", 4, 2, 2,
+                                              (72, 24, 7, 5), 1e-3, zero_residual=True, last_head="ce",
+                                              last_dims=(72, 24, 7, 5, 10)),
+    "transformer_enc_small_pipe": _pipeline("transformer_enc_small_pipe", "transformer", 4, 3, 2,
+                                            (64, 2, 136, 40), 2e-3, last_head="ce",
+                                            last_dims=(64, 2, 136, 40, 104)),
+    "reslstm_small_pipe": _pipeline("reslstm_small_pipe", "reslstm", 4, 5, 2, (48, 48, 6, 104), 5e-2,
+                                    last_head="ce"),
+    # sequence 128, head dimension 64 (fused attention) and hidden 96, batch 24 (fused recurrent steps)
+    "transformer_enc_mid_pipe": _pipeline("transformer_enc_mid_pipe", "transformer", 4, 2, 1, (128, 2, 256, 128),
+                                          2e-3, last_head="ce", last_dims=(128, 2, 256, 128, 136)),
+    "reslstm_mid_pipe": _pipeline("reslstm_mid_pipe", "reslstm", 4, 24, 1, (96, 96, 7, 136), 5e-2,
+                                  last_head="ce"),
+}
+
+# The last transformer stage of the pipeline at full size: 3 encoder layers
+# and the 32000-token projection with the mean token cross-entropy.
+HEAD_WORKLOADS: Dict[str, Workload] = {
+    "transformer_enc_last": _single("transformer_enc_last", "transformer", "bf16", "ce", 3, 4, 64, 3,
+                                    (512, 8, 2048, 128, 32000), 5e-5),
+}
+
+ALL_WORKLOADS: Dict[str, Workload] = {**WORKLOADS, **SMALL_WORKLOADS, **PIPELINE_WORKLOADS,
+                                      **SMALL_PIPELINE_WORKLOADS, **HEAD_WORKLOADS}
 
 
 # ----------------------------------------------------------------------------

@@ -60,7 +60,8 @@ def _create(desc, n=None, W=None):
     (dict(momentum=1.5), "momentum"),
     (dict(kind=9), "kind"),
     (dict(dtype=0), "bf16 only"),
-    (dict(head=1), "CE head"),
+    (dict(head=1), "dims[4]"),
+    (dict(head=1, dims=(256, 512, 8, 8, 7)), "classes must be even"),
     (dict(dims=(250, 512, 8, 8)), "multiple of 8"),
     (dict(weight_policy=2), "weight_policy"),
     (dict(weight_policy=-1), "weight_policy"),
@@ -73,6 +74,16 @@ def test_bad_descriptor_is_rejected_before_any_device_work(change, needle):
     fields.update(change)
     desc = native.make_desc(**fields)
     rc, h, msg = _create(desc, synth.num_params(spec))
+    assert rc == native.EINVAL and not h.value, msg
+    assert needle in msg
+
+
+@pytest.mark.parametrize("dims,needle", [((512, 8, 2048, 128), "dims[4]"), ((512, 8, 2048, 128, 1001), "vocab")])
+def test_transformer_ce_head_needs_a_vocabulary(dims, needle):
+    spec = synth.WORKLOADS["transformer_enc"].stages[0]
+    desc = native.make_desc(spec.kind, spec.dtype, "ce", 3, 4, spec.batch, spec.num_layers, dims, spec.lr,
+                            spec.momentum)
+    rc, h, msg = _create(desc, 1)
     assert rc == native.EINVAL and not h.value, msg
     assert needle in msg
 

@@ -60,3 +60,24 @@ def test_stepwise_full_size_vgg_policies(policy):
     print(f"[stepwise-full] {wl.name} steps=4", flush=True)
     worst = run_stepwise(wl, 4, torch, derived=True)
     print(f"[stepwise-full] {wl.name}: {worst.report()}", flush=True)
+
+
+# Whole 4-stage pipelines of each bf16 model (every stage simulated, the
+# last stage's loss head or synthetic upstream gradient starting each
+# backward): every task of every stage against the oracle.
+@pytest.mark.parametrize("name", ["vgg_conv_small_pipe", "resnet_bottleneck_small_pipe", "transformer_enc_small_pipe",
+                                  "transformer_enc_mid_pipe", "reslstm_small_pipe", "reslstm_mid_pipe"])
+def test_stepwise_pipeline(name):
+    wl = synth.ALL_WORKLOADS[name]
+    print(f"[stepwise-pipe] {name}", flush=True)
+    worst = run_stepwise(wl, wl.steps, torch, derived=True)
+    print(f"[stepwise-pipe] {name}: {worst.report()}", flush=True)
+
+
+def test_stepwise_transformer_vocab_head_full_size():
+    """The transformer's last stage at full size: 3 layers and the
+    32000-token projection with the mean token cross-entropy."""
+    wl = synth.ALL_WORKLOADS["transformer_enc_last"]
+    print("[stepwise-full] transformer_enc_last steps=2", flush=True)
+    worst = run_stepwise(wl, 2, torch, derived=True)
+    print(f"[stepwise-full] transformer_enc_last: {worst.report()}", flush=True)

@@ -15,7 +15,10 @@ TINY = {
     "fc_ce": synth.StageSpec("fc", "fp32", "ce", 1, 2, 4, 2, (5, 3, 6), 0.01, 0.9),
     "conv3x3": synth.StageSpec("conv3x3", "bf16", "none", 1, 4, 2, 2, (2, 3, 4, 3), 0.01, 0.9),
     "bottleneck": synth.StageSpec("bottleneck", "bf16", "none", 1, 4, 2, 2, (4, 2, 3, 4), 0.01, 0.9),
+    "conv3x3_ce": synth.StageSpec("conv3x3", "bf16", "ce", 3, 4, 3, 2, (2, 3, 4, 3, 5), 0.01, 0.9),
+    "bottleneck_ce": synth.StageSpec("bottleneck", "bf16", "ce", 3, 4, 3, 2, (4, 2, 3, 4, 5), 0.01, 0.9),
     "transformer": synth.StageSpec("transformer", "bf16", "none", 1, 4, 2, 2, (8, 2, 6, 4), 0.01, 0.9),
+    "transformer_ce": synth.StageSpec("transformer", "bf16", "ce", 3, 4, 2, 2, (8, 2, 6, 4, 7), 0.01, 0.9),
     "reslstm": synth.StageSpec("reslstm", "bf16", "none", 1, 4, 2, 2, (3, 3, 4, 7), 0.01, 0.9),
     "reslstm_ce": synth.StageSpec("reslstm", "bf16", "ce", 3, 4, 2, 2, (3, 3, 4, 7), 0.01, 0.9),
 }
@@ -112,6 +115,34 @@ def test_conv_stage_backward_matches_torch_autograd():
     np.testing.assert_allclose(dx, a.grad.numpy(), rtol=1e-9, atol=1e-12)
     for k in T:
         np.testing.assert_allclose(grads[k], T[k].grad.numpy(), rtol=1e-9, atol=1e-12)
+
+
+def test_conv_classifier_head_matches_torch_autograd():
+    """conv3x3 stage with the classifier head: torch conv2d, ReLU,
+    adaptive_avg_pool2d, linear and cross_entropy give the same loss, logits
+    and gradients."""
+    spec = TINY["conv3x3_ce"]
+    rng = np.random.default_rng(9)
+    flat = _random_params(spec, rng)
+    x = rng.standard_normal(spec.input_shape())
+    lab = rng.integers(0, spec.num_classes(), size=spec.label_shape())
+    P = stages.unpack(spec, flat)
+    logits, loss, st = stages.forward(spec, P, x, lab, exact=True)
+    dx, grads = stages.backward(spec, P, st, None, exact=True)
+    T = {k: torch.tensor(v, requires_grad=True) for k, v in P.items()}
+    a = torch.tensor(x, requires_grad=True)
+    h = a.permute(0, 3, 1, 2)
+    for l in range(spec.num_layers):
+        h = torch.relu(torch.nn.functional.conv2d(h, T[f"conv{l}.weight"].permute(0, 3, 1, 2), padding=1))
+    pooled = torch.nn.functional.adaptive_avg_pool2d(h, 1).flatten(1)
+    z = torch.nn.functional.linear(pooled, T["head.weight"], T["head.bias"])
+    ref = torch.nn.functional.cross_entropy(z, torch.tensor(lab))
+    np.testing.assert_allclose(logits, z.detach().numpy(), rtol=1e-10, atol=1e-12)
+    assert abs(loss - ref.item()) < 1e-12
+    ref.backward()
+    np.testing.assert_allclose(dx, a.grad.numpy(), rtol=1e-9, atol=1e-13)
+    for k in T:
+        np.testing.assert_allclose(grads[k], T[k].grad.numpy(), rtol=1e-9, atol=1e-13, err_msg=k)
 
 
 def test_lstm_stage_matches_torch_lstm():
@@ -213,20 +244,23 @@ def test_cross_entropy_zero_logits_and_torch():
     np.testing.assert_allclose(d, zt.grad.numpy(), rtol=1e-10, atol=1e-15)
 
 
-def test_zero_head_weights_give_ln_classes():
+@pytest.mark.parametrize("name", ["reslstm_ce", "transformer_ce", "conv3x3_ce", "bottleneck_ce"])
+def test_zero_head_weights_give_ln_classes(name):
     """CE head with zero vocabulary weights and bias: loss = ln C exactly and
-    the head gradient is (1/C - onehot)/count."""
-    spec = TINY["reslstm_ce"]
+    the head gradient is (1/C - onehot)/count, with one target per token."""
+    spec = TINY[name]
     rng = np.random.default_rng(2)
     flat = _random_params(spec, rng)
     P = stages.unpack(spec, flat)
-    P["vocab.weight"][:] = 0
-    P["vocab.bias"][:] = 0
+    head = "head" if spec.kind in ("conv3x3", "bottleneck") else "vocab"
+    P[head + ".weight"][:] = 0
+    P[head + ".bias"][:] = 0
     x = rng.standard_normal(spec.input_shape())
-    lab = rng.integers(0, 7, size=spec.label_shape())
+    C = spec.num_classes()
+    lab = rng.integers(0, C, size=spec.label_shape())
     _, loss, st = stages.forward(spec, P, x, lab, exact=True)
-    assert abs(loss - np.log(7)) < 1e-12
-    n = spec.batch * spec.dims[2]
-    expect = np.full((n, 7), 1.0 / 7)
+    assert abs(loss - np.log(C)) < 1e-12
+    n = int(np.prod(spec.label_shape()))
+    expect = np.full((n, C), 1.0 / C)
     expect[np.arange(n), lab.reshape(-1)] -= 1
     np.testing.assert_allclose(st["dlogits"], expect / n, rtol=1e-12)
