@@ -188,6 +188,101 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* partial,
 }
 
 // ---------------------------------------------------- cross-entropy ----
+// Long rows (CE_LDS_MIN <= C <= CE_LDS_MAX, C % 4 == 0): the row is read from
+// memory once into LDS (128 KB), and the max, the sum of exponentials and
+// the gradient passes read it there. One 1024-thread block per row and CU.
+constexpr int CE_LDS_MAX = 32768, CE_LDS_MIN = 4096, CE_LDS_NT = 1024;
+__global__ __launch_bounds__(CE_LDS_NT) void softmax_ce_lds_kernel(const float* logits, const int32_t* labels, int R,
+                                                                   int C, bf16_t* dlogits, float* row_loss) {
+  __shared__ float4 row[CE_LDS_MAX / 4];
+  __shared__ float sh[CE_LDS_NT / 64];
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const float4* z = reinterpret_cast<const float4*>(logits + static_cast<long>(r) * C);
+  const int C4 = C / 4;
+  auto reduce = [&](float v, bool is_max) {
+    v = is_max ? wave_max(v) : wave_sum(v);
+    __syncthreads();   // sh may still be read by the previous reduction
+    if (lane == 0) sh[wv] = v;
+    __syncthreads();
+    float t = sh[0];
+#pragma unroll
+    for (int w = 1; w < CE_LDS_NT / 64; ++w) t = is_max ? fmaxf(t, sh[w]) : t + sh[w];
+    return t;
+  };
+  float m = -INFINITY;
+#pragma unroll 4
+  for (int c = tid; c < C4; c += CE_LDS_NT) {
+    const float4 v = z[c];
+    row[c] = v;
+    m = fmaxf(m, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+  }
+  m = reduce(m, true);   // its barriers also publish the row
+  // the target's score comes from memory: the LDS row is overwritten below
+  const int lab = labels[r];
+  const bool lab_ok = lab >= 0 && lab < C;
+  const float zl = (tid == 0 && lab_ok) ? logits[static_cast<long>(r) * C + lab] : 0.0f;
+  // exp(z - m) with the hardware exponential (relative error near 1e-7, far
+  // below the bf16 rounding of the gradient), kept in LDS for the last pass
+  float s = 0.0f;
+  for (int c = tid; c < C4; c += CE_LDS_NT) {
+    const float4 v = row[c];
+    const float4 e = make_float4(__expf(v.x - m), __expf(v.y - m), __expf(v.z - m), __expf(v.w - m));
+    row[c] = e;
+    s += (e.x + e.y) + (e.z + e.w);
+  }
+  s = reduce(s, false);   // its barriers also publish the exponentials
+  if (tid == 0) row_loss[r] = lab_ok ? (m + logf(s)) - zl : NAN;
+  const float inv_s = 1.0f / s, inv_r = 1.0f / static_cast<float>(R);
+  uint2* out = reinterpret_cast<uint2*>(dlogits + static_cast<long>(r) * C);
+  for (int c = tid; c < C4; c += CE_LDS_NT) {
+    const float4 e = row[c];
+    float p[4] = {e.x * inv_s, e.y * inv_s, e.z * inv_s, e.w * inv_s};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) p[q] = ((4 * c + q == lab) ? p[q] - 1.0f : p[q]) * inv_r;
+    out[c] = make_uint2(f32_to_bf16(p[0]) | (static_cast<uint32_t>(f32_to_bf16(p[1])) << 16),
+                        f32_to_bf16(p[2]) | (static_cast<uint32_t>(f32_to_bf16(p[3])) << 16));
+  }
+}
+
+// Rows of C % 4 == 0 float32 scores with bf16 gradients: 16-byte loads, four
+// chunks in flight per thread in each of the three passes over the row (max,
+// sum of exponentials, gradient), 8-byte gradient stores.
+__global__ __launch_bounds__(NT) void softmax_ce_bf16x4_kernel(const float* logits, const int32_t* labels, int R,
+                                                               int C, bf16_t* dlogits, float* row_loss) {
+  __shared__ float sh[4];
+  const int r = blockIdx.x;
+  const float4* z = reinterpret_cast<const float4*>(logits + static_cast<long>(r) * C);
+  const int C4 = C / 4;
+  float m = -INFINITY;
+#pragma unroll 4
+  for (int c = threadIdx.x; c < C4; c += NT) {
+    const float4 v = z[c];
+    m = fmaxf(m, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+  }
+  m = block_max(m, sh);
+  float s = 0.0f;
+#pragma unroll 4
+  for (int c = threadIdx.x; c < C4; c += NT) {
+    const float4 v = z[c];
+    s += (expf(v.x - m) + expf(v.y - m)) + (expf(v.z - m) + expf(v.w - m));
+  }
+  s = block_sum(s, sh);
+  const int lab = labels[r];
+  const bool lab_ok = lab >= 0 && lab < C;
+  if (threadIdx.x == 0) row_loss[r] = lab_ok ? (m + logf(s)) - logits[static_cast<long>(r) * C + lab] : NAN;
+  const float inv_s = 1.0f / s, inv_r = 1.0f / static_cast<float>(R);
+  uint2* out = reinterpret_cast<uint2*>(dlogits + static_cast<long>(r) * C);
+#pragma unroll 4
+  for (int c = threadIdx.x; c < C4; c += NT) {
+    const float4 v = z[c];
+    float p[4] = {expf(v.x - m) * inv_s, expf(v.y - m) * inv_s, expf(v.z - m) * inv_s, expf(v.w - m) * inv_s};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) p[q] = ((4 * c + q == lab) ? p[q] - 1.0f : p[q]) * inv_r;
+    out[c] = make_uint2(f32_to_bf16(p[0]) | (static_cast<uint32_t>(f32_to_bf16(p[1])) << 16),
+                        f32_to_bf16(p[2]) | (static_cast<uint32_t>(f32_to_bf16(p[3])) << 16));
+  }
+}
+
 template <int DT>
 __global__ __launch_bounds__(NT) void softmax_ce_kernel(const float* logits, const int32_t* labels, int R, int C,
                                                         void* dlogits, float* row_loss) {
@@ -498,7 +593,15 @@ hipError_t column_sum(const void* X, int dtype, long rows, int cols, long ld, fl
 hipError_t softmax_ce(const float* logits, const int32_t* labels, int R, int C, void* dlogits, int dtype, float* loss,
                       float* row_loss_ws, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  if (dtype == 1)
+  const bool vec = C % 4 == 0 && (reinterpret_cast<uintptr_t>(logits) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(dlogits) & 7) == 0;
+  if (dtype == 1 && vec && C >= CE_LDS_MIN && C <= CE_LDS_MAX)
+    hipLaunchKernelGGL(softmax_ce_lds_kernel, dim3(R), dim3(CE_LDS_NT), 0, s, logits, labels, R, C,
+                       static_cast<bf16_t*>(dlogits), row_loss_ws);
+  else if (dtype == 1 && vec)
+    hipLaunchKernelGGL(softmax_ce_bf16x4_kernel, dim3(R), dim3(NT), 0, s, logits, labels, R, C,
+                       static_cast<bf16_t*>(dlogits), row_loss_ws);
+  else if (dtype == 1)
     hipLaunchKernelGGL(softmax_ce_kernel<1>, dim3(R), dim3(NT), 0, s, logits, labels, R, C, dlogits, row_loss_ws);
   else
     hipLaunchKernelGGL(softmax_ce_kernel<0>, dim3(R), dim3(NT), 0, s, logits, labels, R, C, dlogits, row_loss_ws);
