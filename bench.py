@@ -57,8 +57,8 @@ FAMILY_KERNEL = {
     "gemm_bf16_dyW": "gemm_bf16_kernel<0, 3",
     "gemm_bf16_dyTx": "gemm_bf16_kernel<3, 3",
     "splitk_reduce": "splitk_reduce",
-    "fused_update": "fused_update_kernel",
-}
+    "fused_update": "fused_update",   # fused_update_kernel, or fused_update_partials_kernel where K-slice
+}                                     # partials of filter gradients are summed in the update
 
 
 def traffic_per_launch(workload, family):
