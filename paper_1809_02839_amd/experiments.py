@@ -20,6 +20,7 @@ Command line:
 
     python -m paper_1809_02839_amd.experiments rmse [--layers 32 --hidden 2048 --steps 100]
     python -m paper_1809_02839_amd.experiments policies [--workload mlp3 --steps 60]
+    python -m paper_1809_02839_amd.experiments policies --workload vgg_conv_pipe --steps 200
 """
 import argparse
 import dataclasses
@@ -106,15 +107,21 @@ def prediction_rmse(spec, steps: int, s_values: Sequence[int] = (1, 2, 3), W0: O
 def teacher_labels(workload, seed: int = 4242):
     """A learnable labelling of a workload's synthetic inputs: the class a fixed
     seeded random linear map of the first stage's input scores highest (the
-    uniform random labels of the parity tests carry nothing to learn)."""
+    uniform random labels of the parity tests carry nothing to learn). For
+    workloads whose loss head takes one label per sample (FC, conv)."""
     import synth
     first, last = workload.stages[0], workload.stages[-1]
     classes = last.num_classes() if hasattr(last, "num_classes") else last.dims[1]
     rng = np.random.default_rng(seed)
-    T = rng.standard_normal((int(np.prod(first.input_shape()[1:])), classes))
+    # conv models end in a global average pool, so their teacher reads the
+    # input averaged over positions (a function the pooled head can express)
+    pooled = first.kind in ("conv3x3", "bottleneck")
+    width = first.input_shape()[-1] if pooled else int(np.prod(first.input_shape()[1:]))
+    T = rng.standard_normal((width, classes))
 
     def labels(sp, m):
-        x = synth.stage_input(first, m).reshape(first.batch, -1).astype(np.float64)
+        x = synth.stage_input(first, m).astype(np.float64)
+        x = x.mean(axis=(1, 2)) if pooled else x.reshape(first.batch, -1)
         return np.argmax(x @ T, axis=1).astype(np.int32)
     return labels
 
@@ -135,10 +142,15 @@ def policy_losses(workload, steps: int, policies: Sequence[str] = ("spectrain", 
         specs = [dataclasses.replace(s, policy=policy) for s in workload.stages]
         pipe = Pipeline(specs, [synth.initial_params(s) for s in workload.stages], device=device)
 
+        full = len(specs) == specs[0].num_stages
+
         def draw(sp, m):
+            # in a whole pipeline only stage 0 reads its input (the others take
+            # the previous stage's output)
+            x = synth.stage_input(sp, m) if (not full or sp.stage_index == 0) else None
             if sp.head != "ce":
-                return synth.stage_input(sp, m), None, None
-            return synth.stage_input(sp, m), None, (labels or synth.labels)(sp, m)
+                return x, None, None
+            return x, None, (labels or synth.labels)(sp, m)
         out = pipe.run(steps, draw)
         torch.cuda.synchronize()
         losses[policy] = [out["loss"][m].item() for m in range(steps)]

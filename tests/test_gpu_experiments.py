@@ -47,14 +47,16 @@ def test_prediction_rmse_small_stack():
         assert min(r[s]["stale"]) > 0.0
 
 
-def test_policy_losses_match_oracle():
-    """Loss of every mini-batch of the 3-stage reduced MLP pipeline under each
-    staleness policy, against the oracle run with the same policy."""
+@pytest.mark.parametrize("name", ["mlp3_small", "vgg_conv_small_pipe"])
+def test_policy_losses_match_oracle(name):
+    """Loss of every mini-batch of a reduced pipeline (the 3-stage MLP, the
+    4-stage VGG with its classifier) under each staleness policy, against
+    the oracle run with the same policy."""
     from paper_1809_02839_amd import experiments
-    wl = synth.ALL_WORKLOADS["mlp3_small"]
+    wl = synth.ALL_WORKLOADS[name]
     steps = 12
     got = experiments.policy_losses(wl, steps)
-    tol = TOL["fp32"]
+    tol = TOL[wl.stages[0].dtype]
     for policy, losses in got.items():
         ref_wl = synth.Workload(wl.name, tuple(dataclasses.replace(s, policy=policy) for s in wl.stages), steps)
         ref = trajectory.run(ref_wl)
