@@ -675,6 +675,10 @@ void Stage::bwd_fc(int slot, const void* dy, void* dx) {
 }
 
 // ========================================================== CONV 3x3 ====
+// stash ids: l - 1 the output of layer l - 1 (input of layer l, l >= 1); with a
+// CE head also L - 1 the last output, L the pooled tensor, L + 1 the
+// class-score gradient. workspace: 0/1 gradient ping-pong, 2 class scores
+// (f32), 3 per-sample losses, 4 pooled gradient, then column-sum partials.
 void Stage::fwd_conv(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
   const int L = d_.num_layers, B = d_.batch, Cin = d_.dims[0], Cout = d_.dims[1], H = d_.dims[2], W = d_.dims[3];
   const int P = B * H * W;
@@ -759,6 +763,10 @@ void Stage::bwd_conv(int slot, const void* dy, void* dx) {
 
 // ======================================================== BOTTLENECK ====
 // y = relu(x + conv1x1_3(relu(conv3x3_2(relu(conv1x1_1(x)))))).
+// stash ids 3 l + j: 0 t1, 1 t2, 2 block output (l < L - 1, or every block with
+// a CE head); with a CE head 3 L the pooled tensor, 3 L + 1 the class-score
+// gradient. workspace: 0/1 output-gradient ping-pong, 2 dt2, 3 dt1, 4 class
+// scores (f32), 5 per-sample losses, 6 pooled gradient, then column-sum partials.
 void Stage::fwd_bneck(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
   const int L = d_.num_layers, B = d_.batch, C = d_.dims[0], Cm = d_.dims[1], H = d_.dims[2], W = d_.dims[3];
   const int P = B * H * W;
@@ -836,7 +844,8 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
 // Post-LN encoder layer; per layer stash ids 13*l + j:
 // 0 qkv, 1 P (f32; with the fused attention core the softmax row statistics),
 // 2 P (bf16; unused with the fused core), 3 ctx, 4 r1, 5 mean1, 6 rstd1, 7 h,
-// 8 f1, 9 r2, 10 mean2, 11 rstd2, 12 layer output (l < L-1).
+// 8 f1, 9 r2, 10 mean2, 11 rstd2, 12 layer output (l < L-1, or every layer
+// with a CE head); id 13 L: dlogits (bf16) with a CE head.
 void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
   const int L = d_.num_layers, B = d_.batch, d = d_.dims[0], Hh = d_.dims[1], F = d_.dims[2], S = d_.dims[3];
   const int T = B * S, dh = d / Hh;
@@ -923,7 +932,8 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
 }
 
 // workspace ids: 0 scores/dP (f32), 1 dS, 2/3 layer-output gradient ping-pong,
-// 4 dr2, 5 df1, 6 dh, 7 dr1, 8 dctx, 9 dqkv, 10 partials
+// 4 dr2, 5 df1, 6 dh, 7 dr1, 8 dctx, 9 dqkv, 10 logits (f32, CE head),
+// 11 per-token losses (CE head), 12 column-sum partials
 void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
   const int L = d_.num_layers, B = d_.batch, d = d_.dims[0], Hh = d_.dims[1], F = d_.dims[2], S = d_.dims[3];
   const int T = B * S, dh = d / Hh;
