@@ -108,21 +108,36 @@ def teacher_labels(workload, seed: int = 4242):
     """A learnable labelling of a workload's synthetic inputs: the class a fixed
     seeded random linear map of the first stage's input scores highest (the
     uniform random labels of the parity tests carry nothing to learn). For
-    workloads whose loss head takes one label per sample (FC, conv)."""
+    FC, conv and transformer pipelines (one label per token)."""
     import synth
     first, last = workload.stages[0], workload.stages[-1]
     classes = last.num_classes() if hasattr(last, "num_classes") else last.dims[1]
     rng = np.random.default_rng(seed)
     # conv models end in a global average pool, so their teacher reads the
-    # input averaged over positions (a function the pooled head can express)
+    # input averaged over positions (a function the pooled head can express);
+    # a transformer labels every token from that token's input embedding
+    # (its targets come from the first 1024 tokens of the vocabulary; the head
+    # still scores all of them). Labels are cached per mini-batch.
     pooled = first.kind in ("conv3x3", "bottleneck")
-    width = first.input_shape()[-1] if pooled else int(np.prod(first.input_shape()[1:]))
-    T = rng.standard_normal((width, classes))
+    per_token = last.kind == "transformer"
+    if pooled or per_token:
+        width = first.input_shape()[-1]
+    else:
+        width = int(np.prod(first.input_shape()[1:]))
+    used = min(classes, 1024) if per_token else classes
+    T = rng.standard_normal((width, used)).astype(np.float32)
+    cache = {}
 
     def labels(sp, m):
-        x = synth.stage_input(first, m).astype(np.float64)
-        x = x.mean(axis=(1, 2)) if pooled else x.reshape(first.batch, -1)
-        return np.argmax(x @ T, axis=1).astype(np.int32)
+        if m not in cache:
+            x = synth.stage_input(first, m)
+            if per_token:
+                cache[m] = np.argmax(x.reshape(-1, width) @ T, axis=1).astype(np.int32).reshape(sp.label_shape())
+            else:
+                x = x.astype(np.float64)
+                x = x.mean(axis=(1, 2)) if pooled else x.reshape(first.batch, -1)
+                cache[m] = np.argmax(x @ T, axis=1).astype(np.int32)
+        return cache[m]
     return labels
 
 
@@ -151,7 +166,10 @@ def policy_losses(workload, steps: int, policies: Sequence[str] = ("spectrain", 
             if sp.head != "ce":
                 return x, None, None
             return x, None, (labels or synth.labels)(sp, m)
-        out = pipe.run(steps, draw)
+        def progress(k, count, st):
+            if k == 0 and count % 50 == 0:
+                print(f"[policies] {policy}: {count} of {steps} updates at stage 0", file=sys.stderr, flush=True)
+        out = pipe.run(steps, draw, on_update=progress)
         torch.cuda.synchronize()
         losses[policy] = [out["loss"][m].item() for m in range(steps)]
         print(f"[policies] {policy}: {steps} mini-batches", file=sys.stderr, flush=True)
@@ -173,6 +191,7 @@ def main(argv=None):
     b.add_argument("--steps", type=int, default=60)
     b.add_argument("--random-labels", action="store_true",
                    help="uniform random labels instead of the linear-teacher labels")
+    b.add_argument("--lr", type=float, default=None, help="learning rate for every stage instead of the workload's")
     args = ap.parse_args(argv)
     if args.cmd == "rmse":
         spec = snn_spec(args.layers, args.hidden, args.batch, dtype=args.dtype)
@@ -187,9 +206,12 @@ def main(argv=None):
     else:
         import synth
         wl = synth.ALL_WORKLOADS[args.workload]
+        if args.lr is not None:
+            wl = synth.Workload(wl.name, tuple(dataclasses.replace(s, lr=args.lr) for s in wl.stages), wl.steps)
         losses = policy_losses(wl, args.steps, labels=None if args.random_labels else teacher_labels(wl))
         tail = max(1, args.steps // 4)
         print(json.dumps({"experiment": "policy_losses", "workload": args.workload, "steps": args.steps,
+                          "lr": wl.stages[0].lr,
                           "labels": "random" if args.random_labels else "linear teacher",
                           "mean_loss_last_quarter": {p: float(np.mean(l[-tail:])) for p, l in losses.items()},
                           "losses": losses}))
