@@ -187,6 +187,28 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* partial,
   }
 }
 
+// colsum_final_kernel over partial rows of `stride` floats (columns [0, cols)
+// of each row), the same order of additions.
+__global__ __launch_bounds__(256) void colsum_strided_final_kernel(const float* partial, int nchunks, int cols,
+                                                                   int stride, float* out) {
+  __shared__ float sh[16][16];
+  const int cx = threadIdx.x & 15, cy = threadIdx.x >> 4;
+  const int col = blockIdx.x * 16 + cx;
+  float s = 0.0f;
+  if (col < cols) {
+#pragma unroll 8
+    for (int c = cy; c < nchunks; c += 16) s += partial[static_cast<long>(c) * stride + col];
+  }
+  sh[cy][cx] = s;
+  __syncthreads();
+  if (cy == 0 && col < cols) {
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) v += sh[w][cx];
+    out[col] = v;
+  }
+}
+
 // ---------------------------------------------------- cross-entropy ----
 // Long rows (CE_LDS_MIN <= C <= CE_LDS_MAX, C % 4 == 0): the row is read from
 // memory once into LDS (128 KB), and the max, the sum of exponentials and
@@ -384,17 +406,20 @@ __global__ __launch_bounds__(NT) void layernorm_fwd_kernel(const bf16_t* r, cons
 }
 
 // Rows per block in the backward; per-block partial dgamma/dbeta.
+// Partials are [block][3 D]: the column sums of dr, then of dy * x_hat
+// (dgamma), then of dy (dbeta).
 template <int VPL>
 __global__ __launch_bounds__(NT) void layernorm_bwd_kernel(const bf16_t* dy, const bf16_t* r, const float* mean,
                                                            const float* rstd, const bf16_t* gamma, int R, int D,
-                                                           bf16_t* dr, float* part_g, float* part_b) {
+                                                           bf16_t* dr, float* part) {
   __shared__ float shg[4][64 * VPL];
   __shared__ float shb[4][64 * VPL];
+  __shared__ float shd[4][64 * VPL];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float gm[VPL], pg[VPL], pb[VPL];
+  float gm[VPL], pg[VPL], pb[VPL], pd[VPL];
   ld_row<VPL>(gamma + lane * VPL, gm);
 #pragma unroll
-  for (int j = 0; j < VPL; ++j) pg[j] = pb[j] = 0.0f;
+  for (int j = 0; j < VPL; ++j) pg[j] = pb[j] = pd[j] = 0.0f;
   // wave w takes rows w, w + 4, ...: all of its rows are loaded before any
   // is reduced, so the loads overlap the cross-lane sums
   constexpr int RPW = LNB_ROWS / 4;
@@ -430,18 +455,24 @@ __global__ __launch_bounds__(NT) void layernorm_bwd_kernel(const bf16_t* dy, con
     }
     const float m1 = wave_sum(s1) / static_cast<float>(D), m2 = wave_sum(s2) / static_cast<float>(D);
 #pragma unroll
-    for (int j = 0; j < VPL; ++j) d[j] = rs * (d[j] - m1 - xh[j] * m2);
+    for (int j = 0; j < VPL; ++j) {
+      d[j] = rs * (d[j] - m1 - xh[j] * m2);
+      pd[j] += bf16_to_f32(f32_to_bf16(d[j]));   // the value stored below
+    }
     st_row<VPL>(dr + base, d);
   }
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
     shg[w][lane * VPL + j] = pg[j];
     shb[w][lane * VPL + j] = pb[j];
+    shd[w][lane * VPL + j] = pd[j];
   }
   __syncthreads();
+  float* prow = part + static_cast<long>(blockIdx.x) * 3 * D;
   for (int c = threadIdx.x; c < D; c += NT) {
-    part_g[static_cast<long>(blockIdx.x) * D + c] = (shg[0][c] + shg[1][c]) + (shg[2][c] + shg[3][c]);
-    part_b[static_cast<long>(blockIdx.x) * D + c] = (shb[0][c] + shb[1][c]) + (shb[2][c] + shb[3][c]);
+    prow[c] = (shd[0][c] + shd[1][c]) + (shd[2][c] + shd[3][c]);
+    prow[D + c] = (shg[0][c] + shg[1][c]) + (shg[2][c] + shg[3][c]);
+    prow[2 * D + c] = (shb[0][c] + shb[1][c]) + (shb[2][c] + shb[3][c]);
   }
 }
 
@@ -626,23 +657,31 @@ hipError_t layernorm_fwd(const bf16_t* r, const bf16_t* gamma, const bf16_t* bet
 }
 
 hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd, const bf16_t* gamma,
-                         int R, int D, bf16_t* dr, float* dgamma, float* dbeta, float* partial_ws, hipStream_t s) {
+                         int R, int D, bf16_t* dr, float* dgamma, float* dbeta, float* dsum, float* partial_ws,
+                         hipStream_t s) {
   if (D % 64 || D > 64 * 32) return hipErrorInvalidValue;
   const int nb = (R + LNB_ROWS - 1) / LNB_ROWS;
-  float* pg = partial_ws;
-  float* pb = partial_ws + static_cast<long>(nb) * D;
   const dim3 grid(nb), block(NT);
+  float* p = partial_ws;
   switch (D / 64) {
-    case 1: hipLaunchKernelGGL(layernorm_bwd_kernel<1>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
-    case 2: hipLaunchKernelGGL(layernorm_bwd_kernel<2>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
-    case 4: hipLaunchKernelGGL(layernorm_bwd_kernel<4>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
-    case 8: hipLaunchKernelGGL(layernorm_bwd_kernel<8>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
-    case 16: hipLaunchKernelGGL(layernorm_bwd_kernel<16>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
-    case 32: hipLaunchKernelGGL(layernorm_bwd_kernel<32>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, pg, pb); break;
+    case 1: hipLaunchKernelGGL(layernorm_bwd_kernel<1>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, p); break;
+    case 2: hipLaunchKernelGGL(layernorm_bwd_kernel<2>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, p); break;
+    case 4: hipLaunchKernelGGL(layernorm_bwd_kernel<4>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, p); break;
+    case 8: hipLaunchKernelGGL(layernorm_bwd_kernel<8>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, p); break;
+    case 16: hipLaunchKernelGGL(layernorm_bwd_kernel<16>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, p); break;
+    case 32: hipLaunchKernelGGL(layernorm_bwd_kernel<32>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, p); break;
     default: return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 15) / 16), dim3(256), 0, s, pg, nb, D, dgamma, 0);
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((D + 15) / 16), dim3(256), 0, s, pb, nb, D, dbeta, 0);
+  // partial columns [0, D) sum dr, [D, 2D) dgamma, [2D, 3D) dbeta
+  if (dsum && dsum + D == dgamma && dgamma + D == dbeta) {
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((3 * D + 15) / 16), dim3(256), 0, s, p, nb, 3 * D, dsum, 0);
+    return hipGetLastError();
+  }
+  float* out[3] = {dsum, dgamma, dbeta};
+  for (int i = 0; i < 3; ++i)
+    if (out[i])
+      hipLaunchKernelGGL(colsum_strided_final_kernel, dim3((D + 15) / 16), dim3(256), 0, s, p + i * D, nb, D, 3 * D,
+                         out[i]);
   return hipGetLastError();
 }
 

@@ -129,7 +129,7 @@ hipError_t attention_bwd(const bf16_t* qkv, const bf16_t* dctx, const float* sta
 constexpr int COLSUM_ROWS = 64;   // rows summed per block in the first pass
 constexpr int LNB_ROWS = 16;      // rows per block of the layer-norm backward
 inline long column_sum_ws_floats(long rows, long cols) { return ((rows + COLSUM_ROWS - 1) / COLSUM_ROWS) * cols; }
-inline long layernorm_bwd_ws_floats(long rows, long d) { return 2 * ((rows + LNB_ROWS - 1) / LNB_ROWS) * d; }
+inline long layernorm_bwd_ws_floats(long rows, long d) { return 3 * ((rows + LNB_ROWS - 1) / LNB_ROWS) * d; }
 
 // ------------------------------------------------------------ elementwise ----
 // dst[i] = src[i] * (mask[i] > 0), bf16 (dtype 1) or float32 (dtype 0).
@@ -146,9 +146,12 @@ hipError_t softmax_ce(const float* logits, const int32_t* labels, int R, int C, 
 hipError_t layernorm_fwd(const bf16_t* r, const bf16_t* gamma, const bf16_t* beta, int R, int D, float eps,
                          bf16_t* y, float* mean, float* rstd, hipStream_t s);
 // Layer-norm backward for bf16 dy: dr = bf16(...); dgamma/dbeta (float32,
-// overwritten) reduced over rows deterministically.
+// overwritten) reduced over rows deterministically. dsum (may be null): the
+// column sums of the stored dr as well (the bias gradient of the linear layer
+// that produced the normalised sum); when dsum, dgamma, dbeta are adjacent
+// D-float ranges one final reduction writes all three.
 hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd,
-                         const bf16_t* gamma, int R, int D, bf16_t* dr, float* dgamma, float* dbeta,
+                         const bf16_t* gamma, int R, int D, bf16_t* dr, float* dgamma, float* dbeta, float* dsum,
                          float* partial_ws, hipStream_t s);
 // Row softmax of float32 scores [R, C] -> P float32 and bf16(P).
 hipError_t softmax_rows(const float* S, int R, int C, float* P, bf16_t* Pb, hipStream_t s);

@@ -975,11 +975,11 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     bf16_t* dqkv = ws<bf16_t>(9);
 
     LAUNCH("layernorm_bwd", 0, 0, layernorm_bwd(static_cast<const bf16_t*>(gy), r2, stash<float>(slot, q + 10), stash<float>(slot, q + 11),
-                            static_cast<const bf16_t*>(wb(p + 10)), T, d, dr2, grad(p + 10), grad(p + 11), part, s_));
+                            static_cast<const bf16_t*>(wb(p + 10)), T, d, dr2, grad(p + 10), grad(p + 11), grad(p + 9),
+                            part, s_));   // also the FFN output bias gradient: column sums of dr2
     GemmDesc w2 = gd(d, F, T, opR(dr2, d), opR(f1, F), F);
     w2.epi.out_f32 = grad(p + 8);
     gemm(w2);
-    LAUNCH("bias_grad", 0, 0, column_sum(dr2, 1, T, d, d, grad(p + 9), 0, part, s_));
     GemmDesc x2 = gd(T, F, d, opK(dr2, d), opR(wb(p + 8), F), F);
     x2.epi.mask = f1;
     x2.epi.out_bf16 = df1;
@@ -993,11 +993,11 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     x1.epi.out_bf16 = dhh;
     gemm(x1);
     LAUNCH("layernorm_bwd", 0, 0, layernorm_bwd(dhh, r1, stash<float>(slot, q + 5), stash<float>(slot, q + 6),
-                            static_cast<const bf16_t*>(wb(p + 4)), T, d, dr1, grad(p + 4), grad(p + 5), part, s_));
+                            static_cast<const bf16_t*>(wb(p + 4)), T, d, dr1, grad(p + 4), grad(p + 5), grad(p + 3),
+                            part, s_));   // also the attention output bias gradient: column sums of dr1
     GemmDesc wo = gd(d, d, T, opR(dr1, d), opR(ctx, d), d);
     wo.epi.out_f32 = grad(p + 2);
     gemm(wo);
-    LAUNCH("bias_grad", 0, 0, column_sum(dr1, 1, T, d, d, grad(p + 3), 0, part, s_));
     GemmDesc xo = gd(T, d, d, opK(dr1, d), opR(wb(p + 2), d), d);
     xo.epi.out_bf16 = dctx;
     gemm(xo);
