@@ -18,6 +18,10 @@ Output: one JSON line on stdout. `value` is samples per second; `roofline`
 describes the kernel family with the largest share of the step time, measured
 in a separate pass with HIP events around each launch on the stage's stream;
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+`step_roofline_frac` is the step's lower bound (every contraction at the MFMA
+peak plus the update's algorithmic bytes at the HBM peak) over the measured
+step; `predict_update_GBps_cold` is the fused update's bandwidth in a pass
+that evicts every cache before each update.
 """
 import argparse
 import dataclasses
@@ -35,6 +39,8 @@ PEAK_HBM_GBPS = 8000.0
 METRIC = "stage samples/sec (fwd+bwd+predict+update); MFMA util %; predict/update GB/s"
 
 DESCRIPTIONS = {
+    "mlp3": "3-stage pipeline of one fully connected layer per stage (784->256->256->10), batch 32, float32, "
+            "softmax-CE head on the last stage",
     "vgg_conv": "VGG-16-style conv stage: 4x conv3x3 256->512->512->512->512, 8x8 maps, NHWC, ReLU",
     "resnet_bottleneck": "ResNet-152-style stage: 8 bottlenecks 1024->256->256->1024, 14x14 maps, identity skip",
     "transformer_enc": "Transformer encoder stage: 3 post-LN layers, d=512, 8 heads, FFN 2048, seq 128",
@@ -45,6 +51,8 @@ DESCRIPTIONS = {
                             "softmax-CE head on the last stage",
     "reslstm_pipe": "4-stage pipeline of residual LSTM stages (8 layers, hidden 1024, T=35) with a "
                     "10000-token softmax-CE head on the last stage",
+    "transformer_enc_last": "Last transformer encoder stage: 3 post-LN layers, d=512, seq 128, with the "
+                            "32000-token vocabulary projection and softmax-CE head",
 }
 
 
@@ -124,10 +132,12 @@ class StageLoop:
         else:
             self.st.forward(m, self.x[r], self.y[m % (self.depth + 1)])
 
-    def steps(self, n):
+    def steps(self, n, before_update=None):
         for _ in range(n):
             m = self.next_b
             self.st.backward(m, None if self.dy is None else self.dy[m % self.ring], self.dx)
+            if before_update is not None:
+                before_update()
             self.st.update(self.sf, self.sb)
             self._forward(m + self.depth)
             self.next_b += 1
@@ -144,7 +154,7 @@ class PipeLoop:
         import synth
         self.torch, self.specs, self.stream = torch, list(specs), stream
         dev = torch.device("cuda")
-        dt = torch.bfloat16
+        dt = torch.bfloat16 if self.specs[0].dtype == "bf16" else torch.float32
         self.N = len(self.specs)
         self.ring = ring
         self.st, self.sf, self.sb = [], [], []
@@ -178,7 +188,7 @@ class PipeLoop:
         self.m0 = 0
         stream.synchronize()
 
-    def steps(self, n):
+    def steps(self, n, before_update=None):
         """n mini-batches through the whole pipeline (fill and drain included)."""
         from paper_1809_02839_amd.pipeline import pipeline_task_order
         N, d = self.N, self.depth
@@ -198,6 +208,8 @@ class PipeLoop:
                     dy = None if self.dy is None else self.dy[m % self.ring]
                 dx = self.dx[k][m % d] if k > 0 else self.dx0
                 st.backward(m, dy, dx)
+                if before_update is not None:
+                    before_update()
                 st.update(self.sf[k], self.sb[k])
         self.m0 += n
 
@@ -285,6 +297,9 @@ def main():
     ap.add_argument("--policy", default="spectrain", choices=["spectrain", "vanilla", "stash"],
                     help="weight staleness treatment (Section 4.2): SpecTrain prediction (default), Vanilla "
                          "pipelining (latest weights) or weight stashing (backward reuses the forward's weights)")
+    ap.add_argument("--cold-steps", type=int, default=10,
+                    help="steps of a second per-launch pass in which a 1 GiB write evicts the caches (MALL "
+                         "included) before every update, for the update's cold-cache bandwidth (0: skip)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (a known-size reference "
                          "dispatch for scaling hardware byte counters)")
@@ -341,6 +356,27 @@ def main():
         prof = loop.st.profile_read()
         loop.st.profile(False)
     torch.cuda.synchronize()
+    upd_cold_gbps = None
+    if args.cold_steps > 0:
+        # the same per-launch pass with the caches evicted before every update:
+        # W, v and g then come from HBM, as they would after a long backward
+        evict = torch.empty(1 << 28, device="cuda")   # 1 GiB, four times the MALL
+
+        def flush():
+            with torch.cuda.stream(stream):
+                evict.fill_(0.0)
+        target = loop if pipeline else loop.st
+        target.profile(True)
+        loop.steps(args.cold_steps, before_update=flush)
+        cold = loop.profile_read() if pipeline else loop.st.profile_read()
+        target.profile(False)
+        torch.cuda.synchronize()
+        del evict
+        u = cold.get("fused_update")
+        if u and u["ms_total"] > 0:
+            upd_cold_gbps = u["bytes_total"] / (u["ms_total"] / 1e3) / 1e9
+            log(f"[bench]   fused_update cold     {u['ms_total'] / u['launches'] * 1e3:9.1f} us/launch  "
+                f"{upd_cold_gbps:.0f} GB/s (caches evicted before each update)")
     fam_ms = {k: v["ms_total"] / args.profile_steps for k, v in prof.items()}
     for k, v in prof.items():
         extra = ""
@@ -369,6 +405,10 @@ def main():
     gemm_ms = sum(v["ms_total"] for k, v in prof.items() if v["flops_total"] > 0)
     upd = prof.get("fused_update")
     upd_gbps = upd["bytes_total"] / (upd["ms_total"] / 1e3) / 1e9 if upd else None
+    # Lower bound of the step: every contraction at the MFMA peak plus the
+    # update's algorithmic bytes at the HBM peak (other passes count as zero).
+    upd_bytes = upd["bytes_total"] / args.profile_steps if upd else 0.0
+    bound_us = (gemm_flops / args.profile_steps / (peak_mfma * 1e12) + upd_bytes / (PEAK_HBM_GBPS * 1e9)) * 1e6
 
     cpu = None
     if not args.no_cpu:
@@ -399,6 +439,9 @@ def main():
         "mfma_util_pct_of_step": round(100.0 * gemm_flops / args.profile_steps / (ms_step / 1e3) / 1e12 / peak_mfma, 2),
         "predict_update_GBps": round(upd_gbps, 1) if upd_gbps else None,
         "predict_update_frac_hbm": round(upd_gbps / PEAK_HBM_GBPS, 4) if upd_gbps else None,
+        "predict_update_GBps_cold": round(upd_cold_gbps, 1) if upd_cold_gbps else None,
+        "step_bound_us": round(bound_us, 2),
+        "step_roofline_frac": round(bound_us / (ms_step * 1e3), 4),
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -11,11 +11,17 @@ Two summaries, written as short markdown files:
   sources the counters were taken with; a reader compares it with the current
   sources and treats the figures as stale when they differ.
 
+* matrix-core activity: per-kernel means of one `--pmc` run over
+  `SQ_VALU_MFMA_BUSY_CYCLES` (and any other counters), with the MFMA-busy
+  fraction = MFMA busy cycles / (dispatch duration x 2.4 GHz x 1024 SIMDs),
+  the duration taken from the dispatch's own start and end timestamps.
+
 Command line:
 
     python -m paper_1809_02839_amd.profiling stats <kernel_stats.csv> <out.md> --title T --command C
     python -m paper_1809_02839_amd.profiling traffic <fetch_dir> <write_dir> <out.md>
         --calib-bytes B --calib-marker neg --title T --command C
+    python -m paper_1809_02839_amd.profiling counters <pmc_dir> <out.md> --title T --command C
 """
 import argparse
 import csv
@@ -144,6 +150,55 @@ def read_traffic(md_path):
     return digest, table
 
 
+SIMDS = 256 * 4          # MI355X: 256 compute units of four SIMDs
+NOMINAL_CLOCK_HZ = 2.4e9  # the clock of the published peaks
+DURATION = "duration ns"
+
+
+def counter_means(run_dir):
+    """{kernel short name: (dispatches, {counter: mean per dispatch})} of one
+    --pmc run; the pseudo-counter DURATION is the mean dispatch duration."""
+    per = {}
+    names = {}
+    for r in _counter_rows(run_dir):
+        d = int(r["Dispatch_Id"])
+        key = (d, r["Counter_Name"])
+        per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+        names[d] = short_name(r["Kernel_Name"])
+        if "Start_Timestamp" in r and "End_Timestamp" in r:
+            per[(d, DURATION)] = float(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    acc = {}
+    for (d, c), v in per.items():
+        k = names[d]
+        ds, sums = acc.setdefault(k, (set(), {}))
+        ds.add(d)
+        sums[c] = sums.get(c, 0.0) + v
+    return {k: (len(ds), {c: v / len(ds) for c, v in sums.items()}) for k, (ds, sums) in acc.items()}
+
+
+def write_counters(run_dir, out_md, title, command, notes=""):
+    table = counter_means(run_dir)
+    counters = sorted({c for _, cs in table.values() for c in cs})
+    mfma = "SQ_VALU_MFMA_BUSY_CYCLES" in counters and DURATION in counters
+    with open(out_md, "w") as f:
+        f.write(f"# {title}\n\n")
+        f.write("Command (repo root on the GPU box):\n\n```\n" + command.strip() + "\n```\n\n")
+        if notes:
+            f.write(notes.strip() + "\n\n")
+        f.write(f"source digest: {source_digest()}\n\n")
+        head = ["kernel", "dispatches"] + [f"{c} / dispatch" for c in counters] + (["MFMA busy %"] if mfma else [])
+        f.write("| " + " | ".join(head) + " |\n")
+        f.write("|:--|" + "--:|" * (len(head) - 1) + "\n")
+        order = sorted(table, key=lambda k: -table[k][1].get(DURATION, 0.0) * table[k][0])
+        for k in order:
+            n, cs = table[k]
+            cells = [k, str(n)] + [f"{cs.get(c, 0.0):.4g}" for c in counters]
+            if mfma:
+                cyc = cs.get(DURATION, 0.0) * 1e-9 * NOMINAL_CLOCK_HZ * SIMDS
+                cells.append(f"{100.0 * cs.get('SQ_VALU_MFMA_BUSY_CYCLES', 0.0) / cyc:.1f}" if cyc else "")
+            f.write("| " + " | ".join(cells) + " |\n")
+
+
 def write_stats(stats_csv, out_md, title, command, notes=""):
     with open(stats_csv, newline="") as fh:
         rows = list(csv.DictReader(fh))
@@ -178,9 +233,17 @@ def main():
     b.add_argument("--calib-marker", default="neg")
     b.add_argument("--title", required=True)
     b.add_argument("--command", required=True)
+    c = sub.add_parser("counters")
+    c.add_argument("pmc_dir")
+    c.add_argument("out_md")
+    c.add_argument("--title", required=True)
+    c.add_argument("--command", required=True)
+    c.add_argument("--notes", default="")
     args = ap.parse_args()
     if args.cmd == "stats":
         write_stats(args.stats_csv, args.out_md, args.title, args.command, args.notes)
+    elif args.cmd == "counters":
+        write_counters(args.pmc_dir, args.out_md, args.title, args.command, args.notes)
     else:
         rows, fr, fw = traffic_table(args.fetch_dir, args.write_dir, args.calib_bytes, args.calib_marker)
         write_traffic(args.out_md, rows, fr, fw, args.calib_bytes, args.title, args.command)
