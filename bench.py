@@ -298,7 +298,7 @@ def main():
                     help="weight staleness treatment (Section 4.2): SpecTrain prediction (default), Vanilla "
                          "pipelining (latest weights) or weight stashing (backward reuses the forward's weights)")
     ap.add_argument("--cold-steps", type=int, default=10,
-                    help="steps of a second per-launch pass in which a 1 GiB write evicts the caches (MALL "
+                    help="steps of a second per-launch pass in which a 1 GiB read evicts the caches (MALL "
                          "included) before every update, for the update's cold-cache bandwidth (0: skip)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (a known-size reference "
@@ -359,19 +359,22 @@ def main():
     upd_cold_gbps = None
     if args.cold_steps > 0:
         # the same per-launch pass with the caches evicted before every update:
-        # W, v and g then come from HBM, as they would after a long backward
-        evict = torch.empty(1 << 28, device="cuda")   # 1 GiB, four times the MALL
+        # W, v and g then come from HBM, as they would after a long backward.
+        # The eviction reads (a sum over 1 GiB, four times the MALL), so it
+        # leaves no dirty lines whose write-back would land in the update.
+        evict = torch.zeros(1 << 28, device="cuda")
+        sink = []
 
         def flush():
             with torch.cuda.stream(stream):
-                evict.fill_(0.0)
+                sink.append(evict.sum())
         target = loop if pipeline else loop.st
         target.profile(True)
         loop.steps(args.cold_steps, before_update=flush)
         cold = loop.profile_read() if pipeline else loop.st.profile_read()
         target.profile(False)
         torch.cuda.synchronize()
-        del evict
+        del evict, sink
         u = cold.get("fused_update")
         if u and u["ms_total"] > 0:
             upd_cold_gbps = u["bytes_total"] / (u["ms_total"] / 1e3) / 1e9
