@@ -2,16 +2,25 @@
 // 64 x 64 block tile, K step 16, 256 threads each computing a 4 x 4 patch
 // with FMAs. Any M, N, K and leading dimension; plain operand modes only.
 // These stages are a few MFLOP per layer, so latency rather than matrix-core
-// throughput bounds them.
+// throughput bounds them: when the tiles are few and K is long, K is split
+// over blocks (each block's K loop stays short) and a second pass sums the
+// partials in split order and applies the epilogue.
+#include <algorithm>
+
 #include "kernels.hpp"
 
 namespace spx {
 namespace {
 
 constexpr int TB = 64, TK = 16, NT = 256;
+constexpr int TARGET_BLOCKS = 128;   // split K until about this many blocks run
+constexpr int MIN_SPLIT_STEPS = 4;   // K steps per split at least
+constexpr int MAX_SPLITS = 64;
 
 struct F32Args {
   int M, N, K;
+  int splits, k_per_split;   // splits > 1: raw partials [split][M][N] to `partial`
+  float* partial;
   const float* A;
   long lda;
   const float* B;
@@ -45,6 +54,18 @@ __device__ __forceinline__ void load_tile(const float* X, long ld, int rows, int
   }
 }
 
+// value = acc * alpha + bias + residual, ReLU, mask, then stored or added.
+__device__ __forceinline__ void epilogue_f32(const F32Args& a, int row, int col, float acc) {
+  const long idx = static_cast<long>(row) * a.ldc + col;
+  float v = acc * a.alpha;
+  if (a.bias) v += a.bias[col];
+  if (a.res) v += a.res[idx];
+  if (a.relu) v = fmaxf(v, 0.0f);
+  if (a.mask && !(a.mask[idx] > 0.0f)) v = 0.0f;
+  if (a.accumulate) a.out[idx] += v;
+  else a.out[idx] = v;
+}
+
 template <int MA, int MB>
 __global__ __launch_bounds__(NT) void gemm_f32_kernel(F32Args a) {
   __shared__ float As[TK][TB + 4];
@@ -53,9 +74,10 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(F32Args a) {
   const int row0 = blockIdx.y * TB, col0 = blockIdx.x * TB;
   const int tx = tid & 15, ty = tid >> 4;
   float acc[4][4] = {};
-  for (int k0 = 0; k0 < a.K; k0 += TK) {
-    load_tile<MA>(a.A, a.lda, a.M, a.K, row0, k0, tid, As);
-    load_tile<MB>(a.B, a.ldb, a.N, a.K, col0, k0, tid, Bs);
+  const int kbeg = blockIdx.z * a.k_per_split, kend = min(a.K, kbeg + a.k_per_split);
+  for (int k0 = kbeg; k0 < kend; k0 += TK) {
+    load_tile<MA>(a.A, a.lda, a.M, kend, row0, k0, tid, As);
+    load_tile<MB>(a.B, a.ldb, a.N, kend, col0, k0, tid, Bs);
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < TK; ++k) {
@@ -79,22 +101,34 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(F32Args a) {
     for (int j = 0; j < 4; ++j) {
       const int col = col0 + tx * 4 + j;
       if (col >= a.N) continue;
-      const long idx = static_cast<long>(row) * a.ldc + col;
-      float v = acc[i][j] * a.alpha;
-      if (a.bias) v += a.bias[col];
-      if (a.res) v += a.res[idx];
-      if (a.relu) v = fmaxf(v, 0.0f);
-      if (a.mask && !(a.mask[idx] > 0.0f)) v = 0.0f;
-      if (a.accumulate) a.out[idx] += v;
-      else a.out[idx] = v;
+      if (a.splits > 1)
+        a.partial[(static_cast<long>(blockIdx.z) * a.M + row) * a.N + col] = acc[i][j];
+      else
+        epilogue_f32(a, row, col, acc[i][j]);
     }
+  }
+}
+
+// Sums the split partials of each output in split order, then the epilogue.
+__global__ __launch_bounds__(256) void gemm_f32_reduce_kernel(F32Args a) {
+  const long mn = static_cast<long>(a.M) * a.N;
+  for (long t = static_cast<long>(blockIdx.x) * 256 + threadIdx.x; t < mn; t += static_cast<long>(gridDim.x) * 256) {
+    float s = a.partial[t];
+    for (int sp = 1; sp < a.splits; ++sp) s += a.partial[sp * mn + t];
+    const int row = static_cast<int>(t / a.N), col = static_cast<int>(t - static_cast<long>(row) * a.N);
+    epilogue_f32(a, row, col, s);
   }
 }
 
 template <int MA, int MB>
 hipError_t launch(const F32Args& a, hipStream_t s) {
-  dim3 grid((a.N + TB - 1) / TB, (a.M + TB - 1) / TB);
+  dim3 grid((a.N + TB - 1) / TB, (a.M + TB - 1) / TB, a.splits);
   hipLaunchKernelGGL((gemm_f32_kernel<MA, MB>), grid, dim3(NT), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.splits == 1) return e;
+  const long mn = static_cast<long>(a.M) * a.N;
+  const long blocks = std::min<long>((mn + 255) / 256, 4096);
+  hipLaunchKernelGGL(gemm_f32_reduce_kernel, dim3(static_cast<int>(blocks)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -119,6 +153,20 @@ hipError_t gemm_f32(const GemmDesc& d, hipStream_t s) {
   a.alpha = d.epi.alpha;
   a.relu = d.epi.relu;
   a.accumulate = d.epi.accumulate;
+  // K split: enough blocks to hide the K loop's latency, each split at least
+  // MIN_SPLIT_STEPS steps long, partials within the workspace.
+  const long tiles = static_cast<long>((a.N + TB - 1) / TB) * ((a.M + TB - 1) / TB);
+  const int ksteps = (a.K + TK - 1) / TK;
+  int splits = 1;
+  if (d.workspace && tiles < TARGET_BLOCKS && ksteps >= 2 * MIN_SPLIT_STEPS) {
+    splits = static_cast<int>(std::min<long>(TARGET_BLOCKS / tiles, ksteps / MIN_SPLIT_STEPS));
+    splits = std::min(splits, MAX_SPLITS);
+    while (splits > 1 && static_cast<size_t>(splits) * a.M * a.N * 4 > d.workspace_bytes) --splits;
+  }
+  const int steps_per = std::max(1, (ksteps + splits - 1) / splits);
+  a.splits = std::max(1, (ksteps + steps_per - 1) / steps_per);   // no empty split
+  a.k_per_split = steps_per * TK;
+  a.partial = d.workspace;
   const int ma = d.A.mode, mb = d.B.mode;
   if (ma == OP_K_PLAIN && mb == OP_K_PLAIN) return launch<OP_K_PLAIN, OP_K_PLAIN>(a, s);
   if (ma == OP_K_PLAIN && mb == OP_R_PLAIN) return launch<OP_K_PLAIN, OP_R_PLAIN>(a, s);

@@ -171,10 +171,8 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
   else if (ma == OP_R_PLAIN && mb == OP_R_PLAIN) name = dt_ ? "gemm_bf16_dyTx" : "gemm_f32_dyTx";
   const double flops = 2.0 * d.M * d.N * static_cast<double>(d.K) * d.batch;
   GemmDesc dd = d;
-  if (dt_) {
-    dd.workspace = ws<float>(static_cast<int>(ws_off_.size()) - 1);
-    dd.workspace_bytes = gemm_ws_bytes_;
-  }
+  dd.workspace = ws<float>(static_cast<int>(ws_off_.size()) - 1);
+  dd.workspace_bytes = gemm_ws_bytes_;
   if (!dt_) {
     LAUNCH(name, flops, 0, gemm_f32(dd, s_));
     return;
@@ -263,7 +261,7 @@ void Stage::plan_buffers() {
   std::vector<size_t> st, ws;   // byte sizes, indexed by buffer id
   auto partial_floats = [](long rows, long cols) { return column_sum_ws_floats(rows, cols); };
   long partial = 0;
-  gemm_ws_bytes_ = dt_ ? (64u << 20) : 0;
+  gemm_ws_bytes_ = dt_ ? (64u << 20) : (8u << 20);   // split-K partials
   switch (d_.kind) {
     case SPECTRAIN_KIND_FC: {
       const long C = dm[1], hid = dm[2], maxw = std::max<long>(std::max<long>(dm[0], dm[1]), dm[2]);
