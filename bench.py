@@ -409,8 +409,11 @@ def main():
     upd = prof.get("fused_update")
     upd_gbps = upd["bytes_total"] / (upd["ms_total"] / 1e3) / 1e9 if upd else None
     # Lower bound of the step: every contraction at the MFMA peak plus the
-    # update's algorithmic bytes at the HBM peak (other passes count as zero).
-    upd_bytes = upd["bytes_total"] / args.profile_steps if upd else 0.0
+    # update's algorithmic bytes at the HBM peak (other passes count as zero):
+    # W, v, g read and W, v written in float32, both predicted slots written
+    # in the operand dtype, once per stage per step.
+    esz = 2 if spec.dtype == "bf16" else 4
+    upd_bytes = float(sum(synth.num_params(sp) for sp in specs)) * (12 + 8 + 2 * esz)
     bound_us = (gemm_flops / args.profile_steps / (peak_mfma * 1e12) + upd_bytes / (PEAK_HBM_GBPS * 1e9)) * 1e6
 
     cpu = None
