@@ -231,6 +231,29 @@ class PipeLoop:
             st.destroy()
 
 
+def host_info():
+    """CPU model and the BLAS library (and its threads) NumPy runs on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        import numpy  # noqa: F401  (loads the BLAS library threadpoolctl reports)
+        from threadpoolctl import threadpool_info
+        libs = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        if libs:
+            blas = f"{libs[0].get('internal_api')} {libs[0].get('version')} ({libs[0].get('num_threads')} threads)"
+    except Exception:
+        pass
+    return {"cpu_model": model, "blas": blas}
+
+
 def cpu_baseline_pipeline(specs, n_steps):
     """The oracle as it stands on the host: n_steps mini-batches through all
     stages of the pipeline workload (each stage's forward, backward, update)."""
@@ -250,7 +273,7 @@ def cpu_baseline_pipeline(specs, n_steps):
     _ = np
     return {"value": specs[0].batch / per_step, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{n_steps} full-size mini-batches through all {len(specs)} stages (forward, backward, "
-                      f"update each), float64 NumPy, {per_step:.2f} s per mini-batch"}
+                      f"update each), float64 NumPy, {per_step:.2f} s per mini-batch", **host_info()}
 
 
 def cpu_baseline(spec, n_steps):
@@ -282,7 +305,7 @@ def cpu_baseline(spec, n_steps):
     per_step = dt / n_steps
     return {"value": spec.batch / per_step, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{n_steps} full-size steps (forward, backward, update) of the same stage, "
-                      f"float64 NumPy, {per_step:.2f} s per step"}
+                      f"float64 NumPy, {per_step:.2f} s per step", **host_info()}
 
 
 def main():
@@ -297,6 +320,8 @@ def main():
     ap.add_argument("--policy", default="spectrain", choices=["spectrain", "vanilla", "stash"],
                     help="weight staleness treatment (Section 4.2): SpecTrain prediction (default), Vanilla "
                          "pipelining (latest weights) or weight stashing (backward reuses the forward's weights)")
+    ap.add_argument("--median-steps", type=int, default=50,
+                    help="steps of a pass with an event between steps, for the median step time (0: skip)")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="steps of a second per-launch pass in which a 1 GiB read evicts the caches (MALL "
                          "included) before every update, for the update's cold-cache bandwidth (0: skip)")
@@ -343,6 +368,20 @@ def main():
     ms_step = ms_total / args.steps
     value = spec.batch / (ms_step / 1e3)
     log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {value:.0f} samples/s")
+
+    # per-step durations (an event between steps, outside the timed region)
+    ms_median = None
+    if args.median_steps > 0:
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.median_steps + 1)]
+        ev[0].record(stream)
+        for i in range(args.median_steps):
+            loop.steps(1)
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.median_steps))
+        ms_median = per[len(per) // 2]
+        log(f"[bench] per-step median {ms_median:.3f} ms, min {per[0]:.3f}, max {per[-1]:.3f} "
+            f"over {args.median_steps} steps")
 
     # per-kernel pass (events around every launch, separate from the timed region)
     if pipeline:
@@ -431,6 +470,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_median": round(ms_median, 4) if ms_median else None,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
