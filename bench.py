@@ -270,10 +270,18 @@ def cpu_baseline_pipeline(specs, n_steps):
     trajectory.run(wl)
     dt = time.perf_counter() - t0
     per_step = dt / n_steps
+    extra = {}
+    if specs[0].dtype == "fp32":
+        # the small float32 pipeline also on one thread (BLAS threading barely helps at its sizes)
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            trajectory.run(wl)
+            extra["value_1thread"] = specs[0].batch / ((time.perf_counter() - t0) / n_steps)
     _ = np
     return {"value": specs[0].batch / per_step, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{n_steps} full-size mini-batches through all {len(specs)} stages (forward, backward, "
-                      f"update each), float64 NumPy, {per_step:.2f} s per mini-batch", **host_info()}
+                      f"update each), float64 NumPy, {per_step:.2f} s per mini-batch", **extra, **host_info()}
 
 
 def cpu_baseline(spec, n_steps):
@@ -458,8 +466,10 @@ def main():
     cpu = None
     if not args.no_cpu:
         log(f"[bench] timing the CPU oracle on {args.cpu_steps} steps ...")
-        cpu = (cpu_baseline_pipeline(specs, max(1, args.cpu_steps // 4)) if pipeline
-               else cpu_baseline(spec, args.cpu_steps))
+        # whole pipelines: a quarter of the steps (each is N stage steps); the
+        # small float32 pipeline: its full 20 mini-batches (well under a second)
+        n_pipe = wl.steps if spec.dtype == "fp32" else max(1, args.cpu_steps // 4)
+        cpu = cpu_baseline_pipeline(specs, n_pipe) if pipeline else cpu_baseline(spec, args.cpu_steps)
         log(f"[bench] oracle: {cpu['value']:.2f} samples/s on {cpu['cores']} threads")
 
     out = {
