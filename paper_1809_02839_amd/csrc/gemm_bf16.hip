@@ -8,7 +8,8 @@
 // tiles are staged in LDS as [row][k] (8 consecutive k per lane make one
 // 16-byte MFMA operand read; the 144-byte row pitch puts eight consecutive
 // rows on disjoint banks); R-mode tiles (rows contiguous in memory) are staged
-// as [k][row] as loaded and transposed by the LDS reads. Global loads run two K steps ahead of
+// as [k][row] as loaded, with the 16-byte units of each 256-byte k row
+// permuted by an XOR with 4 (k mod 4), and transposed by the LDS reads. Global loads run two K steps ahead of
 // the MFMAs (two register stages, two LDS buffers). All global reads are
 // buffer loads whose resource spans exactly the operand tensor: an offset
 // outside it (zero padding of convolutions, ragged tile edges) reads zero.
@@ -25,9 +26,16 @@ namespace {
 
 constexpr int BM = 128, BN = 128, BK = 64, NT = 256;
 constexpr int PITCH = BK + 8;            // K-mode tile [row][k]: bf16 per row (144 bytes)
-constexpr int RPITCH = 128 + 16;         // R-mode tile [k][row]: bf16 per k row (288 bytes)
-constexpr int TILE_ELEMS = 128 * PITCH;  // one operand tile (= BK * RPITCH)
-static_assert(TILE_ELEMS == BK * RPITCH, "both tile layouts occupy the same LDS");
+constexpr int RPITCH = 128;              // R-mode tile [k][row]: bf16 per k row (256 bytes, swizzled)
+constexpr int TILE_ELEMS = 128 * PITCH;  // one operand tile (K-mode; the R-mode tile needs BK * RPITCH)
+static_assert(TILE_ELEMS >= BK * RPITCH, "both tile layouts fit one operand buffer");
+
+// Element offset, inside a k row of an R-mode tile, of row (column) c: the
+// 16-byte unit c / 8 is XORed with 4 (k mod 4). A transposing read covers
+// four consecutive k rows at the same columns in each 16-lane group; the
+// XOR spreads them over disjoint 64-byte bank ranges, where a common pitch
+// would put the two groups of a half-wave on the same banks.
+__device__ __forceinline__ int rcol(int k, int c) { return (((c >> 3) ^ ((k & 3) << 2)) << 3) | (c & 7); }
 constexpr int BUF_FLAGS = 0x00020000;    // gfx9 raw buffer resource word 3
 constexpr int OOB = 0x7ffffff0;          // byte offset past every resource: the load returns 0
 constexpr int MAX_SPLITS = 16;           // K slices of one split-K launch
@@ -50,7 +58,8 @@ __device__ __forceinline__ bf16x8_t frag_k(const bf16_t* s, int row, int k) {
 // lane / 32). The second read takes the next four k.
 __device__ __forceinline__ bf16x8_t frag_r(const bf16_t* s, int m0, int k0, int lane) {
   const int g = lane >> 4, i = lane & 15;
-  const bf16_t* p = s + (k0 + 8 * (g >> 1) + (i >> 2)) * RPITCH + m0 + 16 * (g & 1) + 4 * (i & 3);
+  const int k = k0 + 8 * (g >> 1) + (i >> 2);   // k + 4 (the second read) has the same swizzle
+  const bf16_t* p = s + k * RPITCH + rcol(k, m0 + 16 * (g & 1) + 4 * (i & 3));
   const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p));
   const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p + 4 * RPITCH));
   const u16x8_t v = {static_cast<uint16_t>(lo[0]), static_cast<uint16_t>(lo[1]), static_cast<uint16_t>(lo[2]),
@@ -261,8 +270,10 @@ struct RLoader {
 
   __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[4], int tid) const {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<uint4*>(lds + ((tid >> 4) + 16 * i) * RPITCH + (tid & 15) * 8) = reg[i];
+    for (int i = 0; i < 4; ++i) {
+      const int k = (tid >> 4) + 16 * i;
+      *reinterpret_cast<uint4*>(lds + k * RPITCH + rcol(k, (tid & 15) * 8)) = reg[i];
+    }
   }
 };
 
