@@ -329,7 +329,8 @@ def main():
                     help="weight staleness treatment (Section 4.2): SpecTrain prediction (default), Vanilla "
                          "pipelining (latest weights) or weight stashing (backward reuses the forward's weights)")
     ap.add_argument("--median-steps", type=int, default=50,
-                    help="steps of a pass with an event between steps, for the median step time (0: skip)")
+                    help="steps of a pass with an event between steps, for the median step time of a single-stage "
+                         "workload (0: skip)")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="steps of a second per-launch pass in which a 1 GiB read evicts the caches (MALL "
                          "included) before every update, for the update's cold-cache bandwidth (0: skip)")
@@ -377,9 +378,10 @@ def main():
     value = spec.batch / (ms_step / 1e3)
     log(f"[bench] {args.workload}: {ms_step:.3f} ms/step, {value:.0f} samples/s")
 
-    # per-step durations (an event between steps, outside the timed region)
+    # per-step durations (an event between steps, outside the timed region);
+    # single stages only: a pipeline call runs its own fill and drain
     ms_median = None
-    if args.median_steps > 0:
+    if args.median_steps > 0 and not pipeline:
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.median_steps + 1)]
         ev[0].record(stream)
         for i in range(args.median_steps):
