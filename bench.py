@@ -132,6 +132,13 @@ class StageLoop:
         else:
             self.st.forward(m, self.x[r], self.y[m % (self.depth + 1)])
 
+    def graph_period(self):
+        """Steps after which every pointer the steps use repeats: the input
+        ring, the output ring and the stash slots (the stage reuses the slot
+        the backward just freed, so slots repeat every N - k steps)."""
+        import math
+        return math.lcm(self.ring, self.depth + 1, self.depth)
+
     def steps(self, n, before_update=None):
         for _ in range(n):
             m = self.next_b
@@ -187,6 +194,11 @@ class PipeLoop:
             self.dx0 = torch.empty(first.input_shape(), device=dev, dtype=dt)
         self.m0 = 0
         stream.synchronize()
+
+    def graph_period(self):
+        """Any call starts and ends with every stash empty; the input rings
+        repeat every `ring` mini-batches."""
+        return self.ring
 
     def steps(self, n, before_update=None):
         """n mini-batches through the whole pipeline (fill and drain included)."""
@@ -328,6 +340,9 @@ def main():
     ap.add_argument("--policy", default="spectrain", choices=["spectrain", "vanilla", "stash"],
                     help="weight staleness treatment (Section 4.2): SpecTrain prediction (default), Vanilla "
                          "pipelining (latest weights) or weight stashing (backward reuses the forward's weights)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of a HIP graph that captures a period of steps (the period after which "
+                         "every buffer the steps use repeats); --steps is rounded up to a whole number of periods")
     ap.add_argument("--median-steps", type=int, default=50,
                     help="steps of a pass with an event between steps, for the median step time of a single-stage "
                          "workload (0: skip)")
@@ -368,11 +383,29 @@ def main():
     loop.steps(args.warmup)
     torch.cuda.synchronize()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    loop.steps(args.steps)
-    stop.record(stream)
-    torch.cuda.synchronize()
+    if args.graph:
+        period = loop.graph_period()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            loop.steps(period)
+        reps = -(-args.steps // period)
+        args.steps = reps * period
+        with torch.cuda.stream(stream):
+            graph.replay()   # the captured steps themselves, untimed
+        torch.cuda.synchronize()
+        start.record(stream)
+        with torch.cuda.stream(stream):
+            for _ in range(reps):
+                graph.replay()
+        stop.record(stream)
+        torch.cuda.synchronize()
+        log(f"[bench] HIP graph of {period} steps, {reps} replays")
+    else:
+        torch.cuda.synchronize()
+        start.record(stream)
+        loop.steps(args.steps)
+        stop.record(stream)
+        torch.cuda.synchronize()
     ms_total = start.elapsed_time(stop)
     ms_step = ms_total / args.steps
     value = spec.batch / (ms_step / 1e3)
@@ -488,6 +521,7 @@ def main():
         "vs_baseline": None,
         "dtype": spec.dtype,
         "data": "synthetic",
+        "hip_graph": bool(args.graph),
         "config": {"workload": f"{args.workload}: {DESCRIPTIONS[args.workload]}", "policy": args.policy,
                    "batch": spec.batch,
                    "stage_index": None if pipeline else spec.stage_index, "num_stages": spec.num_stages,
