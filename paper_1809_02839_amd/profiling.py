@@ -21,7 +21,7 @@ Command line:
     python -m paper_1809_02839_amd.profiling stats <kernel_stats.csv> <out.md> --title T --command C
     python -m paper_1809_02839_amd.profiling traffic <fetch_dir> <write_dir> <out.md>
         --calib-bytes B --calib-marker neg --title T --command C
-    python -m paper_1809_02839_amd.profiling counters <pmc_dir> <out.md> --title T --command C
+    python -m paper_1809_02839_amd.profiling counters <pmc_dir> [<pmc_dir> ...] <out.md> --title T --command C
 """
 import argparse
 import csv
@@ -123,7 +123,7 @@ def traffic_table(fetch_dir, write_dir, calib_bytes, marker):
 def write_traffic(out_md, rows, f_read, f_write, calib_bytes, title, command):
     with open(out_md, "w") as f:
         f.write(f"# {title}\n\n")
-        f.write("Commands (repo root on the GPU box, one counter per run):\n\n```\n" + command.strip() + "\n```\n\n")
+        f.write("Commands (from the repository root, one counter per run):\n\n```\n" + command.strip() + "\n```\n\n")
         f.write(f"Reference copy: {calib_bytes} bytes read and written; scale FETCH_SIZE x {f_read:.4f}, "
                 f"WRITE_SIZE x {f_write:.4f} (bytes per KiB-count / 1024).\n\n")
         f.write(f"source digest: {source_digest()}\n\n")
@@ -176,13 +176,18 @@ def counter_means(run_dir):
     return {k: (len(ds), {c: v / len(ds) for c, v in sums.items()}) for k, (ds, sums) in acc.items()}
 
 
-def write_counters(run_dir, out_md, title, command, notes=""):
-    table = counter_means(run_dir)
+def write_counters(run_dirs, out_md, title, command, notes=""):
+    """One table over one or more --pmc runs (each run's counters merged per kernel)."""
+    table = {}
+    for run_dir in ([run_dirs] if isinstance(run_dirs, str) else run_dirs):
+        for k, (n, cs) in counter_means(run_dir).items():
+            n0, cs0 = table.get(k, (n, {}))
+            table[k] = (max(n0, n), {**cs0, **cs})
     counters = sorted({c for _, cs in table.values() for c in cs})
     mfma = "SQ_VALU_MFMA_BUSY_CYCLES" in counters and DURATION in counters
     with open(out_md, "w") as f:
         f.write(f"# {title}\n\n")
-        f.write("Command (repo root on the GPU box):\n\n```\n" + command.strip() + "\n```\n\n")
+        f.write("Command (from the repository root):\n\n```\n" + command.strip() + "\n```\n\n")
         if notes:
             f.write(notes.strip() + "\n\n")
         f.write(f"source digest: {source_digest()}\n\n")
@@ -205,7 +210,7 @@ def write_stats(stats_csv, out_md, title, command, notes=""):
     rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
     with open(out_md, "w") as f:
         f.write(f"# {title}\n\n")
-        f.write("Command (repo root on the GPU box):\n\n```\n" + command.strip() + "\n```\n\n")
+        f.write("Command (from the repository root):\n\n```\n" + command.strip() + "\n```\n\n")
         if notes:
             f.write(notes.strip() + "\n\n")
         f.write(f"source digest: {source_digest()}\n\n")
@@ -234,7 +239,7 @@ def main():
     b.add_argument("--title", required=True)
     b.add_argument("--command", required=True)
     c = sub.add_parser("counters")
-    c.add_argument("pmc_dir")
+    c.add_argument("pmc_dir", nargs="+")
     c.add_argument("out_md")
     c.add_argument("--title", required=True)
     c.add_argument("--command", required=True)
