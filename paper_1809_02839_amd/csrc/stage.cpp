@@ -40,6 +40,16 @@ void DeviceBlock::release() {
   base_ = nullptr;
 }
 
+void PinnedInts::allocate(size_t n) {
+  hip_check(hipHostMalloc(reinterpret_cast<void**>(&host_), n * sizeof(int), hipHostMallocMapped), "hipHostMalloc");
+  for (size_t i = 0; i < n; ++i) host_[i] = 0;
+  hip_check(hipHostGetDevicePointer(reinterpret_cast<void**>(&dev_), host_, 0), "hipHostGetDevicePointer");
+}
+
+PinnedInts::~PinnedInts() {
+  if (host_) (void)hipHostFree(host_);
+}
+
 namespace {
 
 constexpr long TENSOR_ALIGN = 64;   // elements: 256 B of float32, 128 B of bf16
@@ -460,24 +470,28 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
   g_ = arena_.at<float>(og);
   what_[0] = arena_.at<void>(of);
   what_[1] = arena_.at<void>(ob);
-  hip_check(hipHostMalloc(reinterpret_cast<void**>(&flag_host_), sizeof(int), hipHostMallocMapped), "hipHostMalloc");
-  *flag_host_ = 0;
-  hip_check(hipHostGetDevicePointer(reinterpret_cast<void**>(&flag_dev_), flag_host_, 0), "hipHostGetDevicePointer");
+  flag_.allocate(1);
   plan_buffers();
   if (d.weight_policy == SPECTRAIN_POLICY_STASH) {
     for (size_t i = 0; i < slots_.size(); ++i) wstash_off_.push_back(wstash_.add(n_arena_ * esz_));
     wstash_.allocate();
   }
 
-  hip_check(fill_f32(v_, 0.0f, n_arena_, s_), "clear v");
-  hip_check(fill_f32(g_, 0.0f, n_arena_, s_), "clear g");
-  set_state(W0, nullptr);
+  try {
+    hip_check(fill_f32(v_, 0.0f, n_arena_, s_), "clear v");
+    hip_check(fill_f32(g_, 0.0f, n_arena_, s_), "clear g");
+    set_state(W0, nullptr);
+  } catch (...) {
+    // the member buffers are freed on the way out: let the work already
+    // enqueued on them finish first
+    (void)hipStreamSynchronize(s_);
+    throw;
+  }
 }
 
 Stage::~Stage() {
   (void)hipStreamSynchronize(s_);
   for (hipEvent_t e : prof_pool_) (void)hipEventDestroy(e);
-  if (flag_host_) (void)hipHostFree(flag_host_);
 }
 
 void Stage::sync() { hip_check(hipStreamSynchronize(s_), "hipStreamSynchronize"); }
@@ -500,7 +514,7 @@ void Stage::set_state(const float* W, const float* v) {
   predict(0, 0);
   predict(0, 1);
   sync();
-  *flag_host_ = 0;
+  *flag_.host() = 0;
   g_pending_ = false;
 }
 
@@ -551,14 +565,14 @@ void Stage::update(int s_f, int s_b) {
   double bytes = static_cast<double>(n_params_) * (12 + 8 + (s_f >= 0) * esz_ + (s_b >= 0) * esz_);
   if (defer_segs_.empty()) {
     LAUNCH("fused_update", 0, bytes,
-           fused_update(W_, v_, g_, what_[0], what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_dev_, s_));
+           fused_update(W_, v_, g_, what_[0], what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_.dev(), s_));
   } else {
     std::sort(defer_segs_.begin(), defer_segs_.end(),
               [](const UpdateSegment& a, const UpdateSegment& b) { return a.off < b.off; });
     for (const UpdateSegment& sg : defer_segs_) bytes += 4.0 * (sg.splits - 1) * sg.n;   // planes instead of g
     LAUNCH("fused_update", 0, bytes,
            fused_update_partials(W_, v_, g_, defer_segs_.data(), static_cast<int>(defer_segs_.size()), what_[0],
-                                 what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_dev_, s_));
+                                 what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_.dev(), s_));
   }
   defer_segs_.clear();
   defer_used_ = 0;

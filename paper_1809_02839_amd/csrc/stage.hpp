@@ -44,6 +44,23 @@ class DeviceBlock {
   size_t total_ = 0;
 };
 
+// Pinned, device-mapped host memory owned until destruction (also when the
+// owning stage's constructor throws after allocating it).
+class PinnedInts {
+ public:
+  PinnedInts() = default;
+  PinnedInts(const PinnedInts&) = delete;
+  PinnedInts& operator=(const PinnedInts&) = delete;
+  void allocate(size_t n);   // zero-filled
+  int* host() const { return host_; }
+  int* dev() const { return dev_; }
+  ~PinnedInts();
+
+ private:
+  int* host_ = nullptr;
+  int* dev_ = nullptr;
+};
+
 struct TensorInfo {
   long off;   // element offset in the padded arenas
   long n;     // element count
@@ -62,7 +79,7 @@ class Stage {
   void get_state(float* W, float* v);
   void set_state(const float* W, const float* v);
   void get_predicted(int slot, float* out);
-  bool nonfinite() const { return *reinterpret_cast<volatile int*>(flag_host_) != 0; }
+  bool nonfinite() const { return *reinterpret_cast<volatile int*>(flag_.host()) != 0; }
   void sync();
   void profile(bool enable);
   int profile_read(spectrain_kernel_stat* out, int capacity);
@@ -150,8 +167,7 @@ class Stage {
   DeviceBlock wstash_;                   // STASH policy: one weight copy per stash slot
   std::vector<size_t> wstash_off_;
   const void* bwd_weights_ = nullptr;    // base of the weights the current backward reads
-  int* flag_host_ = nullptr;   // pinned, mapped: set by the update kernel on a non-finite value
-  int* flag_dev_ = nullptr;
+  PinnedInts flag_;   // set by the update kernel on a non-finite value
 
   std::vector<Slot> slots_;
   std::vector<DeviceBlock> slot_blocks_;

@@ -93,8 +93,19 @@ def _fptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
 
 
-def _dptr(t):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+def _dptr(t, dtype=None, what="tensor"):
+    """Device pointer of a torch tensor. The library reads raw pointers, so a
+    host tensor, a strided view or the wrong element type is refused here
+    rather than reaching a kernel."""
+    if t is None:
+        return None
+    if not getattr(t, "is_cuda", False):
+        raise ValueError(f"{what} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if dtype is not None and str(t.dtype) != dtype:
+        raise ValueError(f"{what} must be {dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
 
 
 def version_difference(k: int, N: int, forward: bool) -> int:
@@ -155,11 +166,19 @@ class Stage:
     def predict(self, s: int, slot: int):
         _check(lib().spectrain_stage_predict(self.h, s, slot))
 
+    @property
+    def _act(self):
+        return "torch.bfloat16" if self.desc.dtype == BF16 else "torch.float32"
+
     def forward(self, mb: int, x, y=None, labels=None, loss=None):
-        _check(lib().spectrain_stage_forward(self.h, mb, _dptr(x), _dptr(y), _dptr(labels), _dptr(loss)))
+        a = self._act
+        _check(lib().spectrain_stage_forward(self.h, mb, _dptr(x, a, "x"), _dptr(y, a, "y"),
+                                             _dptr(labels, "torch.int32", "labels"),
+                                             _dptr(loss, "torch.float32", "loss")))
 
     def backward(self, mb: int, dy=None, dx=None):
-        _check(lib().spectrain_stage_backward(self.h, mb, _dptr(dy), _dptr(dx)))
+        a = self._act
+        _check(lib().spectrain_stage_backward(self.h, mb, _dptr(dy, a, "dy"), _dptr(dx, a, "dx")))
 
     def update(self, s_next_fwd: int, s_next_bwd: int):
         _check(lib().spectrain_stage_update(self.h, s_next_fwd, s_next_bwd))

@@ -128,3 +128,30 @@ def test_driver_pipeline_order_respects_dependencies(N):
                 assert pos[(k + 1, "B", m)] < pos[(k, "B", m)]
             else:
                 assert pos[(k, "F", m)] < pos[(k, "B", m)]
+
+
+def test_binding_refuses_host_strided_and_mistyped_tensors():
+    # the library reads raw device pointers; the binding stops these before any call
+    torch = pytest.importorskip("torch")
+    from paper_1809_02839_amd import native
+
+    class FakeCuda:
+        is_cuda = True
+
+        def __init__(self, dtype, contiguous=True):
+            self.dtype, self._c = dtype, contiguous
+
+        def is_contiguous(self):
+            return self._c
+
+        def data_ptr(self):
+            return 4096
+
+    with pytest.raises(ValueError, match="GPU tensor"):
+        native._dptr(torch.zeros(4), "torch.float32", "x")
+    with pytest.raises(ValueError, match="contiguous"):
+        native._dptr(FakeCuda(torch.float32, contiguous=False), "torch.float32", "x")
+    with pytest.raises(ValueError, match="torch.bfloat16"):
+        native._dptr(FakeCuda(torch.float32), "torch.bfloat16", "x")
+    assert native._dptr(FakeCuda(torch.int32), "torch.int32", "labels").value == 4096
+    assert native._dptr(None, "torch.float32") is None
