@@ -2,6 +2,8 @@
 // column sums (bias and layer-norm gradients), softmax cross-entropy,
 // layer norm, attention softmax forward/backward and the LSTM cell.
 // Every reduction runs in a fixed order, so results are bitwise reproducible.
+#include <algorithm>
+
 #include "kernels.hpp"
 
 namespace spx {
@@ -210,16 +212,22 @@ __global__ __launch_bounds__(256) void colsum_strided_final_kernel(const float* 
 }
 
 // ---------------------------------------------------- cross-entropy ----
-// Long rows (CE_LDS_MIN <= C <= CE_LDS_MAX, C % 4 == 0): the row is read from
-// memory once into LDS (128 KB), and the max, the sum of exponentials and
-// the gradient passes read it there. One 1024-thread block per row and CU.
-constexpr int CE_LDS_MAX = 32768, CE_LDS_MIN = 4096, CE_LDS_NT = 1024;
-__global__ __launch_bounds__(CE_LDS_NT) void softmax_ce_lds_kernel(const float* logits, const int32_t* labels, int R,
-                                                                   int C, bf16_t* dlogits, float* row_loss) {
-  __shared__ float4 row[CE_LDS_MAX / 4];
-  __shared__ float sh[CE_LDS_NT / 64];
-  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const float4* z = reinterpret_cast<const float4*>(logits + static_cast<long>(r) * C);
+constexpr int CE_ROW_MAX = 32768, CE_ROW_MIN = 4096, CE_ROW_NT = 1024;
+
+// Long rows held in registers (CE_ROW_MIN <= C <= CE_ROW_MAX, C % 4 == 0, bf16
+// gradients): one persistent 1024-thread block per CU walks the rows r =
+// blockIdx.x, + gridDim.x, ...; thread t owns the 16-byte chunks c = t + 1024 i
+// (i < 8) of every row, so the row needs no LDS, and its share of the next row
+// is loaded into a second register set while the current row's exponentials,
+// sums and gradients are formed and stored (each row is read from memory
+// once). Exponentials use the hardware exp2-based __expf (relative error near
+// 1e-7, far below the bf16 rounding of the gradient); the target's score is
+// read back from memory.
+constexpr int CE_ROW_CHUNKS = CE_ROW_MAX / 4 / CE_ROW_NT;   // 16-byte chunks per thread
+__global__ __launch_bounds__(CE_ROW_NT) void softmax_ce_rows_kernel(const float* logits, const int32_t* labels, int R,
+                                                                    int C, bf16_t* dlogits, float* row_loss) {
+  __shared__ float sh[CE_ROW_NT / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int C4 = C / 4;
   auto reduce = [&](float v, bool is_max) {
     v = is_max ? wave_max(v) : wave_sum(v);
@@ -228,41 +236,56 @@ __global__ __launch_bounds__(CE_LDS_NT) void softmax_ce_lds_kernel(const float* 
     __syncthreads();
     float t = sh[0];
 #pragma unroll
-    for (int w = 1; w < CE_LDS_NT / 64; ++w) t = is_max ? fmaxf(t, sh[w]) : t + sh[w];
+    for (int w = 1; w < CE_ROW_NT / 64; ++w) t = is_max ? fmaxf(t, sh[w]) : t + sh[w];
     return t;
   };
-  float m = -INFINITY;
-#pragma unroll 4
-  for (int c = tid; c < C4; c += CE_LDS_NT) {
-    const float4 v = z[c];
-    row[c] = v;
-    m = fmaxf(m, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
-  }
-  m = reduce(m, true);   // its barriers also publish the row
-  // the target's score comes from memory: the LDS row is overwritten below
-  const int lab = labels[r];
-  const bool lab_ok = lab >= 0 && lab < C;
-  const float zl = (tid == 0 && lab_ok) ? logits[static_cast<long>(r) * C + lab] : 0.0f;
-  // exp(z - m) with the hardware exponential (relative error near 1e-7, far
-  // below the bf16 rounding of the gradient), kept in LDS for the last pass
-  float s = 0.0f;
-  for (int c = tid; c < C4; c += CE_LDS_NT) {
-    const float4 v = row[c];
-    const float4 e = make_float4(__expf(v.x - m), __expf(v.y - m), __expf(v.z - m), __expf(v.w - m));
-    row[c] = e;
-    s += (e.x + e.y) + (e.z + e.w);
-  }
-  s = reduce(s, false);   // its barriers also publish the exponentials
-  if (tid == 0) row_loss[r] = lab_ok ? (m + logf(s)) - zl : NAN;
-  const float inv_s = 1.0f / s, inv_r = 1.0f / static_cast<float>(R);
-  uint2* out = reinterpret_cast<uint2*>(dlogits + static_cast<long>(r) * C);
-  for (int c = tid; c < C4; c += CE_LDS_NT) {
-    const float4 e = row[c];
-    float p[4] = {e.x * inv_s, e.y * inv_s, e.z * inv_s, e.w * inv_s};
+  auto load = [&](int r, float4 (&v)[CE_ROW_CHUNKS]) {
+    const float4* z = reinterpret_cast<const float4*>(logits + static_cast<long>(r) * C);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) p[q] = ((4 * c + q == lab) ? p[q] - 1.0f : p[q]) * inv_r;
-    out[c] = make_uint2(f32_to_bf16(p[0]) | (static_cast<uint32_t>(f32_to_bf16(p[1])) << 16),
-                        f32_to_bf16(p[2]) | (static_cast<uint32_t>(f32_to_bf16(p[3])) << 16));
+    for (int i = 0; i < CE_ROW_CHUNKS; ++i) {
+      const int c = tid + CE_ROW_NT * i;
+      if (c < C4) v[i] = z[c];
+    }
+  };
+  const float inv_r = 1.0f / static_cast<float>(R);
+  float4 cur[CE_ROW_CHUNKS], nxt[CE_ROW_CHUNKS];
+  int r = blockIdx.x;
+  if (r < R) load(r, nxt);
+  for (; r < R; r += gridDim.x) {
+#pragma unroll
+    for (int i = 0; i < CE_ROW_CHUNKS; ++i) cur[i] = nxt[i];
+    if (r + static_cast<int>(gridDim.x) < R) load(r + gridDim.x, nxt);   // in flight during this row
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < CE_ROW_CHUNKS; ++i)
+      if (tid + CE_ROW_NT * i < C4) m = fmaxf(m, fmaxf(fmaxf(cur[i].x, cur[i].y), fmaxf(cur[i].z, cur[i].w)));
+    m = reduce(m, true);
+    const int lab = labels[r];
+    const bool lab_ok = lab >= 0 && lab < C;
+    const float zl = (tid == 0 && lab_ok) ? logits[static_cast<long>(r) * C + lab] : 0.0f;
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < CE_ROW_CHUNKS; ++i)
+      if (tid + CE_ROW_NT * i < C4) {
+        const float4 v = cur[i];
+        cur[i] = make_float4(__expf(v.x - m), __expf(v.y - m), __expf(v.z - m), __expf(v.w - m));
+        s += (cur[i].x + cur[i].y) + (cur[i].z + cur[i].w);
+      }
+    s = reduce(s, false);
+    if (tid == 0) row_loss[r] = lab_ok ? (m + logf(s)) - zl : NAN;
+    const float inv_s = 1.0f / s;
+    uint2* out = reinterpret_cast<uint2*>(dlogits + static_cast<long>(r) * C);
+#pragma unroll
+    for (int i = 0; i < CE_ROW_CHUNKS; ++i) {
+      const int c = tid + CE_ROW_NT * i;
+      if (c >= C4) continue;
+      const float4 e = cur[i];
+      float p[4] = {e.x * inv_s, e.y * inv_s, e.z * inv_s, e.w * inv_s};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) p[q] = ((4 * c + q == lab) ? p[q] - 1.0f : p[q]) * inv_r;
+      out[c] = make_uint2(f32_to_bf16(p[0]) | (static_cast<uint32_t>(f32_to_bf16(p[1])) << 16),
+                          f32_to_bf16(p[2]) | (static_cast<uint32_t>(f32_to_bf16(p[3])) << 16));
+    }
   }
 }
 
@@ -626,9 +649,12 @@ hipError_t softmax_ce(const float* logits, const int32_t* labels, int R, int C, 
   if (R <= 0) return hipSuccess;
   const bool vec = C % 4 == 0 && (reinterpret_cast<uintptr_t>(logits) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(dlogits) & 7) == 0;
-  if (dtype == 1 && vec && C >= CE_LDS_MIN && C <= CE_LDS_MAX)
-    hipLaunchKernelGGL(softmax_ce_lds_kernel, dim3(R), dim3(CE_LDS_NT), 0, s, logits, labels, R, C,
-                       static_cast<bf16_t*>(dlogits), row_loss_ws);
+  if (dtype == 1 && vec && C >= CE_ROW_MIN && C <= CE_ROW_MAX) {
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    hipLaunchKernelGGL(softmax_ce_rows_kernel, dim3(std::min(R, std::max(cus, 1))), dim3(CE_ROW_NT), 0, s, logits,
+                       labels, R, C, static_cast<bf16_t*>(dlogits), row_loss_ws);
+  }
   else if (dtype == 1 && vec)
     hipLaunchKernelGGL(softmax_ce_bf16x4_kernel, dim3(R), dim3(NT), 0, s, logits, labels, R, C,
                        static_cast<bf16_t*>(dlogits), row_loss_ws);
