@@ -3,6 +3,7 @@
 // layer norm, attention softmax forward/backward and the LSTM cell.
 // Every reduction runs in a fixed order, so results are bitwise reproducible.
 #include <algorithm>
+#include <atomic>
 
 #include "kernels.hpp"
 
@@ -650,8 +651,16 @@ hipError_t softmax_ce(const float* logits, const int32_t* labels, int R, int C, 
   const bool vec = C % 4 == 0 && (reinterpret_cast<uintptr_t>(logits) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(dlogits) & 7) == 0;
   if (dtype == 1 && vec && C >= CE_ROW_MIN && C <= CE_ROW_MAX) {
+    // one persistent block per CU; the count is read once per device
+    static std::atomic<int> cu_count[64];
     int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess) (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
+      cus = cu_count[dev].load(std::memory_order_relaxed);
+      if (cus <= 0) {
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+        cu_count[dev].store(cus, std::memory_order_relaxed);
+      }
+    }
     hipLaunchKernelGGL(softmax_ce_rows_kernel, dim3(std::min(R, std::max(cus, 1))), dim3(CE_ROW_NT), 0, s, logits,
                        labels, R, C, static_cast<bf16_t*>(dlogits), row_loss_ws);
   }
