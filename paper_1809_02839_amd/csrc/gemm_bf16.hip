@@ -98,6 +98,7 @@ struct KArgs {
   long a_bs1, a_bs2, b_bs1, b_bs2, c_bs1, c_bs2;
   float* partial;        // splits > 1: [split][batch][M][N] float32
   int vec_epi;           // output, bias, residual and mask allow the four-column epilogue
+  int bn;                // block tile width in N (host side: selects the kernel)
   EpiDev e;
 };
 
@@ -115,12 +116,13 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, int byte_off) {
 }
 
 // ---- K-mode: 8 consecutive k of one row ----------------------------------
-// Thread t loads vectors v = t + 256 i (i < 4): tile row v / 8, k chunk t % 8.
+// Thread t loads vectors v = t + 256 i (i < ROWS / 32): tile row v / 8, k chunk t % 8.
 // TAPK (convolutions whose channel count is a multiple of BK): every K step
 // lies inside one filter tap, so the tap and its pixel shift are uniform for
 // the whole block and each vector costs one add and a bounds check.
-template <int MODE, bool TAPK>
+template <int MODE, bool TAPK, int ROWS = 128>
 struct KLoader {
+  static constexpr int V = ROWS / 32;   // 16-byte vectors per thread
   int row_ok[4];
   int base[4];       // byte offset of the row (PLAIN) or of the pixel's channel 0 (CONV)
   int ph[4], pw[4];  // CONV: pixel coordinates
@@ -129,7 +131,7 @@ struct KLoader {
   __device__ void init(const OperandDev& o, int row0, int tid, int /*k0*/) {
     kq8 = (tid & 7) * 8;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < V; ++i) {
       const int r = row0 + ((tid + NT * i) >> 3);
       row_ok[i] = r < o.rows;
       const uint32_t rr = row_ok[i] ? r : 0;
@@ -151,7 +153,7 @@ struct KLoader {
     const bool kok = k < o.K;
     if (MODE == OP_K_PLAIN) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) reg[i] = bload(rs, (row_ok[i] & kok) ? base[i] + k * 2 : OOB);
+      for (int i = 0; i < V; ++i) reg[i] = bload(rs, (row_ok[i] & kok) ? base[i] + k * 2 : OOB);
     } else if (TAPK) {
       const int tap = static_cast<int>(o.fdC.div(k0));     // uniform
       const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
@@ -159,7 +161,7 @@ struct KLoader {
       const int dw = (MODE == OP_K_CONV_FWD) ? kw - 1 : 1 - kw;
       const int shift = ((dh * o.W + dw) * o.C + (k0 - tap * o.C) + kq8) * 2;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < V; ++i) {
         const int hh = ph[i] + dh, ww = pw[i] + dw;
         const bool ok = row_ok[i] & (static_cast<unsigned>(hh) < static_cast<unsigned>(o.H)) &
                         (static_cast<unsigned>(ww) < static_cast<unsigned>(o.W));
@@ -174,7 +176,7 @@ struct KLoader {
       const int dw = (MODE == OP_K_CONV_FWD) ? kw - 1 : 1 - kw;
       const int shift = ((dh * o.W + dw) * o.C + c) * 2;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < V; ++i) {
         const int hh = ph[i] + dh, ww = pw[i] + dw;
         const bool ok = row_ok[i] & kok & (static_cast<unsigned>(hh) < static_cast<unsigned>(o.H)) &
                         (static_cast<unsigned>(ww) < static_cast<unsigned>(o.W));
@@ -185,7 +187,7 @@ struct KLoader {
 
   __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[4], int tid) const {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < V; ++i) {
       const int v = tid + NT * i;
       *reinterpret_cast<uint4*>(lds + (v >> 3) * PITCH + (v & 7) * 8) = reg[i];
     }
@@ -195,12 +197,13 @@ struct KLoader {
 // ---- R-mode: 8 consecutive rows of one k ----------------------------------
 // The tile is kept in LDS as [k][row] (rows contiguous, RPITCH elements per k)
 // exactly as loaded, and the MFMA operand reads transpose it (see frag_r).
-// Thread t loads row group t % 16 (rows 8 (t % 16) .. + 7) at
-// k = k0 + t / 16 + 16 i (i < 4): sixteen lanes cover one k row of the tile.
-// Loads must be issued for consecutive K steps (the filter-gradient gather
-// advances its pixel coordinates by BK per call).
-template <int MODE, bool TAPK>
+// With G = ROWS / 8 row groups, thread t loads row group t % G (rows
+// 8 (t % G) .. + 7) at k = k0 + t / G + (256 / G) i (i < ROWS / 32): G lanes
+// cover one k row of the tile. Loads must be issued for consecutive K steps
+// (the filter-gradient gather advances its pixel coordinates by BK per call).
+template <int MODE, bool TAPK, int ROWS = 128>
 struct RLoader {
+  static constexpr int G = ROWS / 8, V = ROWS / 32, KS = NT / G;
   int rows_ok;
   int colb;      // byte offset of the row group (PLAIN, FILTER_T) or of its channel + tap shift (WGRAD)
   int tkh, tkw;  // WGRAD: filter tap of the row group
@@ -208,8 +211,8 @@ struct RLoader {
   int h[4], w[4];
 
   __device__ void init(const OperandDev& o, int row0, int tid, int k0) {
-    kk0 = tid >> 4;
-    const int r = row0 + (tid & 15) * 8;
+    kk0 = tid / G;
+    const int r = row0 + (tid % G) * 8;
     rows_ok = r < o.rows;  // rows are a multiple of 8
     const uint32_t rr = rows_ok ? r : 0;
     tkh = tkw = 0;
@@ -219,8 +222,8 @@ struct RLoader {
       tkw = tap - 3 * tkh;
       colb = (((tkh - 1) * o.W + (tkw - 1)) * o.C + static_cast<int>(rr) - tap * o.C) * 2;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t kk = k0 + kk0 + 16 * i;
+      for (int i = 0; i < V; ++i) {
+        const uint32_t kk = k0 + kk0 + KS * i;
         const uint32_t b = o.fdHW.div(kk);
         const uint32_t rem = kk - b * static_cast<uint32_t>(o.H * o.W);
         h[i] = o.fdW.div(rem);
@@ -238,8 +241,8 @@ struct RLoader {
       c0 = k0 - t0 * o.C2;
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int k = k0 + kk0 + 16 * i;
+    for (int i = 0; i < V; ++i) {
+      const int k = k0 + kk0 + KS * i;
       const bool kok = rows_ok & (k < o.K);
       if (MODE == OP_R_PLAIN) {
         reg[i] = bload(rs, kok ? static_cast<int>(k * o.ld * 2) + colb : OOB);
@@ -258,7 +261,7 @@ struct RLoader {
         int t, c2;
         if (TAPK) {
           t = t0;
-          c2 = c0 + kk0 + 16 * i;
+          c2 = c0 + kk0 + KS * i;
         } else {
           t = static_cast<int>(o.fdC2.div(k < o.K ? k : 0));
           c2 = k - t * o.C2;
@@ -270,17 +273,17 @@ struct RLoader {
 
   __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[4], int tid) const {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int k = (tid >> 4) + 16 * i;
-      *reinterpret_cast<uint4*>(lds + k * RPITCH + rcol(k, (tid & 15) * 8)) = reg[i];
+    for (int i = 0; i < V; ++i) {
+      const int k = tid / G + KS * i;
+      *reinterpret_cast<uint4*>(lds + k * RPITCH + rcol(k, (tid % G) * 8)) = reg[i];
     }
   }
 };
 
-template <int MODE, bool TAPK>
+template <int MODE, bool TAPK, int ROWS = 128>
 struct LoaderFor {
-  using type =
-      typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE, TAPK>, RLoader<MODE, TAPK>>::type;
+  using type = typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE, TAPK, ROWS>,
+                                         RLoader<MODE, TAPK, ROWS>>::type;
 };
 
 // value = acc * alpha + bias + residuals, ReLU, then float32 and/or bf16 stores
@@ -360,7 +363,8 @@ __device__ __forceinline__ void epilogue4(const EpiDev& e, long idx, int col, fl
 
 // Stores a block's 128 x 128 accumulator tile: float32 partials of its K
 // split, or the epilogue into the outputs.
-__device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2][2], int row0, int col0, int wm,
+template <int NJ>
+__device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2][NJ], int row0, int col0, int wm,
                                            int wn, int lane, int split, int z, int z1, int z2) {
   // With B as the first MFMA operand, lane l holds row (l % 32) and columns
   // 8 (r / 4) + 4 (l / 32) + r % 4 of each 32 x 32 tile: four consecutive
@@ -371,12 +375,12 @@ __device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2]
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < NJ; ++j) {
         const int row = row0 + wm * 64 + i * 32 + (lane & 31);
         if (row >= args.M) continue;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int col = col0 + wn * 64 + j * 32 + 8 * g + 4 * (lane >> 5);
+          const int col = col0 + wn * (32 * NJ) + j * 32 + 8 * g + 4 * (lane >> 5);
           float* o = part + static_cast<long>(row) * args.N + col;
           if (vec && col + 3 < args.N) {
             *reinterpret_cast<float4*>(o) =
@@ -394,12 +398,12 @@ __device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2]
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < NJ; ++j) {
       const int row = row0 + wm * 64 + i * 32 + (lane & 31);
       if (row >= args.M) continue;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int col = col0 + wn * 64 + j * 32 + 8 * g + 4 * (lane >> 5);
+        const int col = col0 + wn * (32 * NJ) + j * 32 + 8 * g + 4 * (lane >> 5);
         const long idx = coff + static_cast<long>(row) * args.e.ldc + col;
         const float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
         if (args.vec_epi && col + 3 < args.N) {
@@ -414,8 +418,11 @@ __device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2]
     }
 }
 
-template <int MA, int MB, bool TAPK>
+// BNT: block tile width in N (128, or 64 for launches whose 128-wide tiles
+// cannot give every CU two blocks); each wave owns 64 x (BNT / 2).
+template <int MA, int MB, bool TAPK, int BNT>
 __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
+  constexpr int NJ = BNT / 64;   // 32-column MFMA tiles per wave
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TILE_ELEMS];  // [buffer][A|B]
 
   const int tid = threadIdx.x;
@@ -425,7 +432,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
   int tile = bid;
   if ((args.tiles_total & 7) == 0) tile = (bid & 7) * (args.tiles_total >> 3) + (bid >> 3);
   const int tm = tile / args.tiles_n, tn = tile - tm * args.tiles_n;
-  const int row0 = tm * BM, col0 = tn * BN;
+  const int row0 = tm * BM, col0 = tn * BNT;
 
   const int zs = blockIdx.y;
   const int z = zs / args.splits, split = zs - z * args.splits;
@@ -442,18 +449,18 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
   typename LoaderFor<MA, TAPK>::type la;
-  typename LoaderFor<MB, TAPK>::type lb;
+  typename LoaderFor<MB, TAPK, BNT>::type lb;
   la.init(A, row0, tid, kbeg);
   lb.init(B, col0, tid, kbeg);
 
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[2][NJ];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
@@ -463,20 +470,20 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
     if constexpr (MA == OP_K_CONV_DGRAD) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 16) {
-      bf16x8_t fa[2], fb[2];
+      bf16x8_t fa[2], fb[NJ];
       const int kl = kk + (lane >> 5) * 8;
 #pragma unroll
       for (int i = 0; i < 2; ++i)
         fa[i] = (MA <= OP_K_CONV_DGRAD) ? frag_k(sa, wm * 64 + i * 32 + (lane & 31), kl)
                                         : frag_r(sa, wm * 64 + i * 32, kk, lane);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        fb[j] = (MB <= OP_K_CONV_DGRAD) ? frag_k(sb, wn * 64 + j * 32 + (lane & 31), kl)
-                                        : frag_r(sb, wn * 64 + j * 32, kk, lane);
+      for (int j = 0; j < NJ; ++j)
+        fb[j] = (MB <= OP_K_CONV_DGRAD) ? frag_k(sb, wn * (32 * NJ) + j * 32 + (lane & 31), kl)
+                                        : frag_r(sb, wn * (32 * NJ) + j * 32, kk, lane);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < NJ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
     __builtin_amdgcn_iglp_opt(0);
@@ -518,7 +525,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
     if (kt < nk) compute(lds[0][0], lds[0][1]);   // odd step count: the last step is in buffer 0
   }
 
-  write_tile(args, acc, row0, col0, wm, wn, lane, split, z, z1, z2);
+  write_tile<NJ>(args, acc, row0, col0, wm, wn, lane, split, z, z1, z2);
 }
 
 // Sum the split partials in split order and apply the epilogue. Four
@@ -623,7 +630,8 @@ OperandDev make_operand(const Operand& o, int rows, int K, long extent) {
 template <int MA, int MB, bool TAPK = false>
 hipError_t launch(const KArgs& a, hipStream_t s) {
   dim3 grid(a.tiles_total, a.batch * a.splits);
-  hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK>), grid, dim3(NT), 0, s, a);
+  if (a.bn == 64) hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 64>), grid, dim3(NT), 0, s, a);
+  else hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128>), grid, dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
@@ -639,8 +647,19 @@ namespace {
 // long: as many splits as keep all blocks resident at once, each with at
 // least 12 K steps (shorter slices cost more in the reduction than they gain),
 // and no more than the workspace holds.
+constexpr long kTargetBlocks = 2 * 256;
+
+// Block tile width in N: 64 when 128-wide tiles cannot give every CU two
+// blocks but 64-wide ones fill at least three quarters of the two-per-CU
+// slots, so the launch needs no K split; 128 otherwise.
+int tile_width(int M, int N, int batch) {
+  const long rows = static_cast<long>((M + BM - 1) / BM) * batch;
+  const long t128 = rows * ((N + 127) / 128), t64 = rows * ((N + 63) / 64);
+  return (t128 < kTargetBlocks && 4 * t64 >= 3 * kTargetBlocks) ? 64 : 128;
+}
+
 int split_rule(int M, int N, int K, int batch, size_t workspace_bytes) {
-  constexpr long kTargetBlocks = 2 * 256;
+  if (tile_width(M, N, batch) == 64) return 1;
   const long tiles = static_cast<long>((N + BN - 1) / BN) * ((M + BM - 1) / BM) * batch;
   if (tiles >= kTargetBlocks || K < 2 * 12 * BK) return 1;
   int splits = static_cast<int>(kTargetBlocks / tiles);   // all blocks resident in one round
@@ -667,7 +686,8 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   a.K = d.K;
   a.batch = d.batch;
   a.zdiv = zdiv;
-  a.tiles_n = (d.N + BN - 1) / BN;
+  a.bn = tile_width(d.M, d.N, d.batch);
+  a.tiles_n = (d.N + a.bn - 1) / a.bn;
   a.tiles_total = a.tiles_n * ((d.M + BM - 1) / BM);
   const int splits = d.workspace ? split_rule(d.M, d.N, d.K, d.batch, d.workspace_bytes) : 1;
   const int ksteps = (d.K + BK - 1) / BK;
