@@ -3,8 +3,9 @@
 // layers, 3x3 convolutions as implicit GEMM (forward, data gradient, filter
 // gradient) and the batched products inside attention.
 //
-// Block tile 128 x 128, K step 64, 256 threads = 4 waves in a 2 x 2 grid, each
-// wave owning a 64 x 64 sub-tile (2 x 2 MFMA tiles of 32 x 32). K-mode operand
+// Block tile 128 x 128 (or 128 x 64, see tile_width), K step 64, 256 threads =
+// 4 waves in a 2 x 2 grid, each wave owning a 64 x 64 (64 x 32) sub-tile of
+// 2 x 2 (2 x 1) MFMA tiles of 32 x 32. K-mode operand
 // tiles are staged in LDS as [row][k] (8 consecutive k per lane make one
 // 16-byte MFMA operand read; the 144-byte row pitch puts eight consecutive
 // rows on disjoint banks); R-mode tiles (rows contiguous in memory) are staged
@@ -14,9 +15,10 @@
 // buffer loads whose resource spans exactly the operand tensor: an offset
 // outside it (zero padding of convolutions, ragged tile edges) reads zero.
 //
-// Split-K: a launch may divide K into `splits` ranges; each writes float32
-// partial tiles to a workspace and an elementwise pass sums the partials in a
-// fixed order and applies the epilogue, so results do not depend on timing.
+// Split-K: a 128 x 128 launch may divide K into `splits` ranges; each writes
+// float32 partial tiles to a workspace and an elementwise pass sums the
+// partials in a fixed order and applies the epilogue, so results do not
+// depend on timing.
 #include <algorithm>
 
 #include "kernels.hpp"
