@@ -70,16 +70,19 @@ FAMILY_KERNEL = {
 
 
 def traffic_per_launch(workload, family):
-    """HBM bytes per launch of the family's kernel from the committed counter
-    summary of this workload, or None when there is none or the kernel
-    sources changed since the counters were taken."""
+    """HBM bytes per launch of the family's kernels (the dispatch-weighted mean
+    when the family launches several instantiations, such as both tile
+    widths) from the committed counter summary of this workload, or None when
+    there is none or the kernel sources changed since the counters were taken."""
     from paper_1809_02839_amd import profiling
-    digest, table = profiling.read_traffic(os.path.join(ROOT, "profiles", f"stage_kernels_{workload}_hbm_traffic.md"))
+    digest, table = profiling.read_traffic(os.path.join(ROOT, "profiles", f"stage_kernels_{workload}_hbm_traffic.md"),
+                                           with_dispatches=True)
     prefix = FAMILY_KERNEL.get(family)
     if digest is None or prefix is None or digest != profiling.source_digest():
         return None
     hits = [v for k, v in table.items() if k.startswith(prefix)]
-    return round(hits[0]) if len(hits) == 1 else None
+    n = sum(d for d, _ in hits)
+    return round(sum(d * b for d, b in hits) / n) if n else None
 
 
 def log(*a):

@@ -134,8 +134,9 @@ def write_traffic(out_md, rows, f_read, f_write, calib_bytes, title, command):
                     f"{r['bytes']:.0f} |\n")
 
 
-def read_traffic(md_path):
-    """(digest, {kernel: bytes per dispatch}) from a traffic summary, or (None, {})."""
+def read_traffic(md_path, with_dispatches=False):
+    """(digest, {kernel: bytes per dispatch}) from a traffic summary, or (None, {});
+    with_dispatches: the values are (dispatches, bytes per dispatch)."""
     if not os.path.exists(md_path):
         return None, {}
     digest, table = None, {}
@@ -146,7 +147,7 @@ def read_traffic(md_path):
             elif line.startswith("| ") and not line.startswith("| kernel"):
                 cells = [c.strip() for c in line.strip().strip("|").split("|")]
                 if len(cells) == 5:
-                    table[cells[0]] = float(cells[4])
+                    table[cells[0]] = (int(cells[1]), float(cells[4])) if with_dispatches else float(cells[4])
     return digest, table
 
 

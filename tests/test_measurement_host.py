@@ -100,3 +100,13 @@ def test_bench_refuses_more_than_one_gpu():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_traffic_of_a_family_with_two_instantiations_is_dispatch_weighted(monkeypatch):
+    import bench
+    table = {"gemm_bf16_kernel<2, 5, true, 64>": (3, 60.0), "gemm_bf16_kernel<2, 5, true, 128>": (1, 100.0),
+             "gemm_bf16_kernel<3, 4, false, 128>": (4, 7.0)}
+    monkeypatch.setattr(profiling, "read_traffic", lambda path, with_dispatches=False: ("d" * 16, table))
+    monkeypatch.setattr(profiling, "source_digest", lambda: "d" * 16)
+    assert bench.traffic_per_launch("vgg_conv", "conv3x3_dgrad") == 70   # (3 * 60 + 100) / 4
+    assert bench.traffic_per_launch("vgg_conv", "conv3x3_wgrad") == 7
