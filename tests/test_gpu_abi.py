@@ -116,3 +116,16 @@ def test_batch_one_stage_stepwise(kind):
     print(f"[stepwise] {wl.name}", flush=True)
     worst = run_stepwise(wl, wl.steps, torch, derived=True)
     print(f"[stepwise] {wl.name}: {worst.report()}", flush=True)
+
+
+def test_narrow_tile_ragged_edges_stepwise():
+    # 12283 x 200 outputs: the 128 x 128 tiles (97 x 2) cannot give every CU two
+    # blocks but 128 x 64 tiles (97 x 4) can, so the forward GEMMs and the
+    # second layer's data gradient run on 128 x 64 tiles with no K split, with
+    # a ragged last row tile (12283 = 95 * 128 + 123) and a ragged last column
+    # tile (200 = 3 * 64 + 8), on both a row-major and a transposed B operand
+    spec = synth.StageSpec("fc", "bf16", "none", 1, 3, 12283, 2, (64, 200, 200), 0.01, 0.9)
+    wl = synth.Workload("fc_narrow_ragged", (spec,), 4)
+    print(f"[stepwise] {wl.name}", flush=True)
+    worst = run_stepwise(wl, wl.steps, torch, derived=True)
+    print(f"[stepwise] {wl.name}: {worst.report()}", flush=True)
