@@ -60,12 +60,30 @@ __device__ __forceinline__ f32x16_t mfma(bf16x8_t b, bf16x8_t a, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a, c, 0, 0, 0);
 }
 
-// Copy a 128 x 64 bf16 block (rows `ld` apart in global memory) into LDS [128][PD].
-__device__ __forceinline__ void stage_rows(bf16_t* dst, const bf16_t* src, long ld, int tid) {
-  for (int e = tid; e < S * (DH / 8); e += NT) {
-    const int r = e >> 3, c = (e & 7) * 8;
-    *reinterpret_cast<uint4*>(dst + r * PD + c) = *reinterpret_cast<const uint4*>(src + r * ld + c);
-  }
+// A thread's four 16-byte vectors of a 128 x 64 bf16 block (rows ld apart in
+// global memory) and their copy into an LDS tile [128][PD]. Loading several
+// blocks before storing any makes their copies cost one round trip to
+// memory rather than one per vector.
+struct Rows4 {
+  uint4 v0, v1, v2, v3;
+};
+static_assert(S * (DH / 8) == 4 * NT, "four 16-byte vectors per thread");
+
+__device__ __forceinline__ uint4 row_vec(const bf16_t* src, long ld, int e) {
+  return *reinterpret_cast<const uint4*>(src + (e >> 3) * ld + (e & 7) * 8);
+}
+
+__device__ __forceinline__ Rows4 stage_load(const bf16_t* src, long ld, int tid) {
+  return Rows4{row_vec(src, ld, tid), row_vec(src, ld, tid + NT), row_vec(src, ld, tid + 2 * NT),
+               row_vec(src, ld, tid + 3 * NT)};
+}
+
+__device__ __forceinline__ void stage_store(bf16_t* dst, const Rows4& r, int tid) {
+  auto at = [&](int e) { return reinterpret_cast<uint4*>(dst + (e >> 3) * PD + (e & 7) * 8); };
+  *at(tid) = r.v0;
+  *at(tid + NT) = r.v1;
+  *at(tid + 2 * NT) = r.v2;
+  *at(tid + 3 * NT) = r.v3;
 }
 
 // Scores of the wave's 32 query rows against all 128 keys: acc[j] holds keys
@@ -113,7 +131,7 @@ __global__ __launch_bounds__(NT) void attention_fwd_kernel(const bf16_t* qkv, in
   const long ld = 3L * d;
   const bf16_t* Qg = qkv + static_cast<long>(b) * S * ld + h * DH;
   const bf16_t* Kg = Qg + d;
-  stage_rows(Vs, Qg + 2 * d, ld, tid);
+  stage_store(Vs, stage_load(Qg + 2 * d, ld, tid), tid);
 
   f32x16_t acc[4];
   scores(Qg, Kg, ld, wave, lane, acc);
@@ -185,9 +203,12 @@ __global__ __launch_bounds__(NT) void attention_bwd_kernel(const bf16_t* qkv, co
   const bf16_t* Vg = Qg + 2 * d;
   const bf16_t* dOg = dctx + static_cast<long>(b) * S * d + h * DH;
   bf16_t* dQg = dqkv + static_cast<long>(b) * S * ld + h * DH;
-  stage_rows(dOs, dOg, d, tid);
-  stage_rows(Qs, Qg, ld, tid);
-  stage_rows(Ks, Kg, ld, tid);
+  {
+    const Rows4 o = stage_load(dOg, d, tid), q = stage_load(Qg, ld, tid), k = stage_load(Kg, ld, tid);
+    stage_store(dOs, o, tid);
+    stage_store(Qs, q, tid);
+    stage_store(Ks, k, tid);
+  }
 
   // P recomputed exactly as in the forward pass
   f32x16_t p[4];
