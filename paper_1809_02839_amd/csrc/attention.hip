@@ -189,12 +189,13 @@ __global__ __launch_bounds__(NT) void attention_fwd_kernel(const bf16_t* qkv, in
   store_rows(ctx + static_cast<long>(b) * S * d + h * DH, d, 32 * wave, o, 1.0f, lane);
 }
 
-__global__ __launch_bounds__(NT) void attention_bwd_kernel(const bf16_t* qkv, const bf16_t* dctx, const float* stats,
+// LDS: bf16(P) (later dS), dO (later Q) and K, 72 KB, so two blocks share a CU.
+__global__ __launch_bounds__(NT, 2) void attention_bwd_kernel(const bf16_t* qkv, const bf16_t* dctx, const float* stats,
                                                            int heads, int d, float scale, bf16_t* dqkv) {
   __shared__ __attribute__((aligned(16))) bf16_t Ps[S * PP];    // bf16(P), later dS
-  __shared__ __attribute__((aligned(16))) bf16_t dOs[S * PD];
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[S * PD];
+  __shared__ __attribute__((aligned(16))) bf16_t dOs[S * PD];   // dO, then Q once dV is formed
   __shared__ __attribute__((aligned(16))) bf16_t Ks[S * PD];
+  bf16_t* const Qs = dOs;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x / heads, h = blockIdx.x - b * heads;
   const long ld = 3L * d;
@@ -204,9 +205,8 @@ __global__ __launch_bounds__(NT) void attention_bwd_kernel(const bf16_t* qkv, co
   const bf16_t* dOg = dctx + static_cast<long>(b) * S * d + h * DH;
   bf16_t* dQg = dqkv + static_cast<long>(b) * S * ld + h * DH;
   {
-    const Rows4 o = stage_load(dOg, d, tid), q = stage_load(Qg, ld, tid), k = stage_load(Kg, ld, tid);
+    const Rows4 o = stage_load(dOg, d, tid), k = stage_load(Kg, ld, tid);
     stage_store(dOs, o, tid);
-    stage_store(Qs, q, tid);
     stage_store(Ks, k, tid);
   }
 
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(NT) void attention_bwd_kernel(const bf16_t* qkv, co
       *reinterpret_cast<uint2*>(Ps + row * PP + col_of(j, 4 * g, lane)) =
           make_uint2(hb[0] | (hb[1] << 16), hb[2] | (hb[3] << 16));
     }
-  __syncthreads();   // dO, Q, K and bf16(P) staged
+  __syncthreads();   // dO, K and bf16(P) staged
 
   // dP = dO V^T for the wave's rows (V rows from global memory), then
   // dS = P * (dP - rowsum(P * dP)) kept in registers until P is consumed
@@ -269,7 +269,9 @@ __global__ __launch_bounds__(NT) void attention_bwd_kernel(const bf16_t* qkv, co
     for (int jn = 0; jn < 2; ++jn) o[jn] = mfma(frag_cols<PD>(dOs, 32 * jn, kk, lane), fa, o[jn]);
   }
   store_rows(dQg + 2 * d, ld, 32 * wave, o, 1.0f, lane);
-  __syncthreads();   // every wave has read bf16(P)
+  const Rows4 q = stage_load(Qg, ld, tid);
+  __syncthreads();   // every wave has read bf16(P) and dO
+  stage_store(Qs, q, tid);
 
 #pragma unroll
   for (int j = 0; j < 4; ++j)
@@ -281,7 +283,7 @@ __global__ __launch_bounds__(NT) void attention_bwd_kernel(const bf16_t* qkv, co
       *reinterpret_cast<uint2*>(Ps + row * PP + col_of(j, 4 * g, lane)) =
           make_uint2(hb[0] | (hb[1] << 16), hb[2] | (hb[3] << 16));
     }
-  __syncthreads();   // dS staged
+  __syncthreads();   // dS and Q staged
 
   // dQ rows (queries 32 w ..) = dS K * scale
 #pragma unroll
