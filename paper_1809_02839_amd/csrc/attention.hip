@@ -103,6 +103,23 @@ __device__ __forceinline__ void scores(const bf16_t* Qg, const bf16_t* Kg, long 
   }
 }
 
+// The same scores with K read from its staged LDS tile [128][PD] (the same
+// bf16 values, so the same products).
+__device__ __forceinline__ void scores_lds_k(const bf16_t* Qg, long ld, const bf16_t* Ks, int wave, int lane,
+                                             f32x16_t (&acc)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.0f;
+  const int kq = 8 * (lane >> 5);
+#pragma unroll
+  for (int kk = 0; kk < DH; kk += 16) {
+    const bf16x8_t fq = gld8(Qg + (32 * wave + (lane & 31)) * ld + kk + kq);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = mfma(frag_rows<PD>(Ks, 32 * j + (lane & 31), kk + kq), fq, acc[j]);
+  }
+}
+
 // Column of register r of tile j for lane l: 32 j + 8 (r / 4) + 4 (l / 32) + r % 4.
 __device__ __forceinline__ int col_of(int j, int r, int lane) { return 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
@@ -209,10 +226,11 @@ __global__ __launch_bounds__(NT, 2) void attention_bwd_kernel(const bf16_t* qkv,
     stage_store(dOs, o, tid);
     stage_store(Ks, k, tid);
   }
+  __syncthreads();   // K staged: the scores read it from LDS
 
   // P recomputed exactly as in the forward pass
   f32x16_t p[4];
-  scores(Qg, Kg, ld, wave, lane, p);
+  scores_lds_k(Qg, ld, Ks, wave, lane, p);
   const int row = 32 * wave + (lane & 31);
   const float* st = stats + (static_cast<long>(blockIdx.x) * S + row) * 2;
   const float m = st[0], inv = st[1];
