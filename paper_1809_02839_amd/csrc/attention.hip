@@ -14,10 +14,11 @@
 // Products use v_mfma_f32_32x32x16_bf16 with the B fragment first, so a lane
 // holds one row and groups of four consecutive columns of each 32 x 32 tile:
 // a row's 128 scores live in lanes l and l ^ 32, and row reductions need one
-// cross-lane exchange. Operands read as rows of 8 consecutive k (Q and K rows
-// for scores, V rows for dP) come straight from global memory; operands
-// needed transposed (V for P V, P and dS for dV and dK, dO, K, Q) are staged
-// in LDS as stored and read with ds_read_b64_tr_b16.
+// cross-lane exchange. Q rows (scores) and V rows (dP) come straight from
+// global memory as rows of 8 consecutive k; K is staged in LDS once per block
+// and read from there by all four waves; operands needed transposed (V for
+// P V, P and dS for dV and dK, dO, K, Q) are staged in LDS as stored and read
+// with ds_read_b64_tr_b16.
 #include "kernels.hpp"
 
 namespace spx {
@@ -87,24 +88,8 @@ __device__ __forceinline__ void stage_store(bf16_t* dst, const Rows4& r, int tid
 }
 
 // Scores of the wave's 32 query rows against all 128 keys: acc[j] holds keys
-// 32 j .. 32 j + 31. Q and K rows come from global memory (row stride ld).
-__device__ __forceinline__ void scores(const bf16_t* Qg, const bf16_t* Kg, long ld, int wave, int lane,
-                                       f32x16_t (&acc)[4]) {
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[j][r] = 0.0f;
-  const int kq = 8 * (lane >> 5);
-#pragma unroll
-  for (int kk = 0; kk < DH; kk += 16) {
-    const bf16x8_t fq = gld8(Qg + (32 * wave + (lane & 31)) * ld + kk + kq);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = mfma(gld8(Kg + (32 * j + (lane & 31)) * ld + kk + kq), fq, acc[j]);
-  }
-}
-
-// The same scores with K read from its staged LDS tile [128][PD] (the same
-// bf16 values, so the same products).
+// 32 j .. 32 j + 31. Q rows come from global memory (row stride ld), K from
+// its staged LDS tile [128][PD].
 __device__ __forceinline__ void scores_lds_k(const bf16_t* Qg, long ld, const bf16_t* Ks, int wave, int lane,
                                              f32x16_t (&acc)[4]) {
 #pragma unroll
@@ -143,15 +128,21 @@ __global__ __launch_bounds__(NT) void attention_fwd_kernel(const bf16_t* qkv, in
                                                            float* stats, bf16_t* ctx) {
   __shared__ __attribute__((aligned(16))) bf16_t Ps[S * PP];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[S * PD];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[S * PD];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x / heads, h = blockIdx.x - b * heads;
   const long ld = 3L * d;
   const bf16_t* Qg = qkv + static_cast<long>(b) * S * ld + h * DH;
   const bf16_t* Kg = Qg + d;
-  stage_store(Vs, stage_load(Qg + 2 * d, ld, tid), tid);
+  {
+    const Rows4 v = stage_load(Qg + 2 * d, ld, tid), k = stage_load(Kg, ld, tid);
+    stage_store(Vs, v, tid);
+    stage_store(Ks, k, tid);
+  }
+  __syncthreads();   // K staged: the scores read it from LDS
 
   f32x16_t acc[4];
-  scores(Qg, Kg, ld, wave, lane, acc);
+  scores_lds_k(Qg, ld, Ks, wave, lane, acc);
   // row softmax: the row's scores are in this lane and lane ^ 32
   // (every operation of P's recomputation is written the same way in the
   // backward pass, with no multiply-add contraction, so both give equal bits)
