@@ -3,9 +3,10 @@
 // layers, 3x3 convolutions as implicit GEMM (forward, data gradient, filter
 // gradient) and the batched products inside attention.
 //
-// Block tile 128 x 128 (or 128 x 64, see tile_width), K step 64, 256 threads =
+// Block tile 128 x 128 (or 128 x 64, see shape_of), K step 64, 256 threads =
 // 4 waves in a 2 x 2 grid, each wave owning a 64 x 64 (64 x 32) sub-tile of
-// 2 x 2 (2 x 1) MFMA tiles of 32 x 32. K-mode operand
+// 2 x 2 (2 x 1) MFMA tiles of 32 x 32; some convolution forwards use 512
+// threads, two waves per sub-tile that share each K step. K-mode operand
 // tiles are staged in LDS as [row][k] (8 consecutive k per lane make one
 // 16-byte MFMA operand read; the 144-byte row pitch puts eight consecutive
 // rows on disjoint banks); R-mode tiles (rows contiguous in memory) are staged
@@ -101,6 +102,7 @@ struct KArgs {
   float* partial;        // splits > 1: [split][batch][M][N] float32
   int vec_epi;           // output, bias, residual and mask allow the four-column epilogue
   int bn;                // block tile width in N (host side: selects the kernel)
+  int ksl;               // waves per output sub-tile (host side: selects the kernel)
   EpiDev e;
 };
 
@@ -118,13 +120,14 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, int byte_off) {
 }
 
 // ---- K-mode: 8 consecutive k of one row ----------------------------------
-// Thread t loads vectors v = t + 256 i (i < ROWS / 32): tile row v / 8, k chunk t % 8.
+// Thread t of NTH loads vectors v = t + NTH i (i < 8 ROWS / NTH): tile row
+// v / 8, k chunk t % 8.
 // TAPK (convolutions whose channel count is a multiple of BK): every K step
 // lies inside one filter tap, so the tap and its pixel shift are uniform for
 // the whole block and each vector costs one add and a bounds check.
-template <int MODE, bool TAPK, int ROWS = 128>
+template <int MODE, bool TAPK, int ROWS, int NTH>
 struct KLoader {
-  static constexpr int V = ROWS / 32;   // 16-byte vectors per thread
+  static constexpr int V = 8 * ROWS / NTH;   // 16-byte vectors per thread
   int row_ok[4];
   int base[4];       // byte offset of the row (PLAIN) or of the pixel's channel 0 (CONV)
   int ph[4], pw[4];  // CONV: pixel coordinates
@@ -134,7 +137,7 @@ struct KLoader {
     kq8 = (tid & 7) * 8;
 #pragma unroll
     for (int i = 0; i < V; ++i) {
-      const int r = row0 + ((tid + NT * i) >> 3);
+      const int r = row0 + ((tid + NTH * i) >> 3);
       row_ok[i] = r < o.rows;
       const uint32_t rr = row_ok[i] ? r : 0;
       if (MODE == OP_K_PLAIN) {
@@ -190,7 +193,7 @@ struct KLoader {
   __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[4], int tid) const {
 #pragma unroll
     for (int i = 0; i < V; ++i) {
-      const int v = tid + NT * i;
+      const int v = tid + NTH * i;
       *reinterpret_cast<uint4*>(lds + (v >> 3) * PITCH + (v & 7) * 8) = reg[i];
     }
   }
@@ -199,17 +202,17 @@ struct KLoader {
 // ---- R-mode: 8 consecutive rows of one k ----------------------------------
 // The tile is kept in LDS as [k][row] (rows contiguous, RPITCH elements per k)
 // exactly as loaded, and the MFMA operand reads transpose it (see frag_r).
-// With G = ROWS / 8 row groups, thread t loads row group t % G (rows
-// 8 (t % G) .. + 7) at k = k0 + t / G + (256 / G) i (i < ROWS / 32): G lanes
+// With G = ROWS / 8 row groups, thread t of NTH loads row group t % G (rows
+// 8 (t % G) .. + 7) at k = k0 + t / G + (NTH / G) i (i < BK G / NTH): G lanes
 // cover one k row of the tile. Loads must be issued for consecutive K steps
 // (the filter-gradient gather advances its pixel coordinates by BK per call).
-template <int MODE, bool TAPK, int ROWS = 128>
+template <int MODE, bool TAPK, int ROWS, int NTH>
 struct RLoader {
-  static constexpr int G = ROWS / 8, V = ROWS / 32, KS = NT / G;
+  static constexpr int G = ROWS / 8, KS = NTH / G, V = BK / KS;
   int rows_ok;
   int colb;      // byte offset of the row group (PLAIN, FILTER_T) or of its channel + tap shift (WGRAD)
   int tkh, tkw;  // WGRAD: filter tap of the row group
-  int kk0;       // t / 16
+  int kk0;       // t / G
   int h[4], w[4];
 
   __device__ void init(const OperandDev& o, int row0, int tid, int k0) {
@@ -282,10 +285,10 @@ struct RLoader {
   }
 };
 
-template <int MODE, bool TAPK, int ROWS = 128>
+template <int MODE, bool TAPK, int ROWS, int NTH>
 struct LoaderFor {
-  using type = typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE, TAPK, ROWS>,
-                                         RLoader<MODE, TAPK, ROWS>>::type;
+  using type = typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE, TAPK, ROWS, NTH>,
+                                         RLoader<MODE, TAPK, ROWS, NTH>>::type;
 };
 
 // value = acc * alpha + bias + residuals, ReLU, then float32 and/or bf16 stores
@@ -422,9 +425,17 @@ __device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2]
 
 // BNT: block tile width in N (128, or 64 for launches whose 128-wide tiles
 // cannot give every CU two blocks); each wave owns 64 x (BNT / 2).
-template <int MA, int MB, bool TAPK, int BNT>
-__global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
+// KSL: waves per output sub-tile. With KSL = 2 (8 waves, 128-wide tiles
+// only) waves w and w + 4 own the same sub-tile and take the first and the
+// second half of every K step; their accumulators are added through LDS at
+// the end (first half + second half), so one block per CU keeps two waves
+// on every SIMD without the narrow tile's extra operand traffic.
+template <int MA, int MB, bool TAPK, int BNT, int KSL>
+__global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
   constexpr int NJ = BNT / 64;   // 32-column MFMA tiles per wave
+  constexpr int NTH = NT * KSL;
+  constexpr int KW = BK / KSL;   // k of each K step that one wave multiplies
+  static_assert(KSL == 1 || BNT == 128, "K-sliced waves use the 128-wide tile");
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TILE_ELEMS];  // [buffer][A|B]
 
   const int tid = threadIdx.x;
@@ -450,13 +461,13 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
   const int kend = min(args.K, kbeg + args.k_per_split);
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
-  typename LoaderFor<MA, TAPK>::type la;
-  typename LoaderFor<MB, TAPK, BNT>::type lb;
+  typename LoaderFor<MA, TAPK, BM, NTH>::type la;
+  typename LoaderFor<MB, TAPK, BNT, NTH>::type lb;
   la.init(A, row0, tid, kbeg);
   lb.init(B, col0, tid, kbeg);
 
   const int wave = tid >> 6, lane = tid & 63;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = (wave >> 1) & 1, wn = wave & 1, kslice = wave >> 2;
 
   f32x16_t acc[2][NJ];
 #pragma unroll
@@ -471,7 +482,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
     // faster for that operand pair only)
     if constexpr (MA == OP_K_CONV_DGRAD) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
+    for (int kk = kslice * KW; kk < (kslice + 1) * KW; kk += 16) {
       bf16x8_t fa[2], fb[NJ];
       const int kl = kk + (lane >> 5) * 8;
 #pragma unroll
@@ -527,6 +538,30 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(KArgs args) {
     if (kt < nk) compute(lds[0][0], lds[0][1]);   // odd step count: the last step is in buffer 0
   }
 
+  if constexpr (KSL == 2) {
+    // second-half waves hand their sums to the first-half waves through LDS
+    // (register r of tile (i, j) of lane l at [sub-tile][i][j][r][l])
+    float* red = reinterpret_cast<float*>(&lds[0][0][0]);
+    static_assert(sizeof(lds) >= 4 * 2 * NJ * 16 * 64 * sizeof(float), "the reduction fits the operand buffers");
+    float* mine = red + (wave & 3) * (2 * NJ * 16 * 64) + lane;
+    __syncthreads();
+    if (kslice == 1) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mine[((i * NJ + j) * 16 + r) * 64] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (kslice == 1) return;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] += mine[((i * NJ + j) * 16 + r) * 64];
+  }
   write_tile<NJ>(args, acc, row0, col0, wm, wn, lane, split, z, z1, z2);
 }
 
@@ -632,8 +667,14 @@ OperandDev make_operand(const Operand& o, int rows, int K, long extent) {
 template <int MA, int MB, bool TAPK = false>
 hipError_t launch(const KArgs& a, hipStream_t s) {
   dim3 grid(a.tiles_total, a.batch * a.splits);
-  if (a.bn == 64) hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 64>), grid, dim3(NT), 0, s, a);
-  else hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128>), grid, dim3(NT), 0, s, a);
+  if (a.bn == 64) {
+    hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 64, 1>), grid, dim3(NT), 0, s, a);
+  } else if (a.ksl == 2) {
+    if constexpr (MA != OP_K_CONV_FWD) return hipErrorInvalidValue;   // 8-wave blocks serve convolution forwards
+    hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 2>), grid, dim3(2 * NT), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 1>), grid, dim3(NT), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -641,37 +682,48 @@ hipError_t launch(const KArgs& a, hipStream_t s) {
 
 namespace {
 
-// Launch parameters of one GEMM: tile counts, the split of K and the device
-// view of both operands. Returns false (with err set) for a shape the kernel
-// cannot address; err stays hipSuccess for an empty problem.
-// Split K when the tiles cannot give every CU two resident blocks (two
-// 4-wave blocks per CU hide each other's barrier and load stalls) and K is
-// long: as many splits as keep all blocks resident at once, each with at
-// least 12 K steps (shorter slices cost more in the reduction than they gain),
-// and no more than the workspace holds.
-constexpr long kTargetBlocks = 2 * 256;
+constexpr long kCUs = 256;
+constexpr long kTargetBlocks = 2 * kCUs;   // two resident 4-wave blocks per CU
 
-// Block tile width in N: 64 when 128-wide tiles cannot give every CU two
-// blocks but 64-wide ones fill at least three quarters of the two-per-CU
-// slots, so the launch needs no K split; 128 otherwise.
-int tile_width(int M, int N, int batch) {
+// Kernel of a launch (block tile width bn, waves per output sub-tile ksl)
+// and its K split.
+//  * 4-wave blocks, two per CU: 128-wide tiles, or 64-wide ones where
+//    128-wide tiles cannot fill the two-per-CU slots but 64-wide ones fill
+//    at least three quarters of them without a K split.
+//  * A convolution forward of that narrow kind whose 128-wide tiles give
+//    between 7/8 of the CUs and every CU one block runs them on 8-wave blocks
+//    instead (ksl = 2; its gathered A operand is then loaded once per
+//    128 x 128 outputs). Other operand pairs, and launches filling fewer CUs,
+//    were measured slower on 8-wave blocks.
+//  * A split gives each slice at least 12 K steps (shorter slices cost more
+//    in the reduction than they gain), at most MAX_SPLITS slices and no more
+//    partials than the workspace holds.
+struct Shape {
+  int bn, ksl, splits;
+};
+
+Shape shape_of(int M, int N, int K, int batch, size_t workspace_bytes, bool conv_fwd) {
   const long rows = static_cast<long>((M + BM - 1) / BM) * batch;
   const long t128 = rows * ((N + 127) / 128), t64 = rows * ((N + 63) / 64);
-  return (t128 < kTargetBlocks && 4 * t64 >= 3 * kTargetBlocks) ? 64 : 128;
-}
-
-int split_rule(int M, int N, int K, int batch, size_t workspace_bytes) {
-  if (tile_width(M, N, batch) == 64) return 1;
-  const long tiles = static_cast<long>((N + BN - 1) / BN) * ((M + BM - 1) / BM) * batch;
-  if (tiles >= kTargetBlocks || K < 2 * 12 * BK) return 1;
-  int splits = static_cast<int>(kTargetBlocks / tiles);   // all blocks resident in one round
+  Shape sh{128, 1, 1};
+  if (t128 < kTargetBlocks && 4 * t64 >= 3 * kTargetBlocks) {
+    if (conv_fwd && t128 <= kCUs && 8 * t128 >= 7 * kCUs) sh.ksl = 2;
+    else sh.bn = 64;
+    return sh;
+  }
+  if (t128 >= kTargetBlocks || K < 2 * 12 * BK) return sh;
+  int splits = static_cast<int>(kTargetBlocks / t128);   // all blocks resident in one round
   splits = std::min(splits, K / (12 * BK));
   splits = std::min(splits, MAX_SPLITS);
   const long per = static_cast<long>(batch) * M * N * 4;
   while (splits > 1 && per * splits > static_cast<long>(workspace_bytes)) --splits;
-  return std::max(splits, 1);
+  sh.splits = std::max(splits, 1);
+  return sh;
 }
 
+// Launch parameters of one GEMM: kernel, tile counts, the split of K and the
+// device view of both operands. Returns false (with err set) for a shape the
+// kernel cannot address; err stays hipSuccess for an empty problem.
 bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   err = hipSuccess;
   if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return false;
@@ -688,10 +740,12 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   a.K = d.K;
   a.batch = d.batch;
   a.zdiv = zdiv;
-  a.bn = tile_width(d.M, d.N, d.batch);
+  const Shape sh = shape_of(d.M, d.N, d.K, d.batch, d.workspace ? d.workspace_bytes : 0, d.A.mode == OP_K_CONV_FWD);
+  a.bn = sh.bn;
+  a.ksl = sh.ksl;
   a.tiles_n = (d.N + a.bn - 1) / a.bn;
   a.tiles_total = a.tiles_n * ((d.M + BM - 1) / BM);
-  const int splits = d.workspace ? split_rule(d.M, d.N, d.K, d.batch, d.workspace_bytes) : 1;
+  const int splits = sh.splits;
   const int ksteps = (d.K + BK - 1) / BK;
   a.k_per_split = ((ksteps + splits - 1) / splits) * BK;
   a.splits = splits;
@@ -754,7 +808,7 @@ hipError_t launch_reduce(const KArgs& a, hipStream_t s) {
 
 int gemm_bf16_split_rule(int M, int N, int K, int batch, size_t workspace_bytes) {
   if (M <= 0 || N <= 0 || K <= 0 || batch <= 0) return 1;
-  return split_rule(M, N, K, batch, workspace_bytes);
+  return shape_of(M, N, K, batch, workspace_bytes, false).splits;
 }
 
 int gemm_bf16_splits(const GemmDesc& d) {

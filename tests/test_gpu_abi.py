@@ -118,13 +118,28 @@ def test_batch_one_stage_stepwise(kind):
     print(f"[stepwise] {wl.name}: {worst.report()}", flush=True)
 
 
+def test_ksliced_conv_forward_ragged_edges_stepwise():
+    # conv3x3 forward with 14490 x 200 outputs (B = 230 at 7 x 9): 114 x 2 tiles
+    # of 128 x 128, one block on most CUs, so both layers' forwards run on 8-wave
+    # blocks whose wave pairs split each K step, with a ragged last row tile
+    # (14490 = 113 * 128 + 26) and a ragged last column tile (200 = 128 + 72);
+    # the first layer (64 input channels) on the per-step tap gather, the
+    # second (200) on the per-vector one. The data gradients run on 128 x 64
+    # tiles.
+    spec = synth.StageSpec("conv3x3", "bf16", "none", 1, 4, 230, 2, (64, 200, 7, 9), 1e-3, 0.9)
+    wl = synth.Workload("conv_ksliced_ragged", (spec,), 4)
+    print(f"[stepwise] {wl.name}", flush=True)
+    worst = run_stepwise(wl, wl.steps, torch, derived=True)
+    print(f"[stepwise] {wl.name}: {worst.report()}", flush=True)
+
+
 def test_narrow_tile_ragged_edges_stepwise():
-    # 12283 x 200 outputs: the 128 x 128 tiles (97 x 2) cannot give every CU two
-    # blocks but 128 x 64 tiles (97 x 4) can, so the forward GEMMs and the
+    # 25000 x 200 outputs: the 128 x 128 tiles (196 x 2) cannot give every CU two
+    # blocks but 128 x 64 tiles (196 x 4) can, so the forward GEMMs and the
     # second layer's data gradient run on 128 x 64 tiles with no K split, with
-    # a ragged last row tile (12283 = 95 * 128 + 123) and a ragged last column
+    # a ragged last row tile (25000 = 195 * 128 + 40) and a ragged last column
     # tile (200 = 3 * 64 + 8), on both a row-major and a transposed B operand
-    spec = synth.StageSpec("fc", "bf16", "none", 1, 3, 12283, 2, (64, 200, 200), 0.01, 0.9)
+    spec = synth.StageSpec("fc", "bf16", "none", 1, 3, 25000, 2, (64, 200, 200), 0.01, 0.9)
     wl = synth.Workload("fc_narrow_ragged", (spec,), 4)
     print(f"[stepwise] {wl.name}", flush=True)
     worst = run_stepwise(wl, wl.steps, torch, derived=True)

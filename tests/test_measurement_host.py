@@ -14,7 +14,7 @@ sys.path.insert(0, ROOT)
 
 from paper_1809_02839_amd import profiling  # noqa: E402
 
-GEMM = "void spx::(anonymous namespace)::gemm_bf16_kernel<3, 4, false>(spx::(anonymous namespace)::KArgs)"
+GEMM = "void spx::(anonymous namespace)::gemm_bf16_kernel<3, 4, false, 128, 1>(spx::(anonymous namespace)::KArgs)"
 UPD = "spx::(anonymous namespace)::fused_update_partials_kernel(float*, float*)"
 NEG = "void at::native::vectorized_elementwise_kernel<4, at::native::neg_kernel_cuda>(int, float*)"
 
@@ -30,7 +30,7 @@ def _counter_csv(path, rows):
 
 
 def test_short_name_strips_namespaces_and_arguments():
-    assert profiling.short_name(GEMM) == "gemm_bf16_kernel<3, 4, false>"
+    assert profiling.short_name(GEMM) == "gemm_bf16_kernel<3, 4, false, 128, 1>"
     assert profiling.short_name(UPD) == "fused_update_partials_kernel"
     assert profiling.short_name("plain_kernel") == "plain_kernel"
 
@@ -48,7 +48,7 @@ def test_traffic_scales_each_counter_by_the_calibration_copy(tmp_path):
     rows, f_read, f_write = profiling.traffic_table(str(tmp_path / "f"), str(tmp_path / "w"), calib, "neg")
     assert f_read == pytest.approx(0.25) and f_write == pytest.approx(1.0)
     (r,) = rows
-    assert r["kernel"] == "gemm_bf16_kernel<3, 4, false>" and r["dispatches"] == 2
+    assert r["kernel"] == "gemm_bf16_kernel<3, 4, false, 128, 1>" and r["dispatches"] == 2
     assert r["fetch_kib"] == pytest.approx(2250.0) and r["write_kib"] == pytest.approx(200.0)
     assert r["bytes"] == pytest.approx(2250.0 * 1024 * 0.25 + 200.0 * 1024)
 
@@ -56,7 +56,7 @@ def test_traffic_scales_each_counter_by_the_calibration_copy(tmp_path):
     profiling.write_traffic(str(md), rows, f_read, f_write, calib, "t", "cmd")
     digest, table = profiling.read_traffic(str(md))
     assert digest == profiling.source_digest()
-    assert table == {"gemm_bf16_kernel<3, 4, false>": pytest.approx(round(r["bytes"]))}
+    assert table == {"gemm_bf16_kernel<3, 4, false, 128, 1>": pytest.approx(round(r["bytes"]))}
 
 
 def test_mfma_busy_is_normalised_by_dispatch_duration(tmp_path):
@@ -65,7 +65,7 @@ def test_mfma_busy_is_normalised_by_dispatch_duration(tmp_path):
     _counter_csv(tmp_path / "c", [(7, GEMM, "SQ_VALU_MFMA_BUSY_CYCLES", busy, 1000, 1000 + dur),
                                   (7, GEMM, "GRBM_GUI_ACTIVE", 123.0, 1000, 1000 + dur)])
     means = profiling.counter_means(str(tmp_path / "c"))
-    n, cs = means["gemm_bf16_kernel<3, 4, false>"]
+    n, cs = means["gemm_bf16_kernel<3, 4, false, 128, 1>"]
     assert n == 1 and cs[profiling.DURATION] == dur
     md = tmp_path / "m.md"
     profiling.write_counters([str(tmp_path / "c")], str(md), "t", "cmd")
@@ -83,7 +83,7 @@ def test_kernel_stats_table_is_sorted_by_total_time(tmp_path):
     md = tmp_path / "s.md"
     profiling.write_stats(str(p), str(md), "t", "cmd", "notes")
     body = [line for line in md.read_text().splitlines() if line.startswith("| ") and not line.startswith("| kernel |")]
-    assert body[0].startswith("| gemm_bf16_kernel<3, 4, false>") and body[1].startswith("| fused_update")
+    assert body[0].startswith("| gemm_bf16_kernel<3, 4, false, 128, 1>") and body[1].startswith("| fused_update")
 
 
 def test_traffic_entry_is_null_once_the_kernel_sources_change(monkeypatch):
@@ -104,8 +104,8 @@ def test_bench_refuses_more_than_one_gpu():
 
 def test_traffic_of_a_family_with_two_instantiations_is_dispatch_weighted(monkeypatch):
     import bench
-    table = {"gemm_bf16_kernel<2, 5, true, 64>": (3, 60.0), "gemm_bf16_kernel<2, 5, true, 128>": (1, 100.0),
-             "gemm_bf16_kernel<3, 4, false, 128>": (4, 7.0)}
+    table = {"gemm_bf16_kernel<2, 5, true, 64, 1>": (3, 60.0), "gemm_bf16_kernel<2, 5, true, 128, 1>": (1, 100.0),
+             "gemm_bf16_kernel<3, 4, false, 128, 1>": (4, 7.0)}
     monkeypatch.setattr(profiling, "read_traffic", lambda path, with_dispatches=False: ("d" * 16, table))
     monkeypatch.setattr(profiling, "source_digest", lambda: "d" * 16)
     assert bench.traffic_per_launch("vgg_conv", "conv3x3_dgrad") == 70   # (3 * 60 + 100) / 4
