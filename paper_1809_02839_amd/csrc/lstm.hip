@@ -14,16 +14,21 @@
 // (row, unit) per thread. The contraction uses v_mfma_f32_16x16x32_bf16 with
 // operands loaded straight from global memory (h or dz rows are shared by all
 // blocks and stay in L2; each block's weight rows are re-read every step from
-// its XCD's L2). A block covers 16 batch rows; its waves split K, issue all
-// their loads at once and add their partial tiles in a fixed order in LDS, so
-// a step costs about one round of load latency.
+// its XCD's L2). A forward block covers 32 batch rows and 8 units (the tile
+// shape that loads the fewest operand bytes per CU at 64 rows and 1024 units:
+// 64 KB of h and 64 KB of weights), a backward block 16 rows and 16 units;
+// the waves of a block split K, issue all their loads at once and add their
+// partial tiles in a fixed order in LDS, so a step costs about one round of
+// load latency.
 #include "kernels.hpp"
 
 namespace spx {
 namespace {
 
-constexpr int FWD_UNITS = 4;    // forward: 4 units x 4 gates = 16 z columns per block
-constexpr int FWD_WAVES = 4;    // forward: K = H split over 4 waves
+constexpr int FWD_UNITS = 8;    // forward: 8 units x 4 gates = 32 z columns per block
+constexpr int FWD_ROWS = 32;    // forward: batch rows per block
+constexpr int FWD_WAVES = 8;    // forward: K = H split over 8 waves
+constexpr int FWD_CHUNK = 4;    // forward: fragments per operand tile a wave loads before its MFMAs
 constexpr int BWD_UNITS = 16;   // backward: 16 units of dh per block
 constexpr int BWD_WAVES = 16;   // backward: K = 4H split over 16 waves
 constexpr int CHUNK = 8;        // fragments a wave loads before its MFMAs
@@ -58,6 +63,42 @@ __device__ __forceinline__ f32x4_t contract16(const bf16_t* arow, const bf16_t* 
   return acc;
 }
 
+// One wave's share of a 32 x 32 tile as 2 x 2 tiles of 16 x 16, like
+// contract16: arow[i] / brow[j] supply rows 16 i + l % 16 of A and 16 j + l % 16
+// of Bm (already offset by the lane's k quarter). Each A and Bm fragment is
+// loaded once for the two tiles that use it. Lane l ends with rows
+// 16 i + 4 (l / 16) + r of column 16 j + l % 16 in acc[i][j][r].
+template <int WAVES>
+__device__ __forceinline__ void contract32(const bf16_t* const (&arow)[2], const bf16_t* const (&brow)[2], int K,
+                                           int wave, f32x4_t (&acc)[2][2]) {
+  const int nf = K / 32;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int f0 = wave * FWD_CHUNK; f0 < nf; f0 += WAVES * FWD_CHUNK) {
+    bf16x8_t a[2][FWD_CHUNK], b[2][FWD_CHUNK];
+#pragma unroll
+    for (int q = 0; q < FWD_CHUNK; ++q)
+      if (f0 + q < nf) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          a[i][q] = ld8(arow[i] + 32 * (f0 + q));
+          b[i][q] = ld8(brow[i] + 32 * (f0 + q));
+        }
+      }
+#pragma unroll
+    for (int q = 0; q < FWD_CHUNK; ++q)
+      if (f0 + q < nf) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+      }
+  }
+}
+
 // Sum the WAVES partial tiles in wave order into tile[16][17] (LDS).
 template <int WAVES>
 __device__ __forceinline__ void reduce_tile(const f32x4_t& acc, float (*red)[16][17], float (*tile)[17], int wave,
@@ -75,19 +116,19 @@ __device__ __forceinline__ void reduce_tile(const f32x4_t& acc, float (*red)[16]
   __syncthreads();
 }
 
-// Block (bx, by): batch rows 16 by .. 16 by + 15, units FWD_UNITS bx ..
+// Block (bx, by): batch rows FWD_ROWS by .., units FWD_UNITS bx ..
 __global__ __launch_bounds__(64 * FWD_WAVES) void lstm_step_fwd_kernel(const float* zx_t, const bf16_t* h_prev,
                                                                        const bf16_t* Wh, const float* c_prev, int B,
                                                                        int H, float* gates_t, float* c_t,
                                                                        bf16_t* h_t) {
-  __shared__ float red[FWD_WAVES][16][17];
-  __shared__ float zs[16][17];
+  __shared__ float red[FWD_WAVES][FWD_ROWS][FWD_ROWS + 1];
+  __shared__ float zs[FWD_ROWS][FWD_ROWS + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int u0 = blockIdx.x * FWD_UNITS, r0 = blockIdx.y * 16;
+  const int u0 = blockIdx.x * FWD_UNITS, r0 = blockIdx.y * FWD_ROWS;
   const long H4 = 4L * H;
   // the cell's own operands are loaded first so their latency overlaps the contraction
   const int crow = r0 + tid / FWD_UNITS, cuu = tid % FWD_UNITS, cu = u0 + cuu;
-  const bool cell = tid < 16 * FWD_UNITS && crow < B;
+  const bool cell = tid < FWD_ROWS * FWD_UNITS && crow < B;
   float zx[4] = {0.0f, 0.0f, 0.0f, 0.0f}, cp = 0.0f;
   if (cell) {
 #pragma unroll
@@ -97,11 +138,34 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void lstm_step_fwd_kernel(const flo
   if (h_prev) {
     // block column c = 4 unit + gate is the weight row gate * H + u0 + unit;
     // rows past B read row 0 (valid memory) and are never read back
-    const int col = lane & 15, kq = 8 * (lane >> 4);
-    const int row = r0 + (lane & 15);
-    const bf16_t* arow = h_prev + static_cast<long>(row < B ? row : 0) * H + kq;
-    const bf16_t* brow = Wh + static_cast<long>((col & 3) * H + u0 + (col >> 2)) * H + kq;
-    reduce_tile<FWD_WAVES>(contract16<FWD_WAVES>(arow, brow, H, wave), red, zs, wave, lane, tid);
+    const int kq = 8 * (lane >> 4);
+    const bf16_t* arow[2];
+    const bf16_t* brow[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int row = r0 + 16 * i + (lane & 15), col = 16 * i + (lane & 15);
+      arow[i] = h_prev + static_cast<long>(row < B ? row : 0) * H + kq;
+      brow[i] = Wh + static_cast<long>((col & 3) * H + u0 + (col >> 2)) * H + kq;
+    }
+    f32x4_t acc[2][2];
+    contract32<FWD_WAVES>(arow, brow, H, wave, acc);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[wave][16 * i + 4 * (lane >> 4) + r][16 * j + (lane & 15)] = acc[i][j][r];
+    __syncthreads();
+    // the partial tiles summed in wave order, two entries per thread
+#pragma unroll
+    for (int e = tid; e < FWD_ROWS * FWD_ROWS; e += 64 * FWD_WAVES) {
+      const int i = e / FWD_ROWS, j = e % FWD_ROWS;
+      float v = 0.0f;
+#pragma unroll
+      for (int w = 0; w < FWD_WAVES; ++w) v += red[w][i][j];
+      zs[i][j] = v;
+    }
+    __syncthreads();
   }
   if (cell) {
     float z[4];
@@ -187,7 +251,7 @@ bool lstm_step_supported(int B, int H) { return B >= 1 && B <= 64 && H >= 32 && 
 hipError_t lstm_step_fwd(const float* zx_t, const bf16_t* h_prev, const bf16_t* Wh, const float* c_prev, int B,
                          int H, float* gates_t, float* c_t, bf16_t* h_t, hipStream_t s) {
   if (!lstm_step_supported(B, H)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(lstm_step_fwd_kernel, dim3(H / FWD_UNITS, (B + 15) / 16), dim3(64 * FWD_WAVES), 0, s, zx_t,
+  hipLaunchKernelGGL(lstm_step_fwd_kernel, dim3(H / FWD_UNITS, (B + FWD_ROWS - 1) / FWD_ROWS), dim3(64 * FWD_WAVES), 0, s, zx_t,
                      h_prev, Wh, c_prev, B, H, gates_t, c_t, h_t);
   return hipGetLastError();
 }
