@@ -59,7 +59,7 @@ DESCRIPTIONS = {
 # Kernel (rocprofv3 short name prefix) behind each launch family of the stage.
 FAMILY_KERNEL = {
     "conv3x3_fwd": "gemm_bf16_kernel<1, 0",
-    "conv3x3_dgrad": "gemm_bf16_kernel<2, 5",
+    "conv3x3_dgrad": "gemm_bf16_kernel<2, ",   # <2, 0: against the transposed filter; <2, 5: read transposed
     "conv3x3_wgrad": "gemm_bf16_kernel<3, 4",
     "gemm_bf16_xwT": "gemm_bf16_kernel<0, 0",
     "gemm_bf16_dyW": "gemm_bf16_kernel<0, 3",

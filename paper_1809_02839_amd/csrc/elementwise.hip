@@ -592,7 +592,58 @@ __global__ void fill_kernel(float* x, float v, long n) {
     x[i] = v;
 }
 
+// Wt[c][t][o] = W[o][t][c] for each 3x3 filter W [Co][9][Ci] of a batch of
+// layers: the convolution data gradient then reads its weight operand with
+// k = t Co + o contiguous, as the forward reads W. One 64 x 64 (o, c) tile of
+// one tap of one layer per block (blockIdx.z = 9 layer + tap) through LDS,
+// 16-byte loads along c and stores along o (Co, Ci multiples of 8).
+__global__ __launch_bounds__(256) void filter_transpose_kernel(FilterBatch fb) {
+  __shared__ bf16_t tile[64][66];   // [o][c]
+  const int layer = blockIdx.z / 9, t = blockIdx.z - 9 * layer;
+  const bf16_t* const W = fb.W[layer];
+  bf16_t* const Wt = fb.Wt[layer];
+  const int Co = fb.Co, Ci = fb.Ci[layer];
+  const int c0 = blockIdx.x * 64, o0 = blockIdx.y * 64, tid = threadIdx.x;
+  if (c0 >= Ci) return;   // the grid covers the widest layer
+#pragma unroll
+  for (int v = tid; v < 512; v += 256) {
+    const int r = v >> 3, q = (v & 7) * 8, o = o0 + r, c = c0 + q;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (o < Co && c < Ci) val = *reinterpret_cast<const uint4*>(W + (static_cast<long>(o) * 9 + t) * Ci + c);
+    const uint32_t w[4] = {val.x, val.y, val.z, val.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      tile[r][q + 2 * j] = static_cast<bf16_t>(w[j] & 0xffff);
+      tile[r][q + 2 * j + 1] = static_cast<bf16_t>(w[j] >> 16);
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int v = tid; v < 512; v += 256) {
+    const int r = v >> 3, q = (v & 7) * 8, c = c0 + r, o = o0 + q;
+    if (c < Ci && o < Co) {
+      uint32_t w[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w[j] = static_cast<uint32_t>(tile[q + 2 * j][r]) | (static_cast<uint32_t>(tile[q + 2 * j + 1][r]) << 16);
+      *reinterpret_cast<uint4*>(Wt + (static_cast<long>(c) * 9 + t) * Co + o) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t filter_transpose_bf16(const FilterBatch& fb, hipStream_t s) {
+  if (fb.n <= 0) return hipSuccess;
+  if (fb.n > FilterBatch::MAX || fb.Co <= 0 || fb.Co % 8) return hipErrorInvalidValue;
+  int cmax = 0;
+  for (int l = 0; l < fb.n; ++l) {
+    if (fb.Ci[l] <= 0 || fb.Ci[l] % 8 || !fb.W[l] || !fb.Wt[l]) return hipErrorInvalidValue;
+    cmax = std::max(cmax, fb.Ci[l]);
+  }
+  hipLaunchKernelGGL(filter_transpose_kernel, dim3((cmax + 63) / 64, (fb.Co + 63) / 64, 9 * fb.n), dim3(256), 0, s, fb);
+  return hipGetLastError();
+}
 
 hipError_t mask_relu_grad(const void* src, const void* mask, void* dst, long n, int dtype, hipStream_t s) {
   if (n <= 0) return hipSuccess;

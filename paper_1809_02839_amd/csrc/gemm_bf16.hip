@@ -480,7 +480,7 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
   auto compute = [&](const bf16_t* sa, const bf16_t* sb) {
     // data gradient: the wave issuing MFMAs goes first while it does (measured
     // faster for that operand pair only)
-    if constexpr (MA == OP_K_CONV_DGRAD) __builtin_amdgcn_s_setprio(1);
+    if constexpr (MA == OP_K_CONV_DGRAD && MB == OP_R_FILTER_T) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kk = kslice * KW; kk < (kslice + 1) * KW; kk += 16) {
       bf16x8_t fa[2], fb[NJ];
@@ -500,7 +500,7 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
     __builtin_amdgcn_iglp_opt(0);
-    if constexpr (MA == OP_K_CONV_DGRAD) __builtin_amdgcn_s_setprio(0);
+    if constexpr (MA == OP_K_CONV_DGRAD && MB == OP_R_FILTER_T) __builtin_amdgcn_s_setprio(0);
   };
 
   if (nk > 0) {
@@ -670,7 +670,8 @@ hipError_t launch(const KArgs& a, hipStream_t s) {
   if (a.bn == 64) {
     hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 64, 1>), grid, dim3(NT), 0, s, a);
   } else if (a.ksl == 2) {
-    if constexpr (MA != OP_K_CONV_FWD) return hipErrorInvalidValue;   // 8-wave blocks serve convolution forwards
+    if constexpr (MB != OP_K_PLAIN || (MA != OP_K_CONV_FWD && MA != OP_K_CONV_DGRAD))
+      return hipErrorInvalidValue;   // 8-wave blocks serve convolution gathers against a row-major filter
     hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 2>), grid, dim3(2 * NT), 0, s, a);
   } else {
     hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 1>), grid, dim3(NT), 0, s, a);
@@ -740,7 +741,8 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   a.K = d.K;
   a.batch = d.batch;
   a.zdiv = zdiv;
-  const Shape sh = shape_of(d.M, d.N, d.K, d.batch, d.workspace ? d.workspace_bytes : 0, d.A.mode == OP_K_CONV_FWD);
+  const bool gather = (d.A.mode == OP_K_CONV_FWD || d.A.mode == OP_K_CONV_DGRAD) && d.B.mode == OP_K_PLAIN;
+  const Shape sh = shape_of(d.M, d.N, d.K, d.batch, d.workspace ? d.workspace_bytes : 0, gather);
   a.bn = sh.bn;
   a.ksl = sh.ksl;
   a.tiles_n = (d.N + a.bn - 1) / a.bn;
@@ -787,6 +789,9 @@ hipError_t launch_main(const GemmDesc& d, const KArgs& a, hipStream_t s) {
   if (ma == OP_K_CONV_DGRAD && mb == OP_R_FILTER_T)
     return (d.A.g.C % BK == 0 && d.B.g.C2 % BK == 0) ? launch<OP_K_CONV_DGRAD, OP_R_FILTER_T, true>(a, s)
                                                     : launch<OP_K_CONV_DGRAD, OP_R_FILTER_T>(a, s);
+  if (ma == OP_K_CONV_DGRAD && mb == OP_K_PLAIN)
+    return (d.A.g.C % BK == 0) ? launch<OP_K_CONV_DGRAD, OP_K_PLAIN, true>(a, s)
+                               : launch<OP_K_CONV_DGRAD, OP_K_PLAIN>(a, s);
   if (ma == OP_R_PLAIN && mb == OP_R_CONV_WGRAD) return launch<OP_R_PLAIN, OP_R_CONV_WGRAD>(a, s);
   return hipErrorInvalidValue;
 }

@@ -134,6 +134,16 @@ inline long layernorm_bwd_ws_floats(long rows, long d) { return 3 * ((rows + LNB
 // ------------------------------------------------------------ elementwise ----
 // dst[i] = src[i] * (mask[i] > 0), bf16 (dtype 1) or float32 (dtype 0).
 hipError_t mask_relu_grad(const void* src, const void* mask, void* dst, long n, int dtype, hipStream_t s);
+// Wt [Ci][9][Co] from each 3x3 filter W [Co][9][Ci] of up to MAX layers, one
+// launch (bf16; Co and every Ci multiples of 8).
+struct FilterBatch {
+  static constexpr int MAX = 16;
+  const bf16_t* W[MAX];
+  bf16_t* Wt[MAX];
+  int Ci[MAX];
+  int n, Co;
+};
+hipError_t filter_transpose_bf16(const FilterBatch& fb, hipStream_t s);
 // out[c] (=|+=) sum over rows r of X[r * ld + c], X bf16 or float32; deterministic.
 hipError_t column_sum(const void* X, int dtype, long rows, int cols, long ld, float* out, int accumulate,
                       float* partial_ws, hipStream_t s);

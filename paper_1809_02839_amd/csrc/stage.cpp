@@ -293,7 +293,8 @@ void Stage::plan_buffers() {
       const long cmax = std::max(dm[0], dm[1]);
       ws = {static_cast<size_t>(P * cmax * esz_), static_cast<size_t>(P * cmax * esz_),
             static_cast<size_t>(B * V * 4), static_cast<size_t>(ce ? B * 4 : 0),
-            static_cast<size_t>(ce ? B * dm[1] * 2 : 0)};
+            static_cast<size_t>(ce ? B * dm[1] * 2 : 0),
+            static_cast<size_t>(9L * dm[1] * (dm[0] + (L - 1L) * dm[1]) * esz_)};   // id 5: transposed filters
       partial = partial_floats(B, V);
       for (int l = 0; l < L && dt_; ++l) {   // filter-gradient partials, reduced by the update
         const int C = l == 0 ? dm[0] : dm[1];
@@ -755,6 +756,31 @@ void Stage::bwd_conv(int slot, const void* dy, void* dx) {
   else
     LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * Cout, 1, s_));
   const void* dz = ws<void>(0);
+  // the data gradients read each filter transposed ([C][9][C_out], k
+  // contiguous), made for every layer that needs one in launches of up to
+  // FilterBatch::MAX layers
+  std::vector<bf16_t*> wt(L);
+  {
+    bf16_t* p = ws<bf16_t>(5);
+    for (int l = 0; l < L; ++l) {
+      wt[l] = p;
+      p += 9L * Cout * (l == 0 ? Cin : Cout);
+    }
+    FilterBatch fb{};
+    fb.Co = Cout;
+    double bytes = 0;
+    for (int l = dx ? 0 : 1; l < L; ++l) {
+      fb.W[fb.n] = static_cast<const bf16_t*>(wb(l));
+      fb.Wt[fb.n] = wt[l];
+      fb.Ci[fb.n] = l == 0 ? Cin : Cout;
+      bytes += 4.0 * 9 * Cout * fb.Ci[fb.n];
+      if (++fb.n == FilterBatch::MAX || l == L - 1) {
+        LAUNCH("filter_transpose", 0, bytes, filter_transpose_bf16(fb, s_));
+        fb.n = 0;
+        bytes = 0;
+      }
+    }
+  }
   int pp = 1;
   for (int l = L - 1; l >= 0; --l) {
     const int C = l == 0 ? Cin : Cout;
@@ -763,8 +789,7 @@ void Stage::bwd_conv(int slot, const void* dy, void* dx) {
     gemm(gw, true);
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
-    GemmDesc gx = gd(P, C, 9 * Cout, opConv(OP_K_CONV_DGRAD, dz, B, H, W, Cout),
-                     opConv(OP_R_FILTER_T, wb(l), B, H, W, C, Cout), C);
+    GemmDesc gx = gd(P, C, 9 * Cout, opConv(OP_K_CONV_DGRAD, dz, B, H, W, Cout), opK(wt[l], 9 * Cout), C);
     gx.epi.out_bf16 = static_cast<bf16_t*>(out);
     if (l > 0) gx.epi.mask = act(l);
     gemm(gx);
