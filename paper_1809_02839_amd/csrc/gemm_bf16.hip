@@ -5,8 +5,9 @@
 //
 // Block tile 128 x 128 (or 128 x 64, see shape_of), K step 64, 256 threads =
 // 4 waves in a 2 x 2 grid, each wave owning a 64 x 64 (64 x 32) sub-tile of
-// 2 x 2 (2 x 1) MFMA tiles of 32 x 32; some convolution forwards use 512
-// threads, two waves per sub-tile that share each K step. K-mode operand
+// 2 x 2 (2 x 1) MFMA tiles of 32 x 32; some convolution gathers (forward, and
+// data gradient against a transposed filter) use 512 threads, two waves per
+// sub-tile that share each K step. K-mode operand
 // tiles are staged in LDS as [row][k] (8 consecutive k per lane make one
 // 16-byte MFMA operand read; the 144-byte row pitch puts eight consecutive
 // rows on disjoint banks); R-mode tiles (rows contiguous in memory) are staged
@@ -478,8 +479,9 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   auto compute = [&](const bf16_t* sa, const bf16_t* sb) {
-    // data gradient: the wave issuing MFMAs goes first while it does (measured
-    // faster for that operand pair only)
+    // data gradient reading the filter through the transposing LDS reads: the
+    // wave issuing MFMAs goes first while it does (measured faster for that
+    // operand pair only; slower against the transposed filter copy)
     if constexpr (MA == OP_K_CONV_DGRAD && MB == OP_R_FILTER_T) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kk = kslice * KW; kk < (kslice + 1) * KW; kk += 16) {
@@ -691,11 +693,12 @@ constexpr long kTargetBlocks = 2 * kCUs;   // two resident 4-wave blocks per CU
 //  * 4-wave blocks, two per CU: 128-wide tiles, or 64-wide ones where
 //    128-wide tiles cannot fill the two-per-CU slots but 64-wide ones fill
 //    at least three quarters of them without a K split.
-//  * A convolution forward of that narrow kind whose 128-wide tiles give
-//    between 7/8 of the CUs and every CU one block runs them on 8-wave blocks
-//    instead (ksl = 2; its gathered A operand is then loaded once per
-//    128 x 128 outputs). Other operand pairs, and launches filling fewer CUs,
-//    were measured slower on 8-wave blocks.
+//  * A convolution gather against a row-major filter (the forward, or the
+//    data gradient against a transposed filter copy) of that narrow kind
+//    whose 128-wide tiles give between 7/8 of the CUs and every CU one block
+//    runs them on 8-wave blocks instead (ksl = 2; its gathered A operand is
+//    then loaded once per 128 x 128 outputs). Other operand pairs, and
+//    launches filling fewer CUs, were measured slower on 8-wave blocks.
 //  * A split gives each slice at least 12 K steps (shorter slices cost more
 //    in the reduction than they gain), at most MAX_SPLITS slices and no more
 //    partials than the workspace holds.
