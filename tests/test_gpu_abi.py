@@ -124,8 +124,9 @@ def test_ksliced_conv_forward_ragged_edges_stepwise():
     # blocks whose wave pairs split each K step, with a ragged last row tile
     # (14490 = 113 * 128 + 26) and a ragged last column tile (200 = 128 + 72);
     # the first layer (64 input channels) on the per-step tap gather, the
-    # second (200) on the per-vector one. The data gradients run on 128 x 64
-    # tiles.
+    # second (200) on the per-vector one. The second layer's data gradient
+    # (into 200 channels, against the transposed filter) runs the same 8-wave
+    # blocks; the first layer's (into 64 channels) 4-wave 128 x 128 tiles.
     spec = synth.StageSpec("conv3x3", "bf16", "none", 1, 4, 230, 2, (64, 200, 7, 9), 1e-3, 0.9)
     wl = synth.Workload("conv_ksliced_ragged", (spec,), 4)
     print(f"[stepwise] {wl.name}", flush=True)
