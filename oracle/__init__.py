@@ -22,8 +22,10 @@ Precision: arithmetic is float64. Where a workload fixes a storage precision
 value is rounded to it at the point the stage definition stores it. Every
 function states the passage it follows.
 
-Pins (tests/test_oracle_*.py): the worked example of Section 3.2, a brute-force
-count of updates between a stage's forward and backward, exact reduction to
+Pins (tests/test_oracle_*.py): the worked example of Section 3.2, Eq. 5 and
+Eq. 6 as brute-force counts of the updates between a pass and the completion
+of the round trip, a count of updates between a stage's forward and backward,
+the stage-to-stage hand-off against the composed network under autograd, exact reduction to
 sequential momentum SGD at s=0, the closed form under a constant gradient
 with dyadic constants, gamma=1 freezing, central finite differences of every
 stage kind, library special cases (torch CPU conv2d, LSTM, layer_norm,

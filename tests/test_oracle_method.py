@@ -43,6 +43,26 @@ def test_update_count_between_forward_and_backward(N):
 
 
 @pytest.mark.parametrize("N", range(1, 9))
+def test_version_difference_counts_updates_until_round_trip_completes(N):
+    """Section 3.2 defines s as the number of time units between the current
+    pass at stage k and the moment the mini-batch completes its round trip
+    (its backward at stage 0). Counted on the oracle's half-unit grid: the
+    updates stage k makes, from other mini-batches' backwards, after the pass
+    and no later than B_0(m) must equal Eq. 5 for F_k(m) and Eq. 6 for B_k(m).
+    The count is taken by enumeration of the task times, not by the formula,
+    so a ceil(k/2) or an off-by-one in either equation fails at some (k, N)."""
+    M = 4 * N + 6
+    for k in range(N):
+        upd_times = {m2: schedule.backward_time(k, N, m2) for m2 in range(M)}
+        for m in range(N, M - N):
+            done = schedule.backward_time(0, N, m)          # round trip completes
+            for forward in (True, False):
+                t = schedule.forward_time(k, N, m) if forward else schedule.backward_time(k, N, m)
+                count = sum(1 for m2, tb in upd_times.items() if m2 != m and t < tb <= done)
+                assert count == method.version_difference(k, N, forward), (N, k, m, forward, count)
+
+
+@pytest.mark.parametrize("N", range(1, 9))
 def test_pipeline_dependencies(N):
     """Every forward at stage k>0 runs after the same mini-batch's forward at
     k-1, every backward after the loss (last forward) and after the backward at
@@ -181,6 +201,38 @@ def test_s0_pipeline_equals_sequential_momentum_sgd_torch():
         opt.step()
     flat = np.concatenate([p.detach().numpy().reshape(-1) for p in params])
     np.testing.assert_allclose(r["W"][0], flat, rtol=2e-6, atol=2e-7)
+
+
+def test_pipeline_handoff_equals_composed_network():
+    """Section 3.1: a mini-batch's forward output at stage k is the input of
+    stage k+1, and its input gradient at stage k+1 is the upstream gradient of
+    stage k. With gamma = 1 (v stays 0, so every pass uses W0) the whole
+    3-stage pipeline must reproduce, for every mini-batch, the composed
+    network's loss, every stage's output and every stage's input gradient, as
+    torch CPU autograd computes them on the three stages chained."""
+    base = synth.SMALL_WORKLOADS["mlp3_small"]
+    wl = dataclasses.replace(base, stages=tuple(dataclasses.replace(s, momentum=1.0) for s in base.stages),
+                             steps=9)
+    r = trajectory.run(wl, exact=True, keep_io=True)
+    Ps = [stages.unpack(s, synth.initial_params(s)) for s in wl.stages]
+    for m in range(wl.steps):
+        x = torch.tensor(synth.stage_input(wl.stages[0], m), dtype=torch.float64, requires_grad=True)
+        lab = torch.tensor(synth.labels(wl.stages[2], m), dtype=torch.long)
+        hs = [x]
+        for k, P in enumerate(Ps):
+            z = hs[-1] @ torch.tensor(P["fc0.weight"]).T + torch.tensor(P["fc0.bias"])
+            if k < 2:
+                z = torch.relu(z)
+                z.retain_grad()
+            hs.append(z)
+        loss = torch.nn.functional.cross_entropy(hs[-1], lab)
+        loss.backward()
+        assert abs(loss.item() - r["loss"][m]) <= 1e-12 * max(1.0, abs(loss.item()))
+        for k in range(2):
+            np.testing.assert_allclose(r["y"][(k, m)], hs[k + 1].detach().numpy(), rtol=1e-12, atol=1e-14)
+            # the input gradient of stage k+1 is the gradient of stage k's output
+            np.testing.assert_allclose(r["dx"][(k + 1, m)], hs[k + 1].grad.numpy(), rtol=1e-10, atol=1e-14)
+        np.testing.assert_allclose(r["dx"][(0, m)], x.grad.numpy(), rtol=1e-10, atol=1e-14)
 
 
 # ------------------------------------------- staleness policies (Section 4.2) ----
