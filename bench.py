@@ -7,21 +7,26 @@ weight slots (Eq. 1, Eq. 4), and the forward of the next mini-batch (against
 the forward-predicted weights, Eq. 5 difference). The stage keeps N - k
 mini-batches in flight, as in the one-forward-one-backward schedule.
 
-Default workload: the VGG-16-style 3x3-conv stage (4 conv layers,
-256->512->512->512->512 channels, 8x8 maps, batch 128, bf16 operands with
-float32 master weights, stage 2 of 4). Inputs are synthetic (seeded normal
-draws, already resident in HBM when the timed region starts; a ring of eight
-mini-batches whose second half repeats the first with negated upstream
-gradients, so the weights stay bounded over hundreds of steps).
+Default workload: the ResNet-152-style bottleneck stage (8 bottleneck blocks
+1x1 1024->256, 3x3 256->256, 1x1 256->1024 with identity skips, 14x14 maps,
+batch 64, bf16 operands with float32 master weights, stage 3 of 4), the
+stage with the most contraction work per step. Inputs are synthetic (seeded
+normal draws, already resident in HBM when the timed region starts; a ring
+of eight mini-batches whose second half repeats the first with negated
+upstream gradients, so the weights stay bounded over hundreds of steps).
 
-Output: one JSON line on stdout. `value` is samples per second; `roofline`
-describes the kernel family with the largest share of the step time, measured
-in a separate pass with HIP events around each launch on the stage's stream;
-`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
-`step_roofline_frac` is the step's lower bound (every contraction at the MFMA
-peak plus the update's algorithmic bytes at the HBM peak) over the measured
-step; `predict_update_GBps_cold` is the fused update's bandwidth in a pass
-that evicts every cache before each update.
+Output: one JSON line on stdout. `value` is samples per second. A separate
+pass times every launch with HIP events on the stage's stream; each kernel
+family (one kernel instantiation) is set against the roof that bounds it,
+MFMA when its algorithmic flops at the MFMA peak take longer than its
+algorithmic bytes at the HBM peak, HBM otherwise. `roofline` describes the
+family with the largest share of the step time; `kernels` lists the largest
+families. `step_roofline_frac` is the step's lower bound (the sum over
+families of max(flops / MFMA peak, bytes / HBM peak)) over the measured step.
+`predict_update_GBps` counts the fused update's 24 algorithmic bytes per
+parameter (28 for float32 stages); `predict_update_GBps_cold` is the same in
+a pass that evicts every cache before each update. `cpu_baseline` times the
+CPU oracle on a bounded sample of the same workload.
 """
 import argparse
 import dataclasses
@@ -56,33 +61,45 @@ DESCRIPTIONS = {
 }
 
 
-# Kernel (rocprofv3 short name prefix) behind each launch family of the stage.
+# Kernel (rocprofv3 short name prefix) behind each pass family that is not
+# named by its kernel (GEMM families are the kernel instantiations).
 FAMILY_KERNEL = {
-    "conv3x3_fwd": "gemm_bf16_kernel<1, 0",
-    "conv3x3_dgrad": "gemm_bf16_kernel<2, ",   # <2, 0: against the transposed filter; <2, 5: read transposed
-    "conv3x3_wgrad": "gemm_bf16_kernel<3, 4",
-    "gemm_bf16_xwT": "gemm_bf16_kernel<0, 0",
-    "gemm_bf16_dyW": "gemm_bf16_kernel<0, 3",
-    "gemm_bf16_dyTx": "gemm_bf16_kernel<3, 3",
-    "splitk_reduce": "splitk_reduce",
     "fused_update": "fused_update",   # fused_update_kernel, or fused_update_partials_kernel where K-slice
-}                                     # partials of filter gradients are summed in the update
+    "attention": "attention_fwd_kernel",   # partials of filter gradients are summed in the update
+    "attention_bwd": "attention_bwd_kernel",
+    "lstm_step": "lstm_step_fwd_kernel",
+    "lstm_step_bwd": "lstm_step_bwd_kernel",
+    "layernorm_bwd": "layernorm_bwd",
+    "softmax_ce": "softmax_ce",
+}
+
+
+def kernel_prefix(family):
+    return family if "<" in family else FAMILY_KERNEL.get(family)
 
 
 def traffic_per_launch(workload, family):
-    """HBM bytes per launch of the family's kernels (the dispatch-weighted mean
-    when the family launches several instantiations, such as both tile
-    widths) from the committed counter summary of this workload, or None when
-    there is none or the kernel sources changed since the counters were taken."""
+    """HBM bytes per launch of the family's kernel from the committed counter
+    summary of this workload, or None when there is none or the kernel
+    sources changed since the counters were taken."""
     from paper_1809_02839_amd import profiling
     digest, table = profiling.read_traffic(os.path.join(ROOT, "profiles", f"stage_kernels_{workload}_hbm_traffic.md"),
                                            with_dispatches=True)
-    prefix = FAMILY_KERNEL.get(family)
+    prefix = kernel_prefix(family)
     if digest is None or prefix is None or digest != profiling.source_digest():
         return None
     hits = [v for k, v in table.items() if k.startswith(prefix)]
     n = sum(d for d, _ in hits)
     return round(sum(d * b for d, b in hits) / n) if n else None
+
+
+def family_roof(v, peak_mfma):
+    """(bound, achieved, peak, unit, roof_ms) of a family's summed launches."""
+    t_mfma = v["flops_total"] / (peak_mfma * 1e12) * 1e3
+    t_hbm = v["bytes_total"] / (PEAK_HBM_GBPS * 1e9) * 1e3
+    if v["flops_total"] > 0 and t_mfma >= t_hbm:
+        return "mfma", v["flops_total"] / (v["ms_total"] / 1e3) / 1e12, peak_mfma, "TFLOP/s", t_mfma
+    return "hbm", v["bytes_total"] / (v["ms_total"] / 1e3) / 1e9, PEAK_HBM_GBPS, "GB/s", t_hbm
 
 
 def log(*a):
@@ -299,9 +316,11 @@ def cpu_baseline_pipeline(specs, n_steps):
                       f"update each), float64 NumPy, {per_step:.2f} s per mini-batch", **extra, **host_info()}
 
 
-def cpu_baseline(spec, n_steps):
+def cpu_baseline(spec, n_steps, layers=0):
     """The oracle as it stands, timed on the host: n_steps (forward, backward,
-    update) of the same stage at full size."""
+    update) of the same stage at full size, median step time. With layers > 0
+    the timed stage holds that many of the workload's (identical) layers and
+    its step time is scaled by num_layers / layers."""
     import numpy as np
     import synth
     from oracle import method, stages
@@ -310,25 +329,33 @@ def cpu_baseline(spec, n_steps):
         cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:
         cores = os.cpu_count()
+    full_layers = spec.num_layers
+    if layers and layers < full_layers:
+        spec = dataclasses.replace(spec, num_layers=layers)
+    scale = full_layers / spec.num_layers
     k, N = spec.stage_index, spec.num_stages
     lr, gamma = float(np.float32(spec.lr)), float(np.float32(spec.momentum))
     W = synth.initial_params(spec).astype(np.float64)
     v = np.zeros_like(W)
     rnd = stages.weight_rounder(spec)
     sf, sb = method.staleness_versions(spec.policy, k, N)
-    t0 = time.perf_counter()
+    per = []
     for m in range(n_steps):
+        t0 = time.perf_counter()
         x = synth.stage_input(spec, m)
         dy = synth.upstream_grad(spec, m) if spec.head == "none" else None
         lab = synth.labels(spec, m) if spec.head == "ce" else None
         _, _, st = stages.forward(spec, stages.unpack(spec, rnd(method.predict(W, v, sf, lr))), x, lab)
         _, g = stages.backward(spec, stages.unpack(spec, rnd(method.predict(W, v, sb, lr))), st, dy)
         W, v = method.momentum_sgd_step(W, v, stages.pack(spec, g), lr, gamma)
-    dt = time.perf_counter() - t0
-    per_step = dt / n_steps
+        per.append((time.perf_counter() - t0) * scale)
+    per_step = float(np.median(per))
+    what = (f"{n_steps} full-size steps (forward, backward, update) of the same stage"
+            if scale == 1 else
+            f"{n_steps} full-size steps (forward, backward, update) of a stage of {spec.num_layers} of its "
+            f"{full_layers} identical layers, step time scaled by {scale:g}")
     return {"value": spec.batch / per_step, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{n_steps} full-size steps (forward, backward, update) of the same stage, "
-                      f"float64 NumPy, {per_step:.2f} s per step", **host_info()}
+            "sample": f"{what}; float64 NumPy, median {per_step:.2f} s per stage step", **host_info()}
 
 
 def main():
@@ -336,9 +363,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default="vgg_conv", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--workload", default="resnet_bottleneck", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--profile-steps", type=int, default=20)
-    ap.add_argument("--cpu-steps", type=int, default=8)
+    ap.add_argument("--cpu-steps", type=int, default=3,
+                    help="oracle steps timed for cpu_baseline (the median step is reported)")
+    ap.add_argument("--cpu-layers", type=int, default=0,
+                    help="time the oracle on a stage of this many of the workload's layers (identical "
+                         "blocks) and scale its step time to the whole stage (0: the whole stage; "
+                         "default 1 for the bottleneck stage, whose whole step takes the oracle ~30 s)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--policy", default="spectrain", choices=["spectrain", "vanilla", "stash"],
                     help="weight staleness treatment (Section 4.2): SpecTrain prediction (default), Vanilla "
@@ -466,40 +498,37 @@ def main():
             log(f"[bench]   fused_update cold     {u['ms_total'] / u['launches'] * 1e3:9.1f} us/launch  "
                 f"{upd_cold_gbps:.0f} GB/s (caches evicted before each update)")
     fam_ms = {k: v["ms_total"] / args.profile_steps for k, v in prof.items()}
-    for k, v in prof.items():
-        extra = ""
-        if v["flops_total"]:
-            extra = f"  {v['flops_total'] / v['ms_total'] / 1e9:.1f} TFLOP/s"
-        elif v["bytes_total"]:
-            extra = f"  {v['bytes_total'] / v['ms_total'] / 1e6:.0f} GB/s"
-        log(f"[bench]   {k:22s} {v['launches'] / args.profile_steps:5.1f}/step "
-            f"{v['ms_total'] / v['launches'] * 1e3:9.1f} us/launch {fam_ms[k] * 1e3:9.1f} us/step{extra}")
+    peak_mfma = PEAK_BF16_TFLOPS if spec.dtype == "bf16" else PEAK_FP32_TFLOPS
+    roofs = {k: family_roof(v, peak_mfma) for k, v in prof.items()}
+    for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms_total"]):
+        bound, ach, peak, unit, _ = roofs[k]
+        log(f"[bench]   {k:40s} {v['launches'] / args.profile_steps:5.1f}/step "
+            f"{v['ms_total'] / v['launches'] * 1e3:8.1f} us/launch {fam_ms[k] * 1e3:8.1f} us/step  "
+            f"{bound} {ach:8.1f} {unit} ({ach / peak:.3f})")
     dom = max(prof, key=lambda k: prof[k]["ms_total"])
     d = prof[dom]
-    peak_mfma = PEAK_BF16_TFLOPS if spec.dtype == "bf16" else PEAK_FP32_TFLOPS
-    if d["flops_total"] > 0:
-        achieved = d["flops_total"] / (d["ms_total"] / 1e3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak_mfma, "unit": "TFLOP/s",
-                "frac": round(achieved / peak_mfma, 4), "traffic": None}
-    else:
-        achieved = d["bytes_total"] / (d["ms_total"] / 1e3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None}
-    roof["traffic"] = traffic_per_launch(args.workload, dom)
-    roof["kernel"] = dom
-    roof["launches_per_step"] = d["launches"] / args.profile_steps
-    roof["us_per_launch"] = round(d["ms_total"] / d["launches"] * 1e3, 2)
+    bound, ach, peak, unit, _ = roofs[dom]
+    roof = {"bound": bound, "achieved": round(ach, 2), "peak": peak, "unit": unit, "frac": round(ach / peak, 4),
+            "traffic": traffic_per_launch(args.workload, dom), "kernel": dom,
+            "launches_per_step": d["launches"] / args.profile_steps,
+            "us_per_launch": round(d["ms_total"] / d["launches"] * 1e3, 2),
+            "algorithmic_bytes_per_launch": round(d["bytes_total"] / d["launches"]),
+            "algorithmic_flops_per_launch": round(d["flops_total"] / d["launches"])}
+    kernels = []
+    for k in sorted(prof, key=lambda k: -prof[k]["ms_total"])[:12]:
+        v = prof[k]
+        b, a, pk, u, _ = roofs[k]
+        kernels.append({"kernel": k, "launches_per_step": v["launches"] / args.profile_steps,
+                        "us_per_launch": round(v["ms_total"] / v["launches"] * 1e3, 2), "bound": b,
+                        "achieved": round(a, 1), "unit": u, "frac": round(a / pk, 4)})
     gemm_flops = sum(v["flops_total"] for v in prof.values())
     gemm_ms = sum(v["ms_total"] for k, v in prof.items() if v["flops_total"] > 0)
     upd = prof.get("fused_update")
     upd_gbps = upd["bytes_total"] / (upd["ms_total"] / 1e3) / 1e9 if upd else None
-    # Lower bound of the step: every contraction at the MFMA peak plus the
-    # update's algorithmic bytes at the HBM peak (other passes count as zero):
-    # W, v, g read and W, v written in float32, both predicted slots written
-    # in the operand dtype, once per stage per step.
-    esz = 2 if spec.dtype == "bf16" else 4
-    upd_bytes = float(sum(synth.num_params(sp) for sp in specs)) * (12 + 8 + 2 * esz)
-    bound_us = (gemm_flops / args.profile_steps / (peak_mfma * 1e12) + upd_bytes / (PEAK_HBM_GBPS * 1e9)) * 1e6
+    upd_extra = upd["extra_bytes_total"] / upd["launches"] if upd else None
+    # Lower bound of the step: every family at its roof (flops at the MFMA
+    # peak or algorithmic bytes at the HBM peak, whichever takes longer)
+    bound_us = sum(r[4] for r in roofs.values()) / args.profile_steps * 1e3
 
     cpu = None
     if not args.no_cpu:
@@ -507,7 +536,8 @@ def main():
         # whole pipelines: a quarter of the steps (each is N stage steps); the
         # small float32 pipeline: its full 20 mini-batches (well under a second)
         n_pipe = wl.steps if spec.dtype == "fp32" else max(1, args.cpu_steps // 4)
-        cpu = cpu_baseline_pipeline(specs, n_pipe) if pipeline else cpu_baseline(spec, args.cpu_steps)
+        layers = args.cpu_layers or (1 if args.workload == "resnet_bottleneck" else 0)
+        cpu = cpu_baseline_pipeline(specs, n_pipe) if pipeline else cpu_baseline(spec, args.cpu_steps, layers)
         log(f"[bench] oracle: {cpu['value']:.2f} samples/s on {cpu['cores']} threads")
 
     out = {
@@ -535,9 +565,12 @@ def main():
         "predict_update_GBps": round(upd_gbps, 1) if upd_gbps else None,
         "predict_update_frac_hbm": round(upd_gbps / PEAK_HBM_GBPS, 4) if upd_gbps else None,
         "predict_update_GBps_cold": round(upd_cold_gbps, 1) if upd_cold_gbps else None,
+        "predict_update_us": round(upd["ms_total"] / upd["launches"] * 1e3, 2) if upd else None,
+        "predict_update_extra_bytes_per_launch": round(upd_extra) if upd else None,
         "step_bound_us": round(bound_us, 2),
         "step_roofline_frac": round(bound_us / (ms_step * 1e3), 4),
         "roofline": roof,
+        "kernels": kernels,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define SPECTRAIN_ABI_VERSION 2u
+#define SPECTRAIN_ABI_VERSION 3u
 
 /* Status codes. */
 enum {
@@ -140,8 +140,13 @@ int spectrain_stage_num_params(spectrain_stage_t st, size_t* n);
  * s < 0 or a bad slot. */
 int spectrain_stage_predict(spectrain_stage_t st, int32_t s, int32_t slot);
 
-/* Forward pass of mini-batch mb_id against slot 0 (with STASH, slot 0 is also
- * copied into the mini-batch's weight stash). x_dev: input activations.
+/* Forward pass of mini-batch mb_id against slot 0, the weights predicted with
+ * the forward version difference (Section 3.2: a pass runs on the weights
+ * predicted for the time its mini-batch completes its round trip, Eq. 4 with
+ * Eq. 5); with STASH, slot 0 is also copied into the mini-batch's weight
+ * stash. The activations the backward pass needs are kept in the stage's
+ * stash until then (Section 3.1: up to N - k mini-batches are in flight at
+ * stage k). x_dev: input activations.
  * y_dev: output activations (HEAD_NONE; NULL with a CE head). labels_dev and
  * loss_dev (one float32, the mean CE) are used with a CE head only. The stage
  * keeps references to x_dev and y_dev until the matching backward returns:
@@ -150,8 +155,11 @@ int spectrain_stage_predict(spectrain_stage_t st, int32_t s, int32_t slot);
 int spectrain_stage_forward(spectrain_stage_t st, int64_t mb_id, const void* x_dev, void* y_dev,
                             const int32_t* labels_dev, float* loss_dev);
 
-/* Backward pass of mini-batch mb_id against slot 1 (PREDICT) or the weights
- * its forward used (STASH) for dX, and the stashed activations (g). dy_dev: dL/dY (HEAD_NONE; ignored with a CE head).
+/* Backward pass of mini-batch mb_id against slot 1 (PREDICT: the weights
+ * predicted with the backward version difference, Eq. 4 with Eq. 6, Section
+ * 3.2) or the weights its forward used (STASH) for dX, and the stashed
+ * activations for g (one gradient per backward, which the next update
+ * applies, Section 3.1). dy_dev: dL/dY (HEAD_NONE; ignored with a CE head).
  * dx_dev: dL/dX output, or NULL to skip it (e.g. at k = 0). Overwrites g with
  * this mini-batch's gradient and frees its stash slot. ESTATE when mb_id is
  * not in flight or a previous gradient is still waiting for its update. */
@@ -182,14 +190,23 @@ int spectrain_stage_get_predicted(spectrain_stage_t st, int32_t slot, float* Wha
  * recorded around every launch on the stage's stream (which serialises the
  * launches: use a separate pass, not the timed one). flops and bytes are the
  * algorithmic work of the launches: 2*M*N*K per GEMM (3x3 convolutions count
- * all 9 taps), and for the fused update 12 bytes read plus 8 + 2*sizeof(operand)
- * written per parameter. */
+ * all 9 taps); for a GEMM each operand tensor read once (a convolution's
+ * feature map once, not once per tap), each output written once and each
+ * epilogue operand (bias, residual, ReLU mask) read once; for the fused
+ * update 12 bytes read plus 8 + 2*sizeof(operand) written per parameter
+ * (24 bytes for bf16 stages); one read of each input and one write of each
+ * output for the elementwise and row passes. extra_bytes_total counts what a
+ * launch moves beyond that by construction: the float32 K-slice partials of
+ * a split GEMM, and the partial planes the update reads in place of g. */
 typedef struct {
-  char name[48];        /* kernel family, e.g. "conv3x3_fwd", "fused_update" */
+  char name[48];        /* kernel family: the kernel's name with its template arguments as a profiler
+                           lists it (e.g. "gemm_bf16_kernel<0, 3, false, 128, 1>"), or a pass name
+                           such as "fused_update", "layernorm_bwd", "lstm_step" */
   int64_t launches;
   double ms_total;      /* summed event-to-event duration */
   double flops_total;   /* algorithmic floating-point operations (0 if not a contraction) */
   double bytes_total;   /* algorithmic HBM bytes (0 if not counted) */
+  double extra_bytes_total;   /* bytes beyond the algorithmic ones (split-K partial planes) */
 } spectrain_kernel_stat;
 
 /* enable != 0: clear the statistics and time every following launch;
@@ -200,6 +217,34 @@ int spectrain_stage_profile(spectrain_stage_t st, int32_t enable);
  * store the number of families in *count. Synchronises the stream. */
 int spectrain_stage_profile_read(spectrain_stage_t st, spectrain_kernel_stat* out, int32_t capacity,
                                  int32_t* count);
+
+/* Copy activation buffer `index` that the forward pass of mini-batch mb_id
+ * stored for its backward pass (the stash of Section 3.1, one per mini-batch
+ * in flight) to host_out, for inspection and testing. *size receives the
+ * buffer's size in bytes (0: the index is unused by this stage); with
+ * host_out NULL nothing is copied. EINVAL for an index outside the kind's
+ * list or a capacity below the size; ESTATE when mb_id is not in flight.
+ * Synchronises the stream. Buffers are row-major in the activation layouts
+ * above, in the compute dtype unless marked f32; P = B*H*W pixels, T = B*S
+ * tokens (transformer) or T*B steps x rows (LSTM):
+ *   FC          l-1: output of layer l-1 [B, hidden] (l = 1 .. L-1);
+ *               L-1 with a CE head: dlogits [B, classes]
+ *   CONV3X3     l-1: output of layer l-1 [P, C_out] (l = 1 .. L-1); with a CE head
+ *               L-1: last output, L: pooled [B, C_out] (bf16), L+1: dlogits [B, classes] (bf16)
+ *   BOTTLENECK  3l: t1 [P, C_mid], 3l+1: t2 [P, C_mid], 3l+2: block output [P, C]
+ *               (l < L-1, or every block with a CE head); 3L: pooled [B, C], 3L+1: dlogits
+ *   TRANSFORMER 13l+j: 0 qkv [T, 3d], 1 softmax row statistics (max, 1/sum) f32 [B*heads*S, 2]
+ *               (sequence 128, head dimension 64) or probabilities f32 [B*heads, S, S],
+ *               2 probabilities bf16 (the second form only), 3 ctx [T, d], 4 r1 = x + attention
+ *               output [T, d], 5 mean of r1 f32 [T], 6 1/std of r1 f32 [T], 7 h = LN1(r1) [T, d],
+ *               8 ReLU(FFN1) [T, F], 9 r2 = h + FFN2 [T, d], 10 mean of r2 f32, 11 1/std of r2 f32,
+ *               12 layer output [T, d] (l < L-1, or every layer with a CE head);
+ *               13L with a CE head: dlogits [T, V]
+ *   RESLSTM     4l+j: 0 activated gates (i, f, g, o) f32 [T, B, 4H], 1 cell state c f32 [T, B, H],
+ *               2 h [T, B, H], 3 layer output [T, B, H] (l < L-1, or every layer with a CE head);
+ *               4L with a CE head: dlogits [T*B, V] */
+int spectrain_stage_read_stash(spectrain_stage_t st, int64_t mb_id, int32_t index, void* host_out, size_t capacity,
+                               size_t* size);
 
 /* Release every device buffer of the stage. Synchronises the stream.
  * Passing NULL returns EINVAL. */

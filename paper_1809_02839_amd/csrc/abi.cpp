@@ -104,6 +104,12 @@ int spectrain_stage_get_predicted(spectrain_stage_t st, int32_t slot, float* Wha
   return guarded(st, [&](spx::Stage& x) { x.get_predicted(slot, What_host); }, false);
 }
 
+int spectrain_stage_read_stash(spectrain_stage_t st, int64_t mb_id, int32_t index, void* host_out, size_t capacity,
+                               size_t* size) {
+  if (!size) return set_error(SPECTRAIN_EINVAL, "size is NULL");
+  return guarded(st, [&](spx::Stage& x) { *size = x.read_stash(mb_id, index, host_out, capacity); }, false);
+}
+
 int spectrain_stage_profile(spectrain_stage_t st, int32_t enable) {
   return guarded(st, [&](spx::Stage& x) { x.profile(enable != 0); }, false);
 }

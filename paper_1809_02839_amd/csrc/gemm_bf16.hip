@@ -22,6 +22,7 @@
 // partials in a fixed order and applies the epilogue, so results do not
 // depend on timing.
 #include <algorithm>
+#include <cstdio>
 
 #include "kernels.hpp"
 
@@ -813,6 +814,29 @@ hipError_t launch_reduce(const KArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+const char* gemm_bf16_kernel_name(const GemmDesc& d) {
+  KArgs a;
+  hipError_t err;
+  if (!plan(d, a, err)) return "gemm_bf16_kernel";
+  const int ma = d.A.mode, mb = d.B.mode;
+  bool tapk = false;
+  if (ma == OP_K_CONV_FWD || (ma == OP_K_CONV_DGRAD && mb == OP_K_PLAIN)) tapk = d.A.g.C % BK == 0;
+  if (ma == OP_K_CONV_DGRAD && mb == OP_R_FILTER_T) tapk = d.A.g.C % BK == 0 && d.B.g.C2 % BK == 0;
+  // the kernel's template arguments as a profiler prints the instantiation
+  static thread_local char buf[64];
+  std::snprintf(buf, sizeof(buf), "gemm_bf16_kernel<%d, %d, %s, %d, %d>", ma, mb, tapk ? "true" : "false",
+                a.bn == 64 ? 64 : 128, a.bn == 64 ? 1 : a.ksl);
+  return buf;
+}
+
+const char* gemm_bf16_reduce_name(const GemmDesc& d) {
+  KArgs a;
+  hipError_t err;
+  if (!plan(d, a, err)) return "splitk_reduce_kernel";
+  if (a.N % 4) return "splitk_reduce_kernel";
+  return a.vec_epi ? "splitk_reduce4_kernel<true>" : "splitk_reduce4_kernel<false>";
+}
 
 int gemm_bf16_split_rule(int M, int N, int K, int batch, size_t workspace_bytes) {
   if (M <= 0 || N <= 0 || K <= 0 || batch <= 0) return 1;

@@ -6,6 +6,7 @@
 // over blocks (each block's K loop stays short) and a second pass sums the
 // partials in split order and applies the epilogue.
 #include <algorithm>
+#include <cstdio>
 
 #include "kernels.hpp"
 
@@ -133,6 +134,12 @@ hipError_t launch(const F32Args& a, hipStream_t s) {
 }
 
 }  // namespace
+
+const char* gemm_f32_kernel_name(const GemmDesc& d) {
+  static thread_local char buf[48];
+  std::snprintf(buf, sizeof(buf), "gemm_f32_kernel<%d, %d>", d.A.mode, d.B.mode);
+  return buf;
+}
 
 hipError_t gemm_f32(const GemmDesc& d, hipStream_t s) {
   if (d.M <= 0 || d.N <= 0) return hipSuccess;

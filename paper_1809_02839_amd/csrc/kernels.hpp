@@ -69,6 +69,12 @@ int gemm_bf16_splits(const GemmDesc& d);   // K splits the launch will use (1 = 
 // The same count from the shape alone, for a workspace of workspace_bytes.
 int gemm_bf16_split_rule(int M, int N, int K, int batch, size_t workspace_bytes);
 hipError_t gemm_f32(const GemmDesc& d, hipStream_t s);
+// Names of the kernels a launch runs, as a profiler lists the instantiations
+// (e.g. "gemm_bf16_kernel<0, 3, false, 128, 1>"); the returned buffer is
+// thread-local and valid until the next call on the thread.
+const char* gemm_bf16_kernel_name(const GemmDesc& d);
+const char* gemm_bf16_reduce_name(const GemmDesc& d);
+const char* gemm_f32_kernel_name(const GemmDesc& d);
 
 // Global average pool of an NHWC bf16 tensor [B, HW, C] -> [B, C] (bf16 of the
 // float32 mean), and its backward through the ReLU of the pooled tensor y:

@@ -93,6 +93,13 @@ GemmDesc gd(int M, int N, int K, const Operand& A, const Operand& B, long ldc) {
 
 void fail(const std::string& m) { throw StageError(SPECTRAIN_EINVAL, m); }
 
+// Algorithmic bytes of the elementwise and row passes (one read of each
+// input, one write of each output).
+double ce_bytes(double R, double C) { return R * C * (4.0 + 2.0) + R * 8.0; }   // scores, gradient, label, loss
+double colsum_bytes(double R, double C, double esz) { return R * C * esz + C * 4.0; }
+double ln_bytes(double R, double D) { return R * D * 4.0 + R * 8.0 + D * 4.0; }  // r in, y out (bf16), stats
+double lnb_bytes(double R, double D) { return R * D * 6.0 + R * 8.0 + D * 14.0; }  // dy, r in, dr out; 3 sums
+
 }  // namespace
 
 // ----------------------------------------------------------------- layout ----
@@ -169,22 +176,42 @@ void Stage::build_layout() {
 const void* Stage::wf(int i) const { return static_cast<const char*>(what_[0]) + tensors_[i].off * esz_; }
 const void* Stage::wb(int i) const { return static_cast<const char*>(bwd_weights_) + tensors_[i].off * esz_; }
 
+// Algorithmic HBM bytes of one GEMM launch: each operand tensor read once
+// (a convolution gather reads its feature map once, not once per tap), the
+// outputs written once (read too when accumulating), and every epilogue
+// operand (bias, residual, mask) read once. Split-K partials are not counted:
+// they are traffic of the implementation, not of the product.
+double gemm_algorithmic_bytes(const GemmDesc& d, size_t esz) {
+  auto operand = [&](const Operand& o, long rows) -> double {
+    switch (o.mode) {
+      case OP_K_PLAIN:
+      case OP_R_PLAIN: return static_cast<double>(rows) * d.K * esz;
+      case OP_R_FILTER_T: return 9.0 * o.g.C * o.g.C2 * esz;
+      default: return static_cast<double>(o.g.B) * o.g.H * o.g.W * o.g.C * esz;
+    }
+  };
+  const Epilogue& e = d.epi;
+  double per_out = 0.0;
+  if (e.out_f32) per_out += e.accumulate ? 8.0 : 4.0;
+  if (e.out_bf16) per_out += 2.0;
+  if (e.res_f32) per_out += 4.0;
+  if (e.res_bf16) per_out += 2.0;
+  if (e.mask) per_out += static_cast<double>(esz);
+  double b = operand(d.A, d.M) + operand(d.B, d.N) + static_cast<double>(d.M) * d.N * per_out;
+  if (e.bias) b += 4.0 * d.N;
+  else if (e.bias_bf16) b += 2.0 * d.N;
+  return b * d.batch;
+}
+
 void Stage::gemm(const GemmDesc& d, bool defer) {
-  const char* name = "gemm";
-  const int ma = d.A.mode, mb = d.B.mode;
-  if (ma == OP_K_CONV_FWD) name = "conv3x3_fwd";
-  else if (ma == OP_K_CONV_DGRAD) name = "conv3x3_dgrad";
-  else if (mb == OP_R_CONV_WGRAD) name = "conv3x3_wgrad";
-  else if (d.batch > 1) name = dt_ ? "gemm_bf16_batched" : "gemm_f32_batched";
-  else if (ma == OP_K_PLAIN && mb == OP_K_PLAIN) name = dt_ ? "gemm_bf16_xwT" : "gemm_f32_xwT";
-  else if (ma == OP_K_PLAIN && mb == OP_R_PLAIN) name = dt_ ? "gemm_bf16_dyW" : "gemm_f32_dyW";
-  else if (ma == OP_R_PLAIN && mb == OP_R_PLAIN) name = dt_ ? "gemm_bf16_dyTx" : "gemm_f32_dyTx";
+  // launch families are the kernel instantiations, as a profiler names them
   const double flops = 2.0 * d.M * d.N * static_cast<double>(d.K) * d.batch;
+  const double bytes = gemm_algorithmic_bytes(d, esz_);
   GemmDesc dd = d;
   dd.workspace = ws<float>(static_cast<int>(ws_off_.size()) - 1);
   dd.workspace_bytes = gemm_ws_bytes_;
   if (!dt_) {
-    LAUNCH(name, flops, 0, gemm_f32(dd, s_));
+    LAUNCH(gemm_f32_kernel_name(dd), flops, bytes, gemm_f32(dd, s_));
     return;
   }
   if (defer) {
@@ -198,7 +225,8 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
         defer_used_ + splits * mn <= defer_cap_ && defer_segs_.size() < static_cast<size_t>(UPDATE_MAX_SEGMENTS)) {
       dd.workspace = defer_ + defer_used_;
       dd.workspace_bytes = static_cast<size_t>(splits * mn) * 4;
-      LAUNCH(name, flops, 0, gemm_bf16(dd, s_, GEMM_MAIN));
+      // the partial planes replace the g write: splits - 1 planes more
+      LAUNCH_X(gemm_bf16_kernel_name(dd), flops, bytes, 4.0 * (splits - 1) * mn, gemm_bf16(dd, s_, GEMM_MAIN));
       UpdateSegment sg;
       sg.off = off;
       sg.n = mn;
@@ -209,14 +237,17 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
       return;
     }
   }
-  LAUNCH(name, flops, 0, gemm_bf16(dd, s_, GEMM_MAIN));
   const int splits = gemm_bf16_splits(dd);
+  const double mn = static_cast<double>(d.M) * d.N * d.batch;
+  // with a K split the GEMM writes float32 partial planes instead of the output
+  LAUNCH_X(gemm_bf16_kernel_name(dd), flops, bytes, splits > 1 ? 4.0 * splits * mn : 0.0,
+           gemm_bf16(dd, s_, GEMM_MAIN));
   if (splits > 1) {
-    // partials read once, output written once (read too when accumulating)
-    const double mn = static_cast<double>(d.M) * d.N * d.batch;
+    // the reduction's own traffic: partials read once, output written once
+    // (read too when accumulating), epilogue operands read once
     const double out = d.epi.out_f32 ? 4.0 : 2.0;
-    const double bytes = mn * (4.0 * splits + out * (d.epi.accumulate ? 2 : 1));
-    LAUNCH("splitk_reduce", 0, bytes, gemm_bf16(dd, s_, GEMM_REDUCE));
+    const double rbytes = mn * (4.0 * splits + out * (d.epi.accumulate ? 2 : 1));
+    LAUNCH(gemm_bf16_reduce_name(dd), 0, rbytes, gemm_bf16(dd, s_, GEMM_REDUCE));
   }
 }
 
@@ -241,6 +272,7 @@ void Stage::prof_collect() {
     k.ms_total += ms;
     k.flops_total += r.flops;
     k.bytes_total += r.bytes;
+    k.extra_bytes_total += r.extra;
   }
   prof_recs_.clear();
   prof_used_ = 0;
@@ -375,6 +407,7 @@ void Stage::plan_buffers() {
     defer_ = defer_block_.at<float>(o);
   }
   DeviceBlock probe;
+  stash_bytes_ = st;
   for (size_t b : st) stash_off_.push_back(probe.add(std::max<size_t>(b, 1)));
   for (size_t b : ws) ws_off_.push_back(ws_block_.add(std::max<size_t>(b, 1)));
   const int nslots = d_.num_stages - d_.stage_index;
@@ -554,6 +587,21 @@ void Stage::get_predicted(int slot, float* out) {
   }
 }
 
+size_t Stage::read_stash(int64_t mb, int index, void* host, size_t capacity) {
+  int slot = -1;
+  for (size_t i = 0; i < slots_.size(); ++i)
+    if (slots_[i].used && slots_[i].mb == mb) slot = static_cast<int>(i);
+  if (slot < 0) throw StageError(SPECTRAIN_ESTATE, "mini-batch is not in flight");
+  if (index < 0 || static_cast<size_t>(index) >= stash_bytes_.size()) fail("stash index outside the stage's list");
+  const size_t n = stash_bytes_[index];
+  if (n == 0 || !host) return n;
+  if (capacity < n) fail("host buffer of " + std::to_string(capacity) + " bytes is smaller than the stash buffer (" +
+                         std::to_string(n) + " bytes)");
+  sync();
+  hip_check(hipMemcpy(host, slot_blocks_[slot].at<char>(stash_off_[index]), n, hipMemcpyDeviceToHost), "copy stash");
+  return n;
+}
+
 // --------------------------------------------------- predict and update ----
 void Stage::predict(int s, int slot) {
   if (s < 0) fail("version difference must be >= 0");
@@ -563,17 +611,20 @@ void Stage::predict(int s, int slot) {
 
 void Stage::update(int s_f, int s_b) {
   if (!g_pending_) throw StageError(SPECTRAIN_ESTATE, "update without a gradient from a backward pass");
-  double bytes = static_cast<double>(n_params_) * (12 + 8 + (s_f >= 0) * esz_ + (s_b >= 0) * esz_);
+  // algorithmic: W, v, g read and W, v written (float32), each refreshed slot
+  // written in the operand dtype
+  const double bytes = static_cast<double>(n_params_) * (12 + 8 + (s_f >= 0) * esz_ + (s_b >= 0) * esz_);
   if (defer_segs_.empty()) {
     LAUNCH("fused_update", 0, bytes,
            fused_update(W_, v_, g_, what_[0], what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_.dev(), s_));
   } else {
     std::sort(defer_segs_.begin(), defer_segs_.end(),
               [](const UpdateSegment& a, const UpdateSegment& b) { return a.off < b.off; });
-    for (const UpdateSegment& sg : defer_segs_) bytes += 4.0 * (sg.splits - 1) * sg.n;   // planes instead of g
-    LAUNCH("fused_update", 0, bytes,
-           fused_update_partials(W_, v_, g_, defer_segs_.data(), static_cast<int>(defer_segs_.size()), what_[0],
-                                 what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_.dev(), s_));
+    double extra = 0.0;   // the partial planes read in place of g: splits - 1 planes more
+    for (const UpdateSegment& sg : defer_segs_) extra += 4.0 * (sg.splits - 1) * sg.n;
+    LAUNCH_X("fused_update", 0, bytes, extra,
+             fused_update_partials(W_, v_, g_, defer_segs_.data(), static_cast<int>(defer_segs_.size()), what_[0],
+                                   what_[1], dt_, n_arena_, d_.lr, d_.momentum, s_f, s_b, flag_.dev(), s_));
   }
   defer_segs_.clear();
   defer_used_ = 0;
@@ -653,7 +704,8 @@ void Stage::fwd_fc(int slot, const void* x, void* y, const int32_t* labels, floa
     a = out;
   }
   if (ce)
-    LAUNCH("softmax_ce", 0, 0, softmax_ce(ws<float>(0), labels, B, d_.dims[1], stash<void>(slot, L - 1), dt_, loss, ws<float>(3), s_));
+    LAUNCH("softmax_ce", 0, ce_bytes(B, d_.dims[1]),
+           softmax_ce(ws<float>(0), labels, B, d_.dims[1], stash<void>(slot, L - 1), dt_, loss, ws<float>(3), s_));
 }
 
 void Stage::bwd_fc(int slot, const void* dy, void* dx) {
@@ -665,7 +717,8 @@ void Stage::bwd_fc(int slot, const void* dy, void* dx) {
   if (d_.head == SPECTRAIN_HEAD_CE) {
     dz = stash<void>(slot, L - 1);
   } else {
-    LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(1), static_cast<long>(B) * d_.dims[1], dt_, s_));
+    LAUNCH("mask", 0, 3.0 * esz_ * B * d_.dims[1],
+           mask_relu_grad(dy, sl.y, ws<void>(1), static_cast<long>(B) * d_.dims[1], dt_, s_));
     dz = ws<void>(1);
   }
   int pp = 2;
@@ -674,7 +727,7 @@ void Stage::bwd_fc(int slot, const void* dy, void* dx) {
     GemmDesc gw = gd(fout, fin, B, opR(dz, fout), opR(act(l), fin), fin);
     gw.epi.out_f32 = grad(2 * l);
     gemm(gw);
-    LAUNCH("bias_grad", 0, 0, column_sum(dz, dt_, B, fout, fout, grad(2 * l + 1), 0, ws<float>(4), s_));
+    LAUNCH("bias_grad", 0, colsum_bytes(B, fout, esz_), column_sum(dz, dt_, B, fout, fout, grad(2 * l + 1), 0, ws<float>(4), s_));
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
     GemmDesc gx = gd(B, fin, fout, opK(dz, fout), opR(wb(2 * l), fin), fin);
@@ -725,7 +778,7 @@ void Stage::pool_head_fwd(int slot, const void* yl, int HW, int C, int t, int id
   g.epi.bias_bf16 = static_cast<const bf16_t*>(wf(t + 1));
   g.epi.out_f32 = ws<float>(wsl);
   gemm(g);
-  LAUNCH("softmax_ce", 0, 0, softmax_ce(ws<float>(wsl), labels, B, V, stash<void>(slot, id_dl), 1, loss,
+  LAUNCH("softmax_ce", 0, ce_bytes(B, V), softmax_ce(ws<float>(wsl), labels, B, V, stash<void>(slot, id_dl), 1, loss,
                                         ws<float>(wsl + 1), s_));
 }
 
@@ -736,7 +789,7 @@ void Stage::pool_head_bwd(int slot, const void* yl, int HW, int C, int t, int id
   GemmDesc gw = gd(V, C, B, opR(dl, V), opR(pooled, C), C);
   gw.epi.out_f32 = grad(t);
   gemm(gw);
-  LAUNCH("bias_grad", 0, 0,
+  LAUNCH("bias_grad", 0, colsum_bytes(B, V, 2),
          column_sum(dl, 1, B, V, V, grad(t + 1), 0, ws<float>(static_cast<int>(ws_off_.size()) - 2), s_));
   bf16_t* dpool = ws<bf16_t>(wsl + 2);
   GemmDesc gx = gd(B, C, V, opK(dl, V), opR(wb(t), C), C);
@@ -754,7 +807,7 @@ void Stage::bwd_conv(int slot, const void* dy, void* dx) {
   if (d_.head == SPECTRAIN_HEAD_CE)
     pool_head_bwd(slot, stash<void>(slot, L - 1), H * W, Cout, L, L, L + 1, 2, ws<void>(0));
   else
-    LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * Cout, 1, s_));
+    LAUNCH("mask", 0, 6.0 * P * Cout, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * Cout, 1, s_));
   const void* dz = ws<void>(0);
   // the data gradients read each filter transposed ([C][9][C_out], k
   // contiguous), made for every layer that needs one in launches of up to
@@ -840,7 +893,7 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
   if (d_.head == SPECTRAIN_HEAD_CE)
     pool_head_bwd(slot, stash<void>(slot, 3 * (L - 1) + 2), H * W, C, 3 * L, 3 * L, 3 * L + 1, 4, ws<void>(0));
   else
-    LAUNCH("mask", 0, 0, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * C, 1, s_));
+    LAUNCH("mask", 0, 6.0 * P * C, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * C, 1, s_));
   int cur = 0;
   bf16_t* dt2 = ws<bf16_t>(2);
   bf16_t* dt1 = ws<bf16_t>(3);
@@ -906,7 +959,8 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     g.epi.out_bf16 = qkv;
     gemm(g);
     if (attention_fused_supported(S, dh, d)) {
-      LAUNCH("attention", 4.0 * B * Hh * S * S * dh, 0, attention_fwd(qkv, B, Hh, d, scale, P, ctx, s_));
+      LAUNCH("attention", 4.0 * B * Hh * S * S * dh, 2.0 * T * 4 * d + 8.0 * B * Hh * S,
+             attention_fwd(qkv, B, Hh, d, scale, P, ctx, s_));
     } else {
     // scores[b, h] = Q K^T * scale
     Operand qa = opK(qkv, 3 * d), kb = opK(qkv + d, 3 * d);
@@ -920,7 +974,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     sc.epi.alpha = scale;
     sc.epi.out_f32 = ws<float>(0);
     gemm(sc);
-    LAUNCH("softmax", 0, 0, softmax_rows(ws<float>(0), B * Hh * S, S, P, Pb, s_));
+    LAUNCH("softmax", 0, 10.0 * B * Hh * S * S, softmax_rows(ws<float>(0), B * Hh * S, S, P, Pb, s_));
     // ctx[b, :, h] = P V
     Operand pa = opK(Pb, S), vb = opR(qkv + 2 * d, 3 * d);
     pa.bs1 = static_cast<long>(Hh) * S * S;
@@ -940,7 +994,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     go.epi.res_bf16 = static_cast<const bf16_t*>(a);
     go.epi.out_bf16 = r1;
     gemm(go);
-    LAUNCH("layernorm", 0, 0, layernorm_fwd(r1, static_cast<const bf16_t*>(wf(p + 4)), static_cast<const bf16_t*>(wf(p + 5)), T, d,
+    LAUNCH("layernorm", 0, ln_bytes(T, d), layernorm_fwd(r1, static_cast<const bf16_t*>(wf(p + 4)), static_cast<const bf16_t*>(wf(p + 5)), T, d,
                             LN_EPS, h, stash<float>(slot, q + 5), stash<float>(slot, q + 6), s_));
     GemmDesc g1 = gd(T, F, d, opK(h, d), opK(wf(p + 6), d), F);
     g1.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 7));
@@ -952,7 +1006,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     g2.epi.res_bf16 = h;
     g2.epi.out_bf16 = r2;
     gemm(g2);
-    LAUNCH("layernorm", 0, 0, layernorm_fwd(r2, static_cast<const bf16_t*>(wf(p + 10)), static_cast<const bf16_t*>(wf(p + 11)), T, d,
+    LAUNCH("layernorm", 0, ln_bytes(T, d), layernorm_fwd(r2, static_cast<const bf16_t*>(wf(p + 10)), static_cast<const bf16_t*>(wf(p + 11)), T, d,
                             LN_EPS, static_cast<bf16_t*>(out), stash<float>(slot, q + 10), stash<float>(slot, q + 11),
                             s_));
     a = out;
@@ -963,7 +1017,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     gv.epi.bias_bf16 = static_cast<const bf16_t*>(wf(12 * L + 1));
     gv.epi.out_f32 = ws<float>(10);
     gemm(gv);
-    LAUNCH("softmax_ce", 0, 0, softmax_ce(ws<float>(10), labels, T, V, stash<void>(slot, 13 * L), 1, loss,
+    LAUNCH("softmax_ce", 0, ce_bytes(T, V), softmax_ce(ws<float>(10), labels, T, V, stash<void>(slot, 13 * L), 1, loss,
                                           ws<float>(11), s_));
   }
 }
@@ -986,7 +1040,7 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     GemmDesc gw = gd(V, d, T, opR(dl, V), opR(yL, d), d);
     gw.epi.out_f32 = grad(12 * L);
     gemm(gw);
-    LAUNCH("bias_grad", 0, 0, column_sum(dl, 1, T, V, V, grad(12 * L + 1), 0, part, s_));
+    LAUNCH("bias_grad", 0, colsum_bytes(T, V, 2), column_sum(dl, 1, T, V, V, grad(12 * L + 1), 0, part, s_));
     GemmDesc gx = gd(T, d, V, opK(dl, V), opR(wb(12 * L), d), d);
     gx.epi.out_bf16 = ws<bf16_t>(2);
     gemm(gx);
@@ -1011,7 +1065,7 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     bf16_t* dctx = ws<bf16_t>(8);
     bf16_t* dqkv = ws<bf16_t>(9);
 
-    LAUNCH("layernorm_bwd", 0, 0, layernorm_bwd(static_cast<const bf16_t*>(gy), r2, stash<float>(slot, q + 10), stash<float>(slot, q + 11),
+    LAUNCH("layernorm_bwd", 0, lnb_bytes(T, d), layernorm_bwd(static_cast<const bf16_t*>(gy), r2, stash<float>(slot, q + 10), stash<float>(slot, q + 11),
                             static_cast<const bf16_t*>(wb(p + 10)), T, d, dr2, grad(p + 10), grad(p + 11), grad(p + 9),
                             part, s_));   // also the FFN output bias gradient: column sums of dr2
     GemmDesc w2 = gd(d, F, T, opR(dr2, d), opR(f1, F), F);
@@ -1024,12 +1078,12 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     GemmDesc w1 = gd(F, d, T, opR(df1, F), opR(h, d), d);
     w1.epi.out_f32 = grad(p + 6);
     gemm(w1);
-    LAUNCH("bias_grad", 0, 0, column_sum(df1, 1, T, F, F, grad(p + 7), 0, part, s_));
+    LAUNCH("bias_grad", 0, colsum_bytes(T, F, 2), column_sum(df1, 1, T, F, F, grad(p + 7), 0, part, s_));
     GemmDesc x1 = gd(T, d, F, opK(df1, F), opR(wb(p + 6), d), d);
     x1.epi.res_bf16 = dr2;
     x1.epi.out_bf16 = dhh;
     gemm(x1);
-    LAUNCH("layernorm_bwd", 0, 0, layernorm_bwd(dhh, r1, stash<float>(slot, q + 5), stash<float>(slot, q + 6),
+    LAUNCH("layernorm_bwd", 0, lnb_bytes(T, d), layernorm_bwd(dhh, r1, stash<float>(slot, q + 5), stash<float>(slot, q + 6),
                             static_cast<const bf16_t*>(wb(p + 4)), T, d, dr1, grad(p + 4), grad(p + 5), grad(p + 3),
                             part, s_));   // also the attention output bias gradient: column sums of dr1
     GemmDesc wo = gd(d, d, T, opR(dr1, d), opR(ctx, d), d);
@@ -1041,7 +1095,8 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
 
     // attention backward: fused, or batched GEMMs over (b, h)
     if (attention_fused_supported(S, dh, d)) {
-      LAUNCH("attention_bwd", 10.0 * B * Hh * S * S * dh, 0, attention_bwd(qkv, dctx, P, B, Hh, d, scale, dqkv, s_));
+      LAUNCH("attention_bwd", 10.0 * B * Hh * S * S * dh, 2.0 * T * 7 * d + 8.0 * B * Hh * S,
+             attention_bwd(qkv, dctx, P, B, Hh, d, scale, dqkv, s_));
     } else {
     const long sS = static_cast<long>(S) * S, sHSS = static_cast<long>(Hh) * S * S;
     const long sQ = static_cast<long>(S) * 3 * d, sO = static_cast<long>(S) * d;
@@ -1073,7 +1128,7 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
       g.epi.out_f32 = ws<float>(0);
       gemm(g);
     }
-    LAUNCH("softmax_bwd", 0, 0, softmax_bwd(P, ws<float>(0), B * Hh * S, S, ws<bf16_t>(1), s_));
+    LAUNCH("softmax_bwd", 0, 10.0 * B * Hh * S * S, softmax_bwd(P, ws<float>(0), B * Hh * S, S, ws<bf16_t>(1), s_));
     {  // dQ = dS K * scale
       Operand A = opK(ws<bf16_t>(1), S), Bk = opR(qkv + d, 3 * d);
       A.bs1 = sHSS;
@@ -1108,7 +1163,7 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     GemmDesc wq = gd(3 * d, d, T, opR(dqkv, 3 * d), opR(a, d), d);
     wq.epi.out_f32 = grad(p);
     gemm(wq);
-    LAUNCH("bias_grad", 0, 0, column_sum(dqkv, 1, T, 3 * d, 3 * d, grad(p + 1), 0, part, s_));
+    LAUNCH("bias_grad", 0, colsum_bytes(T, 3 * d, 2), column_sum(dqkv, 1, T, 3 * d, 3 * d, grad(p + 1), 0, part, s_));
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
     GemmDesc xq = gd(T, d, 3 * d, opK(dqkv, 3 * d), opR(wb(p), d), d);
@@ -1147,7 +1202,7 @@ void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, fl
     const bool fused = lstm_step_supported(B, H);
     for (int t = 0; t < T && fused; ++t) {
       const long o = static_cast<long>(t) * B;
-      LAUNCH("lstm_step", t > 0 ? 8.0 * B * H * H : 0.0, 0,
+      LAUNCH("lstm_step", t > 0 ? 8.0 * B * H * H : 0.0, (t > 0 ? 8.0 * H * H : 0.0) + 34.0 * B * H,
              lstm_step_fwd(zx + o * 4 * H, t > 0 ? hs + (o - B) * H : nullptr, static_cast<const bf16_t*>(wf(p + 1)),
                            t > 0 ? c + (o - B) * H : nullptr, B, H, gates + o * 4 * H, c + o * H, hs + o * H, s_));
     }
@@ -1163,7 +1218,7 @@ void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, fl
                               gates + static_cast<long>(t) * B * 4 * H, c + static_cast<long>(t) * B * H,
                               hs + static_cast<long>(t) * B * H, s_));
     }
-    LAUNCH("residual", 0, 0, add_bf16(static_cast<const bf16_t*>(u), hs, static_cast<bf16_t*>(out), TB * H, s_));
+    LAUNCH("residual", 0, 6.0 * TB * H, add_bf16(static_cast<const bf16_t*>(u), hs, static_cast<bf16_t*>(out), TB * H, s_));
     u = out;
   }
   if (ce) {
@@ -1171,7 +1226,7 @@ void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, fl
     gv.epi.bias_bf16 = static_cast<const bf16_t*>(wf(3 * L + 1));
     gv.epi.out_f32 = ws<float>(1);
     gemm(gv);
-    LAUNCH("softmax_ce", 0, 0, softmax_ce(ws<float>(1), labels, static_cast<int>(TB), V, stash<void>(slot, 4 * L), 1, loss, ws<float>(7),
+    LAUNCH("softmax_ce", 0, ce_bytes(TB, V), softmax_ce(ws<float>(1), labels, static_cast<int>(TB), V, stash<void>(slot, 4 * L), 1, loss, ws<float>(7),
                          s_));
   }
 }
@@ -1190,7 +1245,7 @@ void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
     GemmDesc gw = gd(V, H, static_cast<int>(TB), opR(dl, V), opR(uL, H), H);
     gw.epi.out_f32 = grad(3 * L);
     gemm(gw);
-    LAUNCH("bias_grad", 0, 0, column_sum(dl, 1, TB, V, V, grad(3 * L + 1), 0, part, s_));
+    LAUNCH("bias_grad", 0, colsum_bytes(TB, V, 2), column_sum(dl, 1, TB, V, V, grad(3 * L + 1), 0, part, s_));
     GemmDesc gx = gd(static_cast<int>(TB), H, V, opK(dl, V), opR(wb(3 * L), H), H);
     gx.epi.out_bf16 = ws<bf16_t>(pp);
     gemm(gx);
@@ -1207,14 +1262,14 @@ void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
     const float* gates = stash<float>(slot, q);
     const float* c = stash<float>(slot, q + 1);
     const bf16_t* hs = stash<bf16_t>(slot, q + 2);
-    LAUNCH("clear_dc", 0, 0, fill_f32(dc, 0.0f, static_cast<long>(B) * H, s_));
+    LAUNCH("clear_dc", 0, 4.0 * B * H, fill_f32(dc, 0.0f, static_cast<long>(B) * H, s_));
     const bool fused = lstm_step_supported(B, H);
     if (fused) {
       bf16_t* whT = ws<bf16_t>(8);
       LAUNCH("transpose", 0, 8.0 * H * H * 2, transpose_bf16(static_cast<const bf16_t*>(wb(p + 1)), 4 * H, H, whT, s_));
       for (int t = T - 1; t >= 0; --t) {
         const long o = static_cast<long>(t) * B;
-        LAUNCH("lstm_step_bwd", t < T - 1 ? 8.0 * B * H * H : 0.0, 0,
+        LAUNCH("lstm_step_bwd", t < T - 1 ? 8.0 * B * H * H : 0.0, (t < T - 1 ? 8.0 * H * H : 0.0) + 54.0 * B * H,
                lstm_step_bwd(t < T - 1 ? dz + (o + B) * 4 * H : nullptr, whT, static_cast<const bf16_t*>(du) + o * H,
                              gates + o * 4 * H, c + o * H, t > 0 ? c + (o - B) * H : nullptr, B, H, dc, dz + o * 4 * H,
                              s_));
@@ -1238,9 +1293,9 @@ void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
       wh.epi.out_f32 = grad(p + 1);
       gemm(wh);
     } else {
-      LAUNCH("clear_grad", 0, 0, fill_f32(grad(p + 1), 0.0f, 4L * H * H, s_));
+      LAUNCH("clear_grad", 0, 16.0 * H * H, fill_f32(grad(p + 1), 0.0f, 4L * H * H, s_));
     }
-    LAUNCH("bias_grad", 0, 0, column_sum(dz, 1, TB, 4 * H, 4 * H, grad(p + 2), 0, part, s_));
+    LAUNCH("bias_grad", 0, colsum_bytes(TB, 4 * H, 2), column_sum(dz, 1, TB, 4 * H, 4 * H, grad(p + 2), 0, part, s_));
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
     GemmDesc gxx = gd(static_cast<int>(TB), in, 4 * H, opK(dz, 4 * H), opR(wb(p), in), in);

@@ -12,7 +12,9 @@
 #include "../../include/spectrain.h"
 #include "kernels.hpp"
 
-#define LAUNCH(family, flops, bytes, expr) timed(family, flops, bytes, [&]() { return (expr); })
+#define LAUNCH(family, flops, bytes, expr) timed(family, flops, bytes, 0.0, [&]() { return (expr); })
+// extra: bytes the launch moves beyond its algorithmic ones (reported apart)
+#define LAUNCH_X(family, flops, bytes, extra, expr) timed(family, flops, bytes, extra, [&]() { return (expr); })
 
 namespace spx {
 
@@ -79,6 +81,7 @@ class Stage {
   void get_state(float* W, float* v);
   void set_state(const float* W, const float* v);
   void get_predicted(int slot, float* out);
+  size_t read_stash(int64_t mb, int index, void* host, size_t capacity);
   bool nonfinite() const { return *reinterpret_cast<volatile int*>(flag_.host()) != 0; }
   void sync();
   void profile(bool enable);
@@ -111,7 +114,7 @@ class Stage {
   // Launch wrapper: checks the launch status and, while profiling, brackets
   // the launch with events on the stage's stream.
   template <typename F>
-  void timed(const char* family, double flops, double bytes, F&& launch) {
+  void timed(const char* family, double flops, double bytes, double extra, F&& launch) {
     if (!prof_on_) {
       hip_check(launch(), family);
       return;
@@ -131,7 +134,7 @@ class Stage {
     } else {
       fam = it->second;
     }
-    prof_recs_.push_back({fam, a, b, flops, bytes});
+    prof_recs_.push_back({fam, a, b, flops, bytes, extra});
   }
   hipEvent_t prof_event();
   void prof_collect();
@@ -172,6 +175,7 @@ class Stage {
   std::vector<Slot> slots_;
   std::vector<DeviceBlock> slot_blocks_;
   std::vector<size_t> stash_off_;
+  std::vector<size_t> stash_bytes_;      // size of each stash buffer (0: unused for this stage)
   DeviceBlock ws_block_;
   std::vector<size_t> ws_off_;
   size_t gemm_ws_bytes_ = 0;
@@ -184,7 +188,7 @@ class Stage {
   struct ProfRec {
     int family;
     hipEvent_t a, b;
-    double flops, bytes;
+    double flops, bytes, extra;
   };
   bool prof_on_ = false;
   std::vector<hipEvent_t> prof_pool_;

@@ -11,7 +11,7 @@ import numpy as np
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspectrain.so")
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 OK, EINVAL, ENOMEM, EHIP, ESTATE, ENONFINITE = range(6)
 STATUS_NAMES = {OK: "OK", EINVAL: "EINVAL", ENOMEM: "ENOMEM", EHIP: "EHIP", ESTATE: "ESTATE",
                 ENONFINITE: "ENONFINITE"}
@@ -27,7 +27,7 @@ EXPORTED = ("spectrain_version_difference", "spectrain_stage_create", "spectrain
             "spectrain_stage_predict", "spectrain_stage_forward", "spectrain_stage_backward",
             "spectrain_stage_update", "spectrain_stage_get_state", "spectrain_stage_set_state",
             "spectrain_stage_get_predicted", "spectrain_stage_profile", "spectrain_stage_profile_read",
-            "spectrain_stage_destroy", "spectrain_last_error")
+            "spectrain_stage_read_stash", "spectrain_stage_destroy", "spectrain_last_error")
 
 
 class StageDesc(ctypes.Structure):
@@ -39,7 +39,8 @@ class StageDesc(ctypes.Structure):
 
 class KernelStat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int64), ("ms_total", ctypes.c_double),
-                ("flops_total", ctypes.c_double), ("bytes_total", ctypes.c_double)]
+                ("flops_total", ctypes.c_double), ("bytes_total", ctypes.c_double),
+                ("extra_bytes_total", ctypes.c_double)]
 
 
 class SpecTrainError(RuntimeError):
@@ -74,6 +75,7 @@ def lib():
             "spectrain_stage_profile": (ctypes.c_int, [vp, i32]),
             "spectrain_stage_profile_read": (ctypes.c_int, [vp, ctypes.POINTER(KernelStat), i32,
                                                             ctypes.POINTER(i32)]),
+            "spectrain_stage_read_stash": (ctypes.c_int, [vp, i64, i32, vp, sz, ctypes.POINTER(sz)]),
             "spectrain_stage_destroy": (ctypes.c_int, [vp]),
             "spectrain_last_error": (ctypes.c_char_p, []),
         }
@@ -199,17 +201,29 @@ class Stage:
         _check(lib().spectrain_stage_get_predicted(self.h, slot, _fptr(out)))
         return out
 
+    def read_stash(self, mb: int, index: int) -> np.ndarray:
+        """Stash buffer `index` of mini-batch mb (in flight) as raw bytes
+        (uint8; empty when the stage does not use that index)."""
+        n = ctypes.c_size_t()
+        _check(lib().spectrain_stage_read_stash(self.h, mb, index, None, 0, ctypes.byref(n)))
+        out = np.empty(n.value, np.uint8)
+        if n.value:
+            _check(lib().spectrain_stage_read_stash(self.h, mb, index, ctypes.c_void_p(out.ctypes.data), out.size,
+                                                    ctypes.byref(n)))
+        return out
+
     def profile(self, enable: bool):
         _check(lib().spectrain_stage_profile(self.h, 1 if enable else 0))
 
     def profile_read(self):
-        """{family: dict(launches, ms_total, flops_total, bytes_total)} in first-launch order."""
+        """{family: dict(launches, ms_total, flops_total, bytes_total, extra_bytes_total)} in first-launch order."""
         cap = 64
         arr = (KernelStat * cap)()
         n = ctypes.c_int32()
         _check(lib().spectrain_stage_profile_read(self.h, arr, cap, ctypes.byref(n)))
         return {arr[i].name.decode(): dict(launches=arr[i].launches, ms_total=arr[i].ms_total,
-                                           flops_total=arr[i].flops_total, bytes_total=arr[i].bytes_total)
+                                           flops_total=arr[i].flops_total, bytes_total=arr[i].bytes_total,
+                                           extra_bytes_total=arr[i].extra_bytes_total)
                 for i in range(min(n.value, cap))}
 
     def destroy(self):

@@ -120,9 +120,10 @@ class Pipeline:
         return [(k, kind, m) for kind, m in stage_task_order(k, self.N, M)]
 
     def run(self, M: int, inputs: Callable, on_update: Optional[Callable] = None, keep_io: bool = False,
-            s_override: Optional[Tuple[int, int]] = None):
+            s_override: Optional[Tuple[int, int]] = None, on_forward: Optional[Callable] = None):
         """Run M mini-batches. on_update(k, count, stage) is called after each
-        update (synchronise inside it if device state is read). Returns
+        update, on_forward(k, m, stage) after each forward (synchronise inside
+        them if device state is read). Returns
         {"loss": {m: device scalar}, "y": {(k, m): tensor}, "dx": {(k, m): tensor}}."""
         held_x: Dict[Tuple[int, int], torch.Tensor] = {}
         held_y: Dict[Tuple[int, int], torch.Tensor] = {}
@@ -159,6 +160,8 @@ class Pipeline:
                             out["y"][(k, m)] = y
                     if dy is not None:
                         held_dy[(k, m)] = dy
+                    if on_forward is not None:
+                        on_forward(k, m, st)
                 else:
                     if self.full and k < self.N - 1:
                         dy = dx_out.pop((k + 1, m))

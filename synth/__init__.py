@@ -259,6 +259,10 @@ SMALL_WORKLOADS: Dict[str, Workload] = {
     "transformer_enc_mid": _single("transformer_enc_mid", "transformer", "bf16", "none", 1, 4, 2, 2,
                                    (128, 2, 256, 128), 2e-3),
     "reslstm_small": _single("reslstm_small", "reslstm", "bf16", "ce", 3, 4, 5, 2, (48, 48, 6, 104), 5e-2),
+    # the same stage at an inner position (k = 1 of 4, three mini-batches in
+    # flight): at the last stage a mini-batch's forward and backward are
+    # adjacent and every staleness policy gives the same weights
+    "reslstm_small_k1": _single("reslstm_small_k1", "reslstm", "bf16", "ce", 1, 4, 5, 2, (48, 48, 6, 104), 5e-2),
     # hidden size a multiple of 32 and batch <= 64: the fused recurrent steps
     "reslstm_mid": _single("reslstm_mid", "reslstm", "bf16", "ce", 3, 4, 24, 2, (96, 96, 7, 136), 5e-2),
 }

@@ -1,23 +1,17 @@
 """Comparison helpers for the GPU-vs-oracle parity tests.
 
-Metric: relative error of a whole tensor in the 2-norm,
-    rel(a, b) = ||a - b||_2 / ||b||_2      (b: the oracle's value),
-taken per tensor and per step; the bound applies to the maximum over steps:
-1e-4 for float32 stages and 2e-2 for bf16 stages. The max-abs normwise error
-max|a - b| / max|b| is reported alongside as a diagnostic.
-
-Why the 2-norm: every contraction feeding a ReLU decides a mask from a value
-both sides compute correctly but in different summation orders. Where that
-value sits within rounding noise of zero, the two sides can legitimately take
-opposite decisions; with random-sign upstream gradients each weight-gradient
-element is a random-walk sum of n terms, so one such decision moves one
-element by about 1/sqrt(n) of its size (6 % at n = 256) while moving the whole
-tensor by a negligible amount in the 2-norm.
+Two metrics per tensor and per step (b: the oracle's value):
+    rel(a, b)      = ||a - b||_2 / ||b||_2             relative 2-norm error
+    normwise(a, b) = max_i |a_i - b_i| / max_i |b_i|   max-abs normwise error
+The bound applies to the maximum over steps: 1e-4 for float32 stages and 2e-2
+for bf16 stages. The stepwise tests gate both (check2); the free-running
+trajectory tests gate the 2-norm (check).
 
 The weight change W_t - W_0 gets one more term: W is stored in float32 on both
 sides, so a value computed on opposite sides of a float32 rounding boundary is
 stored one float32 step apart, at most 2^-23 |W| per element. The bound on the
-weight change is therefore tol + 2^-23 ||W_t|| / ||W_t - W_0||, which matters
+weight change is therefore tol + 2^-23 ||W_t|| / ||W_t - W_0|| in the 2-norm
+and tol + 2^-23 max|W_t| / max|W_t - W_0| in the max-abs norm, which matters
 only in the first steps of float32 stages (one step of the float32 MLP moves W
 by ~1e-3 of its norm).
 """
@@ -63,6 +57,25 @@ class Worst:
         self.rel[key] = max(self.rel.get(key, 0.0), r)
         self.nw[key] = max(self.nw.get(key, 0.0), n)
         assert r <= bound, (self.name, key, where, r, bound)
+
+    def check2(self, key, a, b, bound, where=""):
+        """Both metrics within the bound."""
+        r, n = rel(a, b), normwise(a, b)
+        self.rel[key] = max(self.rel.get(key, 0.0), r)
+        self.nw[key] = max(self.nw.get(key, 0.0), n)
+        assert r <= bound and n <= bound, (self.name, key, where, r, n, bound)
+
+    def check_dw(self, a, b, W_t, tol, where=""):
+        """The step's weight change in both metrics, with the float32 storage
+        floor of the weights added to each bound."""
+        W_t = np.asarray(W_t, np.float64).reshape(-1)
+        r, n = rel(a, b), normwise(a, b)
+        db = np.asarray(b, np.float64).reshape(-1)
+        br = tol + 2.0 ** -23 * float(np.linalg.norm(W_t)) / max(float(np.linalg.norm(db)), 1e-300)
+        bn = tol + 2.0 ** -23 * float(np.max(np.abs(W_t))) / max(float(np.max(np.abs(db))), 1e-300)
+        self.rel["step dW"] = max(self.rel.get("step dW", 0.0), r)
+        self.nw["step dW"] = max(self.nw.get("step dW", 0.0), n)
+        assert r <= br and n <= bn, (self.name, "step dW", where, r, br, n, bn)
 
     def note(self, key, a, b):
         """Record both metrics without a bound (diagnostic only)."""

@@ -5,43 +5,178 @@ recording its (W, v) after every update, every stage output y and every input
 gradient dX. The oracle then recomputes each task from the GPU's own state at
 that moment: a forward from the state before it (predicting with Eq. 5's
 difference), a backward plus update from the state before that backward
-(Eq. 6's difference) and the oracle's own stash of the same mini-batch; in a
-full pipeline a stage's input and upstream gradient are the GPU's neighbouring
-outputs. Every task is thus compared against an exact recomputation of the
-same step, with no divergence carried from earlier steps. Under the Vanilla
-and stashing policies the differences are 0 and a stashing backward reuses
-the weights the oracle's forward of the same mini-batch used.
+(Eq. 6's difference); in a full pipeline a stage's input and upstream
+gradient are the GPU's neighbouring outputs. Every task is thus compared
+against an exact recomputation of the same step, with no divergence carried
+from earlier steps. Under the Vanilla and stashing policies the differences
+are 0 and a stashing backward reuses the weights the oracle's forward of the
+same mini-batch used.
 
-With derived=True (every bf16 run) the gradient quantities (v, the step's
-weight change, dX) pass when they are within tol of the oracle's bf16
-emulation, or else when the GPU is as accurate as that emulation: they are
-also recomputed without any bf16 rounding and
-    rel(gpu, exact) <= max(tol, 1.5 * rel(oracle_bf16, exact)).
-Over many layers the two bf16 computations take different ReLU decisions on
-activations within bf16 noise of zero, and each such decision moves a whole
-row of a weight gradient, so two correct bf16 implementations differ from
-each other about as much as each differs from the exact result (measured
-before any GPU run: 5.7 % on the 4-layer VGG stage, 5.4 % on the transformer
-stage and 14 % on the 8-block bottleneck stage). Forward outputs, losses and
-the weights themselves stay under the plain bound.
+Teacher-forced backward (every bf16 run). A ReLU mask (and every other
+decision a backward takes from a forward activation) is a discontinuous
+function of that activation: two correct bf16 computations that sum in
+different orders round a few activations one bf16 step apart, and where such
+an activation sits within that step of zero its mask differs and the gradient
+element behind it changes by its whole size. Measured on the oracle alone
+(2^-20 relative noise on the inputs, float32 accumulation level): a single
+full-size 3x3 conv layer then moves dX by 2.9e-2 and g by 2.3e-2 in the
+max-abs normwise metric, one bottleneck block moves dX by 0.38, one
+transformer layer by 5.1e-2, while the forward outputs move by 2e-3 to 6e-3.
+No bf16 implementation can therefore be held to 2e-2 on the backward of a
+recomputed forward. The backward is instead recomputed by the oracle from
+the GPU's own stashed activations (spectrain_stage_read_stash), the values
+the GPU's backward read: every mask and every stored operand is then common
+to both sides and the bound is the stated one. The forward is compared
+independently: the oracle's own forward from the same input and weights
+against the GPU's output y and against every buffer the GPU stashed.
+
+Bounds (per tensor, per step, maximum over steps), both metrics gated:
+float32 stages 1e-4, bf16 stages 2e-2, on W, v, the step's weight change,
+dX, y, the loss and every stashed forward buffer.
 """
 import numpy as np
 
 import synth
 from oracle import method, stages
-from parity import TOL, Worst, dw_bound, rel, synthetic_inputs
+from parity import TOL, Worst, synthetic_inputs
 
 
-def run_stepwise(wl, steps, torch, derived=False):
+# ---------------------------------------------------------------- stash ----
+
+def stash_count(spec):
+    """Number of stash buffer ids of a stage (the list in include/spectrain.h)."""
+    L = spec.num_layers
+    return {"fc": L, "conv3x3": L + 2, "bottleneck": 3 * L + 2, "transformer": 13 * L + 1,
+            "reslstm": 4 * L + 1}[spec.kind]
+
+
+def read_gpu_stash(spec, st, m):
+    """Raw bytes of every stash buffer of mini-batch m (in flight on stage st)."""
+    return {i: st.read_stash(m, i) for i in range(stash_count(spec))}
+
+
+def _as(raw, shape, f32=False, bf16=True):
+    if f32 or not bf16:
+        return raw.view(np.float32).astype(np.float64).reshape(shape)
+    u = raw.view(np.uint16).astype(np.uint32) << 16
+    return u.view(np.float32).astype(np.float64).reshape(shape)
+
+
+def oracle_stash_from_gpu(spec, bufs, x, y):
+    """The oracle's stash structure (as stages.forward builds it) filled with
+    the GPU's stashed activations of one mini-batch; x and y are the stage's
+    input and (without a loss head) output as the GPU saw them."""
+    bf = spec.dtype == "bf16"
+    A = lambda i, shape, f32=False: _as(bufs[i], shape, f32=f32, bf16=bf)
+    L, B, d = spec.num_layers, spec.batch, spec.dims
+    ce = spec.head == "ce"
+    x = np.asarray(x, np.float64)
+    if spec.kind == "fc":
+        hid = d[2]
+        acts = [x] + [A(l - 1, (B, hid)) for l in range(1, L)]
+        if ce:
+            return {"acts": acts, "dlogits": A(L - 1, (B, d[1]))}
+        return {"acts": acts + [np.asarray(y, np.float64)]}
+    if spec.kind == "conv3x3":
+        Cin, Cout, H, W = d[:4]
+        acts = [x] + [A(l - 1, (B, H, W, Cout)) for l in range(1, L)]
+        if ce:
+            return {"acts": acts + [A(L - 1, (B, H, W, Cout))], "pooled": A(L, (B, Cout)),
+                    "dlogits": A(L + 1, (B, d[4]))}
+        return {"acts": acts + [np.asarray(y, np.float64)]}
+    if spec.kind == "bottleneck":
+        C, Cm, H, W = d[:4]
+        blocks = []
+        for l in range(L):
+            out = A(3 * l + 2, (B, H, W, C)) if (l < L - 1 or ce) else np.asarray(y, np.float64)
+            blocks.append({"x": x if l == 0 else blocks[-1]["y"], "t1": A(3 * l, (B, H, W, Cm)),
+                           "t2": A(3 * l + 1, (B, H, W, Cm)), "y": out})
+        st = {"blocks": blocks}
+        if ce:
+            st["pooled"] = A(3 * L, (B, C))
+            st["dlogits"] = A(3 * L + 1, (B, d[4]))
+        return st
+    if spec.kind == "transformer":
+        dm, _, F, S = d[:4]
+        T = B * S
+        layers = []
+        for l in range(L):
+            q = 13 * l
+            a = x.reshape(T, dm) if l == 0 else A(13 * (l - 1) + 12, (T, dm))
+            layers.append({"a": a, "qkv": A(q, (T, 3 * dm)), "ctx": A(q + 3, (T, dm)), "r1": A(q + 4, (T, dm)),
+                           "h": A(q + 7, (T, dm)), "f1": A(q + 8, (T, F)), "r2": A(q + 9, (T, dm))})
+        st = {"layers": layers}
+        if ce:
+            st["out"] = A(13 * (L - 1) + 12, (T, dm))
+            st["dlogits"] = A(13 * L, (T, d[4]))
+        return st
+    if spec.kind == "reslstm":
+        _, Hd, Tn, V = d[:4]
+        layers = []
+        for l in range(L):
+            u = x if l == 0 else A(4 * (l - 1) + 3, (Tn, B, Hd))
+            layers.append({"u": u, "gates": A(4 * l, (Tn, B, 4 * Hd), f32=True), "c": A(4 * l + 1, (Tn, B, Hd), f32=True),
+                           "h": A(4 * l + 2, (Tn, B, Hd))})
+        st = {"layers": layers}
+        if ce:
+            st["out"] = A(4 * (L - 1) + 3, (Tn, B, Hd))
+            st["dlogits"] = A(4 * L, (Tn * B, V))
+        else:
+            st["out"] = np.asarray(y, np.float64)
+        return st
+    raise ValueError(spec.kind)
+
+
+def forward_buffers(spec, st):
+    """(name, array) pairs of a stash dict that the forward pass produced (the
+    stage input, which both sides share, left out)."""
+    out = []
+    if spec.kind in ("fc", "conv3x3"):
+        out += [(f"act{l}", a) for l, a in enumerate(st["acts"]) if l > 0]
+    elif spec.kind == "bottleneck":
+        for l, b in enumerate(st["blocks"]):
+            out += [(f"b{l}.{k}", b[k]) for k in ("t1", "t2", "y")]
+    elif spec.kind == "transformer":
+        for l, c in enumerate(st["layers"]):
+            out += [(f"l{l}.{k}", c[k]) for k in ("qkv", "ctx", "r1", "h", "f1", "r2")]
+            if l > 0:
+                out.append((f"l{l}.a", c["a"]))
+    elif spec.kind == "reslstm":
+        for l, c in enumerate(st["layers"]):
+            out += [(f"l{l}.{k}", c[k]) for k in ("gates", "c", "h")]
+            if l > 0:
+                out.append((f"l{l}.u", c["u"]))
+    for k in ("pooled", "dlogits"):
+        if k in st:
+            out.append((k, st[k]))
+    return out
+
+
+# -------------------------------------------------------------- harness ----
+
+def run_stepwise(wl, steps, torch, forced=None, check=None):
+    """forced: teacher-forced backward (default for bf16 stages). check: the
+    mini-batches whose forward and backward are recomputed (default: all);
+    the GPU runs every task either way and each checked task starts from the
+    GPU's own state at that moment."""
     from paper_1809_02839_amd.pipeline import Pipeline, stage_task_order
 
     specs = wl.stages
     N = specs[0].num_stages
     full = len(specs) == N
+    if forced is None:
+        forced = specs[0].dtype == "bf16"
     W0s = {s.stage_index: synth.initial_params(s) for s in specs}
+    spec_of = {s.stage_index: s for s in specs}
     pipe = Pipeline(specs, [W0s[s.stage_index] for s in specs])
     states = {}
-    out = pipe.run(steps, synthetic_inputs, keep_io=True,
+    gstash = {}
+
+    def on_forward(k, m, st):
+        if forced and (check is None or m in check):
+            gstash[(k, m)] = read_gpu_stash(spec_of[k], st, m)
+
+    out = pipe.run(steps, synthetic_inputs, keep_io=True, on_forward=on_forward,
                    on_update=lambda k, u, st: states.__setitem__((k, u), st.get_state()))
     torch.cuda.synchronize()
     y_gpu = {key: t.float().cpu().numpy() for key, t in out["y"].items()}
@@ -61,23 +196,35 @@ def run_stepwise(wl, steps, torch, derived=False):
         v = np.zeros_like(W)
         u = 0
         stash = {}
+        xs = {}
         rnd = stages.weight_rounder(spec)
         for kind, m in stage_task_order(k, N, steps):
+            if check is not None and m not in check:
+                if kind == "B":
+                    u += 1
+                    W, v = (a.astype(np.float64) for a in states[(k, u)])
+                continue
             x, dy, lab = synthetic_inputs(spec, m)
             if full and k > 0:
                 x = y_gpu[(k - 1, m)]
             if kind == "F":
                 P = stages.unpack(spec, rnd(method.predict(W, v, sf, lr)))
                 y, loss, st = stages.forward(spec, P, x, lab)
-                stash[m] = st
                 if policy == "stash":
                     stash[("weights", m)] = P   # the backward reuses the forward's weights
-                if derived:
-                    stash[("exact", m)] = stages.forward(spec, P, x, lab, exact=True)[2]
                 if spec.head == "ce":
-                    worst.check("loss", [loss_gpu[m]], [loss], tol, f"k{k} m{m}")
+                    worst.check2("loss", [loss_gpu[m]], [loss], tol, f"k{k} m{m}")
                 else:
-                    worst.check("y", y_gpu[(k, m)], y, tol, f"k{k} m{m}")
+                    worst.check2("y", y_gpu[(k, m)], y, tol, f"k{k} m{m}")
+                if forced:
+                    yg = None if spec.head == "ce" else y_gpu[(k, m)]
+                    g_st = oracle_stash_from_gpu(spec, gstash.pop((k, m)), x, yg)
+                    for (name, a), (_, b) in zip(forward_buffers(spec, g_st), forward_buffers(spec, st)):
+                        worst.check2("fwd " + name.split(".")[-1], a, b, tol, f"k{k} m{m} {name}")
+                    stash[m] = g_st
+                else:
+                    stash[m] = st
+                xs[m] = x
             else:
                 if full and k < N - 1:
                     dy = dx_gpu[(k + 1, m)]
@@ -86,28 +233,16 @@ def run_stepwise(wl, steps, torch, derived=False):
                 else:
                     P = stages.unpack(spec, rnd(method.predict(W, v, sb, lr)))
                 dx, grads = stages.backward(spec, P, stash.pop(m), dy)
+                xs.pop(m)
                 W1, v1 = method.momentum_sgd_step(W, v, stages.pack(spec, grads), lr, gamma)
                 u += 1
                 Wg, vg = states[(k, u)]
-                worst.check("W", Wg, W1, tol, f"k{k} u{u}")
-                if derived:
-                    dxe, ge = stages.backward(spec, P, stash.pop(("exact", m)), dy, exact=True)
-                    W1e, v1e = method.momentum_sgd_step(W, v, stages.pack(spec, ge), lr, gamma)
-                    pairs = [("v", vg, v1, v1e), ("step dW", Wg.astype(np.float64) - W, W1 - W, W1e - W)]
-                    if (k, m) in dx_gpu:
-                        pairs.append(("dx", dx_gpu[(k, m)], dx, dxe))
-                    for key, a, b, e in pairs:
-                        worst.note(key, a, b)
-                        if rel(a, b) <= tol:
-                            worst.note(key + " vs exact", a, e)
-                            continue
-                        bound = max(tol, 1.5 * rel(b, e))
-                        worst.check(key + " vs exact", a, e, bound, f"k{k} u{u} (oracle bf16 vs exact {rel(b, e):.2e})")
-                else:
-                    worst.check("v", vg, v1, tol, f"k{k} u{u}")
-                    worst.check("step dW", Wg.astype(np.float64) - W, W1 - W, dw_bound(tol, W1, W), f"k{k} u{u}")
-                    if (k, m) in dx_gpu:
-                        worst.check("dx", dx_gpu[(k, m)], dx, tol, f"k{k} m{m}")
+                where = f"k{k} u{u}"
+                worst.check2("W", Wg, W1, tol, where)
+                worst.check2("v", vg, v1, tol, where)
+                worst.check_dw(Wg.astype(np.float64) - W, W1 - W, Wg, tol, where)
+                if (k, m) in dx_gpu:
+                    worst.check2("dx", dx_gpu[(k, m)], dx, tol, f"k{k} m{m}")
                 # continue from the GPU's state: each step is checked on its own
                 W, v = Wg.astype(np.float64), vg.astype(np.float64)
     return worst

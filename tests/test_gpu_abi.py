@@ -114,7 +114,7 @@ EDGE = {
 def test_batch_one_stage_stepwise(kind):
     wl = synth.Workload(f"{kind}_batch1", (EDGE[kind],), 8)
     print(f"[stepwise] {wl.name}", flush=True)
-    worst = run_stepwise(wl, wl.steps, torch, derived=True)
+    worst = run_stepwise(wl, wl.steps, torch)
     print(f"[stepwise] {wl.name}: {worst.report()}", flush=True)
 
 
@@ -130,7 +130,7 @@ def test_ksliced_conv_forward_ragged_edges_stepwise():
     spec = synth.StageSpec("conv3x3", "bf16", "none", 1, 4, 230, 2, (64, 200, 7, 9), 1e-3, 0.9)
     wl = synth.Workload("conv_ksliced_ragged", (spec,), 4)
     print(f"[stepwise] {wl.name}", flush=True)
-    worst = run_stepwise(wl, wl.steps, torch, derived=True)
+    worst = run_stepwise(wl, wl.steps, torch)
     print(f"[stepwise] {wl.name}: {worst.report()}", flush=True)
 
 
@@ -143,5 +143,5 @@ def test_narrow_tile_ragged_edges_stepwise():
     spec = synth.StageSpec("fc", "bf16", "none", 1, 3, 25000, 2, (64, 200, 200), 0.01, 0.9)
     wl = synth.Workload("fc_narrow_ragged", (spec,), 4)
     print(f"[stepwise] {wl.name}", flush=True)
-    worst = run_stepwise(wl, wl.steps, torch, derived=True)
+    worst = run_stepwise(wl, wl.steps, torch)
     print(f"[stepwise] {wl.name}: {worst.report()}", flush=True)

@@ -88,11 +88,25 @@ def test_kernel_stats_table_is_sorted_by_total_time(tmp_path):
 
 def test_traffic_entry_is_null_once_the_kernel_sources_change(monkeypatch):
     import bench
-    real = bench.traffic_per_launch("vgg_conv", "conv3x3_wgrad")
+    fam = "gemm_bf16_kernel<3, 4, false, 128, 1>"
+    real = bench.traffic_per_launch("vgg_conv", fam)
     assert real is None or real > 0
     monkeypatch.setattr(profiling, "source_digest", lambda: "0" * 16)
-    assert bench.traffic_per_launch("vgg_conv", "conv3x3_wgrad") is None
-    assert bench.traffic_per_launch("no_such_workload", "conv3x3_wgrad") is None
+    assert bench.traffic_per_launch("vgg_conv", fam) is None
+    assert bench.traffic_per_launch("no_such_workload", fam) is None
+
+
+def test_family_roof_takes_the_slower_of_the_two_roofs():
+    import bench
+    # 1 GFLOP and 100 MB in 0.1 ms: 0.4 us at the MFMA peak, 12.5 us at the HBM peak -> HBM
+    b, ach, peak, unit, t = bench.family_roof({"flops_total": 1e9, "bytes_total": 1e8, "ms_total": 0.1}, 2500.0)
+    assert (b, unit, peak) == ("hbm", "GB/s", bench.PEAK_HBM_GBPS)
+    assert ach == pytest.approx(1000.0) and t == pytest.approx(1e8 / 8e12 * 1e3)
+    # 100 GFLOP and 10 MB: 40 us at the MFMA peak, 1.25 us at the HBM peak -> MFMA
+    b, ach, peak, unit, t = bench.family_roof({"flops_total": 1e11, "bytes_total": 1e7, "ms_total": 0.1}, 2500.0)
+    assert (b, unit) == ("mfma", "TFLOP/s") and ach == pytest.approx(1000.0) and t == pytest.approx(0.04)
+    # a pass with no flops is always HBM-bound
+    assert bench.family_roof({"flops_total": 0.0, "bytes_total": 8e6, "ms_total": 0.002}, 2500.0)[0] == "hbm"
 
 
 def test_bench_refuses_more_than_one_gpu():
@@ -102,11 +116,12 @@ def test_bench_refuses_more_than_one_gpu():
     assert "one GPU" in r.stderr and r.stdout == ""
 
 
-def test_traffic_of_a_family_with_two_instantiations_is_dispatch_weighted(monkeypatch):
+def test_traffic_of_a_family_with_two_kernels_is_dispatch_weighted(monkeypatch):
     import bench
-    table = {"gemm_bf16_kernel<2, 5, true, 64, 1>": (3, 60.0), "gemm_bf16_kernel<2, 5, true, 128, 1>": (1, 100.0),
-             "gemm_bf16_kernel<3, 4, false, 128, 1>": (4, 7.0)}
+    table = {"fused_update_kernel": (3, 60.0), "fused_update_partials_kernel": (1, 100.0),
+             "gemm_bf16_kernel<2, 5, true, 64, 1>": (4, 7.0), "gemm_bf16_kernel<2, 5, true, 128, 1>": (2, 9.0)}
     monkeypatch.setattr(profiling, "read_traffic", lambda path, with_dispatches=False: ("d" * 16, table))
     monkeypatch.setattr(profiling, "source_digest", lambda: "d" * 16)
-    assert bench.traffic_per_launch("vgg_conv", "conv3x3_dgrad") == 70   # (3 * 60 + 100) / 4
-    assert bench.traffic_per_launch("vgg_conv", "conv3x3_wgrad") == 7
+    assert bench.traffic_per_launch("vgg_conv", "fused_update") == 70   # (3 * 60 + 100) / 4
+    # a GEMM family is one instantiation
+    assert bench.traffic_per_launch("vgg_conv", "gemm_bf16_kernel<2, 5, true, 64, 1>") == 7
