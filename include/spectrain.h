@@ -165,6 +165,21 @@ int spectrain_stage_forward(spectrain_stage_t st, int64_t mb_id, const void* x_d
  * not in flight or a previous gradient is still waiting for its update. */
 int spectrain_stage_backward(spectrain_stage_t st, int64_t mb_id, const void* dy_dev, void* dx_dev);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * backward pass above, identical in arguments, state rules and results
+ * (bitwise), whose split-K partial planes live in the library's per-device
+ * scratch array instead of the stage's workspace. The call allocates and
+ * frees nothing; the array (64 MiB, SPECTRAIN_NOALLOC_SCRATCH_BYTES) is held
+ * by every GPU the library runs on until the process ends, and its address
+ * is looked up on the first such call on a device. EINVAL when the stage's
+ * split-K workspace exceeds the array. Every call on one GPU shares that
+ * GPU's array, and the array keeps the last call's contents (every partial
+ * a call reads it first writes, so nothing needs clearing): calls that
+ * overlap on one GPU, on different streams, race. */
+#define SPECTRAIN_NOALLOC_SCRATCH_BYTES (64u << 20)
+int spectrain_stage_backward_noalloc(spectrain_stage_t st, int64_t mb_id, const void* dy_dev, void* dx_dev);
+
 /* One fused pass over the arenas: Eq. 1, W <- W - eta v, then Eq. 4 for both
  * slots (slot 0 with s_next_fwd, slot 1 with s_next_bwd; a negative s leaves
  * that slot unchanged). ESTATE unless a backward produced g since the last

@@ -88,6 +88,10 @@ int spectrain_stage_backward(spectrain_stage_t st, int64_t mb_id, const void* dy
   return guarded(st, [&](spx::Stage& x) { x.backward(mb_id, dy_dev, dx_dev); });
 }
 
+int spectrain_stage_backward_noalloc(spectrain_stage_t st, int64_t mb_id, const void* dy_dev, void* dx_dev) {
+  return guarded(st, [&](spx::Stage& x) { x.backward_noalloc(mb_id, dy_dev, dx_dev); });
+}
+
 int spectrain_stage_update(spectrain_stage_t st, int32_t s_next_fwd, int32_t s_next_bwd) {
   return guarded(st, [&](spx::Stage& x) { x.update(s_next_fwd, s_next_bwd); });
 }

@@ -208,7 +208,7 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
   const double flops = 2.0 * d.M * d.N * static_cast<double>(d.K) * d.batch;
   const double bytes = gemm_algorithmic_bytes(d, esz_);
   GemmDesc dd = d;
-  dd.workspace = ws<float>(static_cast<int>(ws_off_.size()) - 1);
+  dd.workspace = ext_ws_ ? ext_ws_ : ws<float>(static_cast<int>(ws_off_.size()) - 1);
   dd.workspace_bytes = gemm_ws_bytes_;
   if (!dt_) {
     LAUNCH(gemm_f32_kernel_name(dd), flops, bytes, gemm_f32(dd, s_));
@@ -495,6 +495,7 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
   if (n_params != n_params_) fail("n_params " + std::to_string(n_params) + " != " + std::to_string(n_params_));
   if (!W0) fail("W0_host is NULL");
 
+  hip_check(hipGetDevice(&device_), "hipGetDevice");
   // arenas: W, v, g (float32), two predicted slots (operand dtype), all padded
   size_t oW = arena_.add(n_arena_ * 4), ov = arena_.add(n_arena_ * 4), og = arena_.add(n_arena_ * 4);
   size_t of = arena_.add(n_arena_ * esz_), ob = arena_.add(n_arena_ * esz_);
@@ -676,6 +677,21 @@ void Stage::backward(int64_t mb, const void* dy, void* dx) {
   }
   slots_[slot] = Slot{};
   g_pending_ = true;
+}
+
+void Stage::backward_noalloc(int64_t mb, const void* dy, void* dx) {
+  if (gemm_ws_bytes_ > SCRATCH_BYTES)
+    fail("the stage's split-K workspace (" + std::to_string(gemm_ws_bytes_) + " bytes) exceeds the " +
+         std::to_string(SCRATCH_BYTES) + "-byte scratch of the allocation-free backward");
+  float* scratch = device_scratch(device_);
+  ext_ws_ = scratch;
+  try {
+    backward(mb, dy, dx);
+  } catch (...) {
+    ext_ws_ = nullptr;
+    throw;
+  }
+  ext_ws_ = nullptr;
 }
 
 // ==================================================================== FC ====

@@ -26,6 +26,13 @@ struct StageError : std::runtime_error {
 
 void hip_check(hipError_t e, const char* what);
 
+// Bytes of the per-device scratch array of the allocation-free backward: the
+// split-K workspace of a bf16 stage, so both backward entry points split
+// every GEMM alike and give bitwise identical results.
+constexpr size_t SCRATCH_BYTES = SPECTRAIN_NOALLOC_SCRATCH_BYTES;
+// Device address of that array on `device` (looked up on first use, cached).
+float* device_scratch(int device);
+
 // A set of device sub-buffers carved from one hipMalloc, each 256-byte aligned.
 class DeviceBlock {
  public:
@@ -77,6 +84,9 @@ class Stage {
   void predict(int s, int slot);
   void forward(int64_t mb, const void* x, void* y, const int32_t* labels, float* loss);
   void backward(int64_t mb, const void* dy, void* dx);
+  // The same backward with every split-K partial plane in the device's
+  // scratch array instead of the stage's workspace; allocates nothing.
+  void backward_noalloc(int64_t mb, const void* dy, void* dx);
   void update(int s_f, int s_b);
   void get_state(float* W, float* v);
   void set_state(const float* W, const float* v);
@@ -179,6 +189,8 @@ class Stage {
   DeviceBlock ws_block_;
   std::vector<size_t> ws_off_;
   size_t gemm_ws_bytes_ = 0;
+  float* ext_ws_ = nullptr;              // split-K partials of the current call, when not the workspace
+  int device_ = -1;                      // device current at create (the stream's device)
   bool g_pending_ = false;
   DeviceBlock defer_block_;              // split-K partials of gradients the update reduces
   float* defer_ = nullptr;

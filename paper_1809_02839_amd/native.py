@@ -25,6 +25,7 @@ KIND_BY_NAME = {"fc": KIND_FC, "conv3x3": KIND_CONV3X3, "bottleneck": KIND_BOTTL
 
 EXPORTED = ("spectrain_version_difference", "spectrain_stage_create", "spectrain_stage_num_params",
             "spectrain_stage_predict", "spectrain_stage_forward", "spectrain_stage_backward",
+            "spectrain_stage_backward_noalloc",
             "spectrain_stage_update", "spectrain_stage_get_state", "spectrain_stage_set_state",
             "spectrain_stage_get_predicted", "spectrain_stage_profile", "spectrain_stage_profile_read",
             "spectrain_stage_read_stash", "spectrain_stage_destroy", "spectrain_last_error")
@@ -68,6 +69,7 @@ def lib():
             "spectrain_stage_predict": (ctypes.c_int, [vp, i32, i32]),
             "spectrain_stage_forward": (ctypes.c_int, [vp, i64, vp, vp, vp, vp]),
             "spectrain_stage_backward": (ctypes.c_int, [vp, i64, vp, vp]),
+            "spectrain_stage_backward_noalloc": (ctypes.c_int, [vp, i64, vp, vp]),
             "spectrain_stage_update": (ctypes.c_int, [vp, i32, i32]),
             "spectrain_stage_get_state": (ctypes.c_int, [vp, fp, fp]),
             "spectrain_stage_set_state": (ctypes.c_int, [vp, fp, fp]),
@@ -181,6 +183,10 @@ class Stage:
     def backward(self, mb: int, dy=None, dx=None):
         a = self._act
         _check(lib().spectrain_stage_backward(self.h, mb, _dptr(dy, a, "dy"), _dptr(dx, a, "dx")))
+
+    def backward_noalloc(self, mb: int, dy=None, dx=None):
+        a = self._act
+        _check(lib().spectrain_stage_backward_noalloc(self.h, mb, _dptr(dy, a, "dy"), _dptr(dx, a, "dx")))
 
     def update(self, s_next_fwd: int, s_next_bwd: int):
         _check(lib().spectrain_stage_update(self.h, s_next_fwd, s_next_bwd))
