@@ -169,15 +169,17 @@ int spectrain_stage_backward(spectrain_stage_t st, int64_t mb_id, const void* dy
  * capture, tight serving loops, harnesses that forbid hipMalloc): the
  * backward pass above, identical in arguments, state rules and results
  * (bitwise), whose split-K partial planes live in the library's per-device
- * scratch array instead of the stage's workspace. The call allocates and
- * frees nothing; the array (64 MiB, SPECTRAIN_NOALLOC_SCRATCH_BYTES) is held
+ * scratch array instead of the stage's workspace (one half for the stage's
+ * stream, one for the stream its weight gradients run on). The call
+ * allocates and frees nothing; the array (128 MiB,
+ * SPECTRAIN_NOALLOC_SCRATCH_BYTES) is held
  * by every GPU the library runs on until the process ends, and its address
  * is looked up on the first such call on a device. EINVAL when the stage's
- * split-K workspace exceeds the array. Every call on one GPU shares that
+ * split-K workspaces exceed the array. Every call on one GPU shares that
  * GPU's array, and the array keeps the last call's contents (every partial
  * a call reads it first writes, so nothing needs clearing): calls that
  * overlap on one GPU, on different streams, race. */
-#define SPECTRAIN_NOALLOC_SCRATCH_BYTES (64u << 20)
+#define SPECTRAIN_NOALLOC_SCRATCH_BYTES (128u << 20)
 int spectrain_stage_backward_noalloc(spectrain_stage_t st, int64_t mb_id, const void* dy_dev, void* dx_dev);
 
 /* One fused pass over the arenas: Eq. 1, W <- W - eta v, then Eq. 4 for both

@@ -17,6 +17,14 @@
 // buffer loads whose resource spans exactly the operand tensor: an offset
 // outside it (zero padding of convolutions, ragged tile edges) reads zero.
 //
+// Epilogue: an unsplit 4-wave launch whose output rows allow 16-byte
+// accesses stages its float32 tile in LDS and then gives each thread eight
+// consecutive columns of a row, so the residual and mask loads and the output
+// stores of a wave cover whole row segments (an output line is never written
+// piecemeal, which had tripled the HBM write traffic of the bottleneck's
+// 1x1 data gradient); other launches write from the MFMA layout, with every
+// epilogue load of a lane issued before its first store.
+//
 // Split-K: a 128 x 128 launch may divide K into `splits` ranges; each writes
 // float32 partial tiles to a workspace and an elementwise pass sums the
 // partials in a fixed order and applies the epilogue, so results do not
@@ -103,6 +111,7 @@ struct KArgs {
   long a_bs1, a_bs2, b_bs1, b_bs2, c_bs1, c_bs2;
   float* partial;        // splits > 1: [split][batch][M][N] float32
   int vec_epi;           // output, bias, residual and mask allow the four-column epilogue
+  int vec8;              // ... and the eight-column one (N, ldc multiples of 8, 16-byte aligned tensors)
   int bn;                // block tile width in N (host side: selects the kernel)
   int ksl;               // waves per output sub-tile (host side: selects the kernel)
   EpiDev e;
@@ -368,6 +377,61 @@ __device__ __forceinline__ void epilogue4(const EpiDev& e, long idx, int col, fl
   }
 }
 
+// epilogue4 with the bf16 bias, residual and mask already loaded (bb, rb, mk:
+// four bf16 each; read only where the epilogue has that operand).
+__device__ __forceinline__ void epilogue4_pre(const EpiDev& e, long idx, int col, float4 a, uint2 bb, uint2 rb,
+                                              uint2 mk) {
+  float v[4] = {a.x * e.alpha, a.y * e.alpha, a.z * e.alpha, a.w * e.alpha};
+  auto unpack = [](uint2 u, float (&f)[4]) {
+    f[0] = bf16_to_f32(static_cast<bf16_t>(u.x & 0xffff));
+    f[1] = bf16_to_f32(static_cast<bf16_t>(u.x >> 16));
+    f[2] = bf16_to_f32(static_cast<bf16_t>(u.y & 0xffff));
+    f[3] = bf16_to_f32(static_cast<bf16_t>(u.y >> 16));
+  };
+  float t[4];
+  if (e.bias) {
+    const float4 b = *reinterpret_cast<const float4*>(e.bias + col);
+    v[0] += b.x; v[1] += b.y; v[2] += b.z; v[3] += b.w;
+  } else if (e.bias_bf16) {
+    unpack(bb, t);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] += t[q];
+  }
+  if (e.res_f32) {
+    const float4 r = *reinterpret_cast<const float4*>(e.res_f32 + idx);
+    v[0] += r.x; v[1] += r.y; v[2] += r.z; v[3] += r.w;
+  }
+  if (e.res_bf16) {
+    unpack(rb, t);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] += t[q];
+  }
+  if (e.relu) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = fmaxf(v[q], 0.0f);
+  }
+  if (e.out_f32) {
+    float4* o = reinterpret_cast<float4*>(e.out_f32 + idx);
+    if (e.accumulate) {
+      const float4 old = *o;
+      v[0] += old.x; v[1] += old.y; v[2] += old.z; v[3] += old.w;
+    }
+    *o = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  if (e.out_bf16) {
+    uint32_t h[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) h[q] = f32_to_bf16(v[q]);
+    if (e.mask) {
+      unpack(mk, t);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (!(t[q] > 0.0f)) h[q] = 0;
+    }
+    *reinterpret_cast<uint2*>(e.out_bf16 + idx) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+  }
+}
+
 // Stores a block's 128 x 128 accumulator tile: float32 partials of its K
 // split, or the epilogue into the outputs.
 template <int NJ>
@@ -402,27 +466,50 @@ __device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2]
     return;
   }
   const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
+  const EpiDev& e = args.e;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 2; ++i) {
+    const int row = row0 + wm * 64 + i * 32 + (lane & 31);
+    if (row >= args.M) continue;
+    // The bf16 epilogue operands (bias, residual, ReLU mask) of this lane's
+    // 4 NJ column groups are all loaded before the first store: the output
+    // may alias nothing the compiler can prove, so a load issued after a
+    // store waits for it, and one memory round trip per group would
+    // serialise the epilogue. Loading first is exact also for an output
+    // that overwrites its own residual element by element.
+    uint2 bb[NJ][4], rb[NJ][4], mk[NJ][4];
+    if (args.vec_epi) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int col = col0 + wn * (32 * NJ) + j * 32 + 8 * g + 4 * (lane >> 5);
+          const long idx = coff + static_cast<long>(row) * e.ldc + col;
+          const bool ok = col + 3 < args.N;
+          bb[j][g] = rb[j][g] = mk[j][g] = make_uint2(0, 0);
+          if (ok && !e.bias && e.bias_bf16) bb[j][g] = *reinterpret_cast<const uint2*>(e.bias_bf16 + col);
+          if (ok && e.res_bf16) rb[j][g] = *reinterpret_cast<const uint2*>(e.res_bf16 + idx);
+          if (ok && e.mask) mk[j][g] = *reinterpret_cast<const uint2*>(e.mask + idx);
+        }
+    }
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-      const int row = row0 + wm * 64 + i * 32 + (lane & 31);
-      if (row >= args.M) continue;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int col = col0 + wn * (32 * NJ) + j * 32 + 8 * g + 4 * (lane >> 5);
-        const long idx = coff + static_cast<long>(row) * args.e.ldc + col;
+        const long idx = coff + static_cast<long>(row) * e.ldc + col;
         const float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
         if (args.vec_epi && col + 3 < args.N) {
-          epilogue4(args.e, idx, col, v);
+          epilogue4_pre(e, idx, col, v, bb[j][g], rb[j][g], mk[j][g]);
         } else {
-          if (col < args.N) epilogue(args.e, idx, col, v.x);
-          if (col + 1 < args.N) epilogue(args.e, idx + 1, col + 1, v.y);
-          if (col + 2 < args.N) epilogue(args.e, idx + 2, col + 2, v.z);
-          if (col + 3 < args.N) epilogue(args.e, idx + 3, col + 3, v.w);
+          if (col < args.N) epilogue(e, idx, col, v.x);
+          if (col + 1 < args.N) epilogue(e, idx + 1, col + 1, v.y);
+          if (col + 2 < args.N) epilogue(e, idx + 2, col + 2, v.z);
+          if (col + 3 < args.N) epilogue(e, idx + 3, col + 3, v.w);
         }
       }
     }
+  }
 }
 
 // BNT: block tile width in N (128, or 64 for launches whose 128-wide tiles
@@ -443,13 +530,25 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
   const int tid = threadIdx.x;
   // XCD-aware tile order: consecutive blocks land on consecutive XCDs; give
   // each XCD a contiguous run of tiles (tiles sharing A rows share an L2).
+  // A launch of batch x split slices enumerates (slice, tile) slice-major;
+  // each XCD takes a contiguous run of that order, so an XCD works on the
+  // same K slice (and batch entry) of neighbouring tiles and reads each
+  // slice of both operands once, instead of every XCD fetching the operand
+  // shared by its tiles for every slice.
   const int bid = blockIdx.x;
-  int tile = bid;
-  if ((args.tiles_total & 7) == 0) tile = (bid & 7) * (args.tiles_total >> 3) + (bid >> 3);
+  int tile = bid, zs = blockIdx.y;
+  const int blocks = gridDim.x * gridDim.y;
+  if ((blocks & 7) == 0) {
+    const int lin = blockIdx.y * gridDim.x + bid;
+    const int ord = (lin & 7) * (blocks >> 3) + (lin >> 3);
+    zs = ord / args.tiles_total;
+    tile = ord - zs * args.tiles_total;
+  } else if ((args.tiles_total & 7) == 0) {
+    tile = (bid & 7) * (args.tiles_total >> 3) + (bid >> 3);
+  }
   const int tm = tile / args.tiles_n, tn = tile - tm * args.tiles_n;
   const int row0 = tm * BM, col0 = tn * BNT;
 
-  const int zs = blockIdx.y;
   const int z = zs / args.splits, split = zs - z * args.splits;
   const int z1 = z / args.zdiv, z2 = z - z1 * args.zdiv;
   OperandDev A = args.A, B = args.B;
@@ -564,6 +663,50 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
       for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] += mine[((i * NJ + j) * 16 + r) * 64];
+  }
+  if constexpr (KSL == 1) {
+    if (args.splits == 1 && args.vec8) {
+      // float32 tile [128][BNT] in LDS (row pitch BNT + 4 floats), then each
+      // thread takes 8 consecutive columns of a row: every load and store of
+      // the epilogue covers whole row segments
+      constexpr int EP = BNT + 4;
+      float* tile = reinterpret_cast<float*>(&lds[0][0][0]);
+      static_assert(sizeof(lds) >= 128 * (BNT + 4) * sizeof(float), "the float32 tile fits the operand buffers");
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int r = wm * 64 + i * 32 + (lane & 31);
+            const int c = wn * (32 * NJ) + j * 32 + 8 * g + 4 * (lane >> 5);
+            *reinterpret_cast<float4*>(tile + r * EP + c) =
+                make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+          }
+      __syncthreads();
+      constexpr int TPR = BNT / 8;          // threads per row
+      constexpr int RPP = NT / TPR;         // rows per pass
+      const int cl = (tid % TPR) * 8, rl = tid / TPR;
+      const int col = col0 + cl;
+      const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
+      const EpiDev& e = args.e;
+#pragma unroll 4
+      for (int rr = rl; rr < 128; rr += RPP) {
+        const int row = row0 + rr;
+        if (row >= args.M || col >= args.N) continue;
+        const long idx = coff + static_cast<long>(row) * e.ldc + col;
+        uint4 rb = make_uint4(0, 0, 0, 0), mk = make_uint4(0, 0, 0, 0), bb = make_uint4(0, 0, 0, 0);
+        if (e.res_bf16) rb = *reinterpret_cast<const uint4*>(e.res_bf16 + idx);
+        if (e.mask) mk = *reinterpret_cast<const uint4*>(e.mask + idx);
+        if (!e.bias && e.bias_bf16) bb = *reinterpret_cast<const uint4*>(e.bias_bf16 + col);
+        const float4 a0 = *reinterpret_cast<const float4*>(tile + rr * EP + cl);
+        const float4 a1 = *reinterpret_cast<const float4*>(tile + rr * EP + cl + 4);
+        epilogue4_pre(e, idx, col, a0, make_uint2(bb.x, bb.y), make_uint2(rb.x, rb.y), make_uint2(mk.x, mk.y));
+        epilogue4_pre(e, idx + 4, col + 4, a1, make_uint2(bb.z, bb.w), make_uint2(rb.z, rb.w), make_uint2(mk.z, mk.w));
+      }
+      return;
+    }
   }
   write_tile<NJ>(args, acc, row0, col0, wm, wn, lane, split, z, z1, z2);
 }
@@ -779,6 +922,9 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   const EpiDev& e = a.e;
   a.vec_epi = e.ldc % 4 == 0 && a.c_bs1 % 4 == 0 && a.c_bs2 % 4 == 0 && al(e.out_f32, 16) && al(e.out_bf16, 8) &&
               al(e.bias, 16) && al(e.bias_bf16, 8) && al(e.res_f32, 16) && al(e.res_bf16, 8) && al(e.mask, 8);
+  a.vec8 = a.vec_epi && d.N % 8 == 0 && e.ldc % 8 == 0 && a.c_bs1 % 8 == 0 && a.c_bs2 % 8 == 0 &&
+           al(e.out_f32, 32) && al(e.out_bf16, 16) && al(e.bias, 32) && al(e.bias_bf16, 16) && al(e.res_f32, 32) &&
+           al(e.res_bf16, 16) && al(e.mask, 16) && !e.res_f32 && !e.bias;
   return true;
 }
 

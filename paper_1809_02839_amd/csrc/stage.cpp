@@ -208,10 +208,12 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
   const double flops = 2.0 * d.M * d.N * static_cast<double>(d.K) * d.batch;
   const double bytes = gemm_algorithmic_bytes(d, esz_);
   GemmDesc dd = d;
-  dd.workspace = ext_ws_ ? ext_ws_ : ws<float>(static_cast<int>(ws_off_.size()) - 1);
+  const bool side = ls_ == s2_;   // each stream has its own split-K partials
+  dd.workspace = ext_ws_ ? ext_ws_ + (side ? gemm_ws_bytes_ / 4 : 0)
+                         : ws<float>(static_cast<int>(ws_off_.size()) - (side ? 1 : 2));
   dd.workspace_bytes = gemm_ws_bytes_;
   if (!dt_) {
-    LAUNCH(gemm_f32_kernel_name(dd), flops, bytes, gemm_f32(dd, s_));
+    LAUNCH(gemm_f32_kernel_name(dd), flops, bytes, gemm_f32(dd, ls_));
     return;
   }
   if (defer) {
@@ -226,7 +228,7 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
       dd.workspace = defer_ + defer_used_;
       dd.workspace_bytes = static_cast<size_t>(splits * mn) * 4;
       // the partial planes replace the g write: splits - 1 planes more
-      LAUNCH_X(gemm_bf16_kernel_name(dd), flops, bytes, 4.0 * (splits - 1) * mn, gemm_bf16(dd, s_, GEMM_MAIN));
+      LAUNCH_X(gemm_bf16_kernel_name(dd), flops, bytes, 4.0 * (splits - 1) * mn, gemm_bf16(dd, ls_, GEMM_MAIN));
       UpdateSegment sg;
       sg.off = off;
       sg.n = mn;
@@ -241,14 +243,35 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
   const double mn = static_cast<double>(d.M) * d.N * d.batch;
   // with a K split the GEMM writes float32 partial planes instead of the output
   LAUNCH_X(gemm_bf16_kernel_name(dd), flops, bytes, splits > 1 ? 4.0 * splits * mn : 0.0,
-           gemm_bf16(dd, s_, GEMM_MAIN));
+           gemm_bf16(dd, ls_, GEMM_MAIN));
   if (splits > 1) {
     // the reduction's own traffic: partials read once, output written once
     // (read too when accumulating), epilogue operands read once
     const double out = d.epi.out_f32 ? 4.0 : 2.0;
     const double rbytes = mn * (4.0 * splits + out * (d.epi.accumulate ? 2 : 1));
-    LAUNCH(gemm_bf16_reduce_name(dd), 0, rbytes, gemm_bf16(dd, s_, GEMM_REDUCE));
+    LAUNCH(gemm_bf16_reduce_name(dd), 0, rbytes, gemm_bf16(dd, ls_, GEMM_REDUCE));
   }
+}
+
+void Stage::side_gemm(const GemmDesc& d) {
+  hip_check(hipEventRecord(fork_ev_, s_), "hipEventRecord");
+  hip_check(hipStreamWaitEvent(s2_, fork_ev_, 0), "hipStreamWaitEvent");
+  ls_ = s2_;
+  try {
+    gemm(d);
+  } catch (...) {
+    ls_ = s_;
+    throw;
+  }
+  ls_ = s_;
+  side_pending_ = true;
+}
+
+void Stage::join_side() {
+  if (!side_pending_) return;
+  hip_check(hipEventRecord(join_ev_, s2_), "hipEventRecord");
+  hip_check(hipStreamWaitEvent(s_, join_ev_, 0), "hipStreamWaitEvent");
+  side_pending_ = false;
 }
 
 // ------------------------------------------------------------ profiling ----
@@ -400,7 +423,8 @@ void Stage::plan_buffers() {
     }
   }
   ws.push_back(static_cast<size_t>(std::max<long>(partial, 1) * 4));  // column-sum partials
-  ws.push_back(std::max<size_t>(gemm_ws_bytes_, 1));                   // split-K partials: last id
+  ws.push_back(std::max<size_t>(gemm_ws_bytes_, 1));                   // split-K partials, stage stream
+  ws.push_back(std::max<size_t>(gemm_ws_bytes_, 1));                   // split-K partials, side stream: last id
   if (defer_cap_ > 0) {
     const size_t o = defer_block_.add(static_cast<size_t>(defer_cap_) * 4);
     defer_block_.allocate();
@@ -496,6 +520,10 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
   if (!W0) fail("W0_host is NULL");
 
   hip_check(hipGetDevice(&device_), "hipGetDevice");
+  ls_ = s_;
+  hip_check(hipStreamCreateWithFlags(&s2_, hipStreamNonBlocking), "hipStreamCreate");
+  hip_check(hipEventCreateWithFlags(&fork_ev_, hipEventDisableTiming), "hipEventCreate");
+  hip_check(hipEventCreateWithFlags(&join_ev_, hipEventDisableTiming), "hipEventCreate");
   // arenas: W, v, g (float32), two predicted slots (operand dtype), all padded
   size_t oW = arena_.add(n_arena_ * 4), ov = arena_.add(n_arena_ * 4), og = arena_.add(n_arena_ * 4);
   size_t of = arena_.add(n_arena_ * esz_), ob = arena_.add(n_arena_ * esz_);
@@ -526,7 +554,11 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
 
 Stage::~Stage() {
   (void)hipStreamSynchronize(s_);
+  if (s2_) (void)hipStreamSynchronize(s2_);
   for (hipEvent_t e : prof_pool_) (void)hipEventDestroy(e);
+  if (fork_ev_) (void)hipEventDestroy(fork_ev_);
+  if (join_ev_) (void)hipEventDestroy(join_ev_);
+  if (s2_) (void)hipStreamDestroy(s2_);
 }
 
 void Stage::sync() { hip_check(hipStreamSynchronize(s_), "hipStreamSynchronize"); }
@@ -668,20 +700,26 @@ void Stage::backward(int64_t mb, const void* dy, void* dx) {
   bwd_weights_ = d_.weight_policy == SPECTRAIN_POLICY_STASH ? wstash_.at<char>(wstash_off_[slot]) : what_[1];
   defer_segs_.clear();
   defer_used_ = 0;
-  switch (d_.kind) {
-    case SPECTRAIN_KIND_FC: bwd_fc(slot, dy, dx); break;
-    case SPECTRAIN_KIND_CONV3X3: bwd_conv(slot, dy, dx); break;
-    case SPECTRAIN_KIND_BOTTLENECK: bwd_bneck(slot, dy, dx); break;
-    case SPECTRAIN_KIND_TRANSFORMER: bwd_tfm(slot, dy, dx); break;
-    case SPECTRAIN_KIND_RESLSTM: bwd_lstm(slot, dy, dx); break;
+  try {
+    switch (d_.kind) {
+      case SPECTRAIN_KIND_FC: bwd_fc(slot, dy, dx); break;
+      case SPECTRAIN_KIND_CONV3X3: bwd_conv(slot, dy, dx); break;
+      case SPECTRAIN_KIND_BOTTLENECK: bwd_bneck(slot, dy, dx); break;
+      case SPECTRAIN_KIND_TRANSFORMER: bwd_tfm(slot, dy, dx); break;
+      case SPECTRAIN_KIND_RESLSTM: bwd_lstm(slot, dy, dx); break;
+    }
+  } catch (...) {
+    join_side();
+    throw;
   }
+  join_side();   // the side stream's gradients are complete before anything later on the stage stream
   slots_[slot] = Slot{};
   g_pending_ = true;
 }
 
 void Stage::backward_noalloc(int64_t mb, const void* dy, void* dx) {
-  if (gemm_ws_bytes_ > SCRATCH_BYTES)
-    fail("the stage's split-K workspace (" + std::to_string(gemm_ws_bytes_) + " bytes) exceeds the " +
+  if (2 * gemm_ws_bytes_ > SCRATCH_BYTES)
+    fail("the stage's two split-K workspaces (" + std::to_string(2 * gemm_ws_bytes_) + " bytes) exceed the " +
          std::to_string(SCRATCH_BYTES) + "-byte scratch of the allocation-free backward");
   float* scratch = device_scratch(device_);
   ext_ws_ = scratch;
@@ -806,7 +844,7 @@ void Stage::pool_head_bwd(int slot, const void* yl, int HW, int C, int t, int id
   gw.epi.out_f32 = grad(t);
   gemm(gw);
   LAUNCH("bias_grad", 0, colsum_bytes(B, V, 2),
-         column_sum(dl, 1, B, V, V, grad(t + 1), 0, ws<float>(static_cast<int>(ws_off_.size()) - 2), s_));
+         column_sum(dl, 1, B, V, V, grad(t + 1), 0, ws<float>(static_cast<int>(ws_off_.size()) - 3), s_));
   bf16_t* dpool = ws<bf16_t>(wsl + 2);
   GemmDesc gx = gd(B, C, V, opK(dl, V), opR(wb(t), C), C);
   gx.epi.out_bf16 = dpool;
@@ -910,6 +948,11 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
     pool_head_bwd(slot, stash<void>(slot, 3 * (L - 1) + 2), H * W, C, 3 * L, 3 * L, 3 * L + 1, 4, ws<void>(0));
   else
     LAUNCH("mask", 0, 6.0 * P * C, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * C, 1, s_));
+  // The data gradients (d3, d2, d1) form the chain on the stage stream; each
+  // weight gradient (g3, g2, g1, with its split-K reduction) runs on the side
+  // stream as soon as its input is produced. The next block's d3 rewrites
+  // dt2 (read by g2), then d2 rewrites dt1 (g1) and d1 the previous dr (g3):
+  // the stage stream joins the side stream before it.
   int cur = 0;
   bf16_t* dt2 = ws<bf16_t>(2);
   bf16_t* dt1 = ws<bf16_t>(3);
@@ -917,16 +960,17 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
     const bf16_t* dr = ws<bf16_t>(cur);
     const bf16_t* t1 = stash<bf16_t>(slot, 3 * l);
     const bf16_t* t2 = stash<bf16_t>(slot, 3 * l + 1);
+    join_side();
     GemmDesc g3 = gd(C, Cm, P, opR(dr, C), opR(t2, Cm), Cm);
     g3.epi.out_f32 = grad(3 * l + 2);
-    gemm(g3);
+    side_gemm(g3);
     GemmDesc d3 = gd(P, Cm, C, opK(dr, C), opR(wb(3 * l + 2), Cm), Cm);
     d3.epi.out_bf16 = dt2;
     d3.epi.mask = t2;
     gemm(d3);
     GemmDesc g2 = gd(Cm, 9 * Cm, P, opR(dt2, Cm), opConv(OP_R_CONV_WGRAD, t1, B, H, W, Cm), 9 * Cm);
     g2.epi.out_f32 = grad(3 * l + 1);
-    gemm(g2);
+    side_gemm(g2);
     GemmDesc d2 = gd(P, Cm, 9 * Cm, opConv(OP_K_CONV_DGRAD, dt2, B, H, W, Cm),
                      opConv(OP_R_FILTER_T, wb(3 * l + 1), B, H, W, Cm, Cm), Cm);
     d2.epi.out_bf16 = dt1;
@@ -934,7 +978,7 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
     gemm(d2);
     GemmDesc g1 = gd(Cm, C, P, opR(dt1, Cm), opR(xin(l), C), C);
     g1.epi.out_f32 = grad(3 * l);
-    gemm(g1);
+    side_gemm(g1);
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(cur ^ 1);
     GemmDesc d1 = gd(P, C, Cm, opK(dt1, Cm), opR(wb(3 * l), C), C);

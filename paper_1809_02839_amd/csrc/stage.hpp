@@ -29,7 +29,7 @@ void hip_check(hipError_t e, const char* what);
 // Bytes of the per-device scratch array of the allocation-free backward: the
 // split-K workspace of a bf16 stage, so both backward entry points split
 // every GEMM alike and give bitwise identical results.
-constexpr size_t SCRATCH_BYTES = SPECTRAIN_NOALLOC_SCRATCH_BYTES;
+constexpr size_t SCRATCH_BYTES = SPECTRAIN_NOALLOC_SCRATCH_BYTES;   // two halves: stage stream, side stream
 // Device address of that array on `device` (looked up on first use, cached).
 float* device_scratch(int device);
 
@@ -120,6 +120,13 @@ class Stage {
   // store into g); when it splits K, its partials stay in the deferred buffer
   // and the update sums them instead of a separate reduction pass.
   void gemm(const GemmDesc& d, bool defer = false);
+  // A weight-gradient GEMM on the side stream: it waits for everything issued
+  // on the stage stream so far (its inputs) and runs beside the data-gradient
+  // chain that follows; join_side() makes the stage stream wait for all of
+  // the side stream's work (before a buffer those GEMMs read is rewritten,
+  // and at the end of every backward).
+  void side_gemm(const GemmDesc& d);
+  void join_side();
 
   // Launch wrapper: checks the launch status and, while profiling, brackets
   // the launch with events on the stage's stream.
@@ -130,9 +137,9 @@ class Stage {
       return;
     }
     hipEvent_t a = prof_event(), b = prof_event();
-    hip_check(hipEventRecord(a, s_), "hipEventRecord");
+    hip_check(hipEventRecord(a, ls_), "hipEventRecord");
     hip_check(launch(), family);
-    hip_check(hipEventRecord(b, s_), "hipEventRecord");
+    hip_check(hipEventRecord(b, ls_), "hipEventRecord");
     auto it = prof_index_.find(family);
     int fam;
     if (it == prof_index_.end()) {
@@ -190,6 +197,10 @@ class Stage {
   std::vector<size_t> ws_off_;
   size_t gemm_ws_bytes_ = 0;
   float* ext_ws_ = nullptr;              // split-K partials of the current call, when not the workspace
+  hipStream_t s2_ = nullptr;             // side stream (weight gradients), default priority
+  hipStream_t ls_ = nullptr;             // stream of the launch being issued: s_ or s2_
+  hipEvent_t fork_ev_ = nullptr, join_ev_ = nullptr;
+  bool side_pending_ = false;
   int device_ = -1;                      // device current at create (the stream's device)
   bool g_pending_ = false;
   DeviceBlock defer_block_;              // split-K partials of gradients the update reduces
