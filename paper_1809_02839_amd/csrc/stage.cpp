@@ -253,7 +253,7 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
   }
 }
 
-void Stage::side_gemm(const GemmDesc& d) {
+void Stage::side_gemm(const GemmDesc& d, std::initializer_list<const void*> reads) {
   hip_check(hipEventRecord(fork_ev_, s_), "hipEventRecord");
   hip_check(hipStreamWaitEvent(s2_, fork_ev_, 0), "hipStreamWaitEvent");
   ls_ = s2_;
@@ -265,9 +265,24 @@ void Stage::side_gemm(const GemmDesc& d) {
   }
   ls_ = s_;
   side_pending_ = true;
+  // completion event of this GEMM for the buffers it reads; a ring entry is
+  // recorded again only after many later side GEMMs, and a wait enqueued
+  // earlier already refers to the record it saw
+  hipEvent_t ev = side_ev_[side_next_];
+  side_next_ = (side_next_ + 1) % side_ev_.size();
+  hip_check(hipEventRecord(ev, s2_), "hipEventRecord");
+  for (const void* b : reads) side_reads_[b] = ev;
+}
+
+void Stage::protect(const void* buf) {
+  auto it = side_reads_.find(buf);
+  if (it == side_reads_.end()) return;
+  hip_check(hipStreamWaitEvent(s_, it->second, 0), "hipStreamWaitEvent");
+  side_reads_.erase(it);
 }
 
 void Stage::join_side() {
+  side_reads_.clear();
   if (!side_pending_) return;
   hip_check(hipEventRecord(join_ev_, s2_), "hipEventRecord");
   hip_check(hipStreamWaitEvent(s_, join_ev_, 0), "hipStreamWaitEvent");
@@ -524,6 +539,8 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
   hip_check(hipStreamCreateWithFlags(&s2_, hipStreamNonBlocking), "hipStreamCreate");
   hip_check(hipEventCreateWithFlags(&fork_ev_, hipEventDisableTiming), "hipEventCreate");
   hip_check(hipEventCreateWithFlags(&join_ev_, hipEventDisableTiming), "hipEventCreate");
+  side_ev_.resize(32, nullptr);
+  for (hipEvent_t& e : side_ev_) hip_check(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreate");
   // arenas: W, v, g (float32), two predicted slots (operand dtype), all padded
   size_t oW = arena_.add(n_arena_ * 4), ov = arena_.add(n_arena_ * 4), og = arena_.add(n_arena_ * 4);
   size_t of = arena_.add(n_arena_ * esz_), ob = arena_.add(n_arena_ * esz_);
@@ -558,6 +575,8 @@ Stage::~Stage() {
   for (hipEvent_t e : prof_pool_) (void)hipEventDestroy(e);
   if (fork_ev_) (void)hipEventDestroy(fork_ev_);
   if (join_ev_) (void)hipEventDestroy(join_ev_);
+  for (hipEvent_t e : side_ev_)
+    if (e) (void)hipEventDestroy(e);
   if (s2_) (void)hipStreamDestroy(s2_);
 }
 
@@ -950,9 +969,9 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
     LAUNCH("mask", 0, 6.0 * P * C, mask_relu_grad(dy, sl.y, ws<void>(0), static_cast<long>(P) * C, 1, s_));
   // The data gradients (d3, d2, d1) form the chain on the stage stream; each
   // weight gradient (g3, g2, g1, with its split-K reduction) runs on the side
-  // stream as soon as its input is produced. The next block's d3 rewrites
-  // dt2 (read by g2), then d2 rewrites dt1 (g1) and d1 the previous dr (g3):
-  // the stage stream joins the side stream before it.
+  // stream as soon as its input is produced. Before the chain rewrites a
+  // workspace buffer (the next block's dt2, dt1, or the dr two blocks back)
+  // it waits for the side GEMM that reads it.
   int cur = 0;
   bf16_t* dt2 = ws<bf16_t>(2);
   bf16_t* dt1 = ws<bf16_t>(3);
@@ -960,27 +979,29 @@ void Stage::bwd_bneck(int slot, const void* dy, void* dx) {
     const bf16_t* dr = ws<bf16_t>(cur);
     const bf16_t* t1 = stash<bf16_t>(slot, 3 * l);
     const bf16_t* t2 = stash<bf16_t>(slot, 3 * l + 1);
-    join_side();
     GemmDesc g3 = gd(C, Cm, P, opR(dr, C), opR(t2, Cm), Cm);
     g3.epi.out_f32 = grad(3 * l + 2);
-    side_gemm(g3);
+    side_gemm(g3, {dr});
     GemmDesc d3 = gd(P, Cm, C, opK(dr, C), opR(wb(3 * l + 2), Cm), Cm);
     d3.epi.out_bf16 = dt2;
     d3.epi.mask = t2;
+    protect(dt2);
     gemm(d3);
     GemmDesc g2 = gd(Cm, 9 * Cm, P, opR(dt2, Cm), opConv(OP_R_CONV_WGRAD, t1, B, H, W, Cm), 9 * Cm);
     g2.epi.out_f32 = grad(3 * l + 1);
-    side_gemm(g2);
+    side_gemm(g2, {dt2});
     GemmDesc d2 = gd(P, Cm, 9 * Cm, opConv(OP_K_CONV_DGRAD, dt2, B, H, W, Cm),
                      opConv(OP_R_FILTER_T, wb(3 * l + 1), B, H, W, Cm, Cm), Cm);
     d2.epi.out_bf16 = dt1;
     d2.epi.mask = t1;
+    protect(dt1);
     gemm(d2);
     GemmDesc g1 = gd(Cm, C, P, opR(dt1, Cm), opR(xin(l), C), C);
     g1.epi.out_f32 = grad(3 * l);
-    side_gemm(g1);
+    side_gemm(g1, {dt1});
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(cur ^ 1);
+    protect(out);
     GemmDesc d1 = gd(P, C, Cm, opK(dt1, Cm), opR(wb(3 * l), C), C);
     d1.epi.res_bf16 = dr;
     d1.epi.out_bf16 = static_cast<bf16_t*>(out);
@@ -1125,35 +1146,39 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     bf16_t* dctx = ws<bf16_t>(8);
     bf16_t* dqkv = ws<bf16_t>(9);
 
+    protect(dr2);
     LAUNCH("layernorm_bwd", 0, lnb_bytes(T, d), layernorm_bwd(static_cast<const bf16_t*>(gy), r2, stash<float>(slot, q + 10), stash<float>(slot, q + 11),
                             static_cast<const bf16_t*>(wb(p + 10)), T, d, dr2, grad(p + 10), grad(p + 11), grad(p + 9),
                             part, s_));   // also the FFN output bias gradient: column sums of dr2
     GemmDesc w2 = gd(d, F, T, opR(dr2, d), opR(f1, F), F);
     w2.epi.out_f32 = grad(p + 8);
-    gemm(w2);
+    side_gemm(w2, {dr2});
     GemmDesc x2 = gd(T, F, d, opK(dr2, d), opR(wb(p + 8), F), F);
     x2.epi.mask = f1;
     x2.epi.out_bf16 = df1;
+    protect(df1);
     gemm(x2);
     GemmDesc w1 = gd(F, d, T, opR(df1, F), opR(h, d), d);
     w1.epi.out_f32 = grad(p + 6);
-    gemm(w1);
+    side_gemm(w1, {df1});
     LAUNCH("bias_grad", 0, colsum_bytes(T, F, 2), column_sum(df1, 1, T, F, F, grad(p + 7), 0, part, s_));
     GemmDesc x1 = gd(T, d, F, opK(df1, F), opR(wb(p + 6), d), d);
     x1.epi.res_bf16 = dr2;
     x1.epi.out_bf16 = dhh;
     gemm(x1);
+    protect(dr1);
     LAUNCH("layernorm_bwd", 0, lnb_bytes(T, d), layernorm_bwd(dhh, r1, stash<float>(slot, q + 5), stash<float>(slot, q + 6),
                             static_cast<const bf16_t*>(wb(p + 4)), T, d, dr1, grad(p + 4), grad(p + 5), grad(p + 3),
                             part, s_));   // also the attention output bias gradient: column sums of dr1
     GemmDesc wo = gd(d, d, T, opR(dr1, d), opR(ctx, d), d);
     wo.epi.out_f32 = grad(p + 2);
-    gemm(wo);
+    side_gemm(wo, {dr1});
     GemmDesc xo = gd(T, d, d, opK(dr1, d), opR(wb(p + 2), d), d);
     xo.epi.out_bf16 = dctx;
     gemm(xo);
 
     // attention backward: fused, or batched GEMMs over (b, h)
+    protect(dqkv);
     if (attention_fused_supported(S, dh, d)) {
       LAUNCH("attention_bwd", 10.0 * B * Hh * S * S * dh, 2.0 * T * 7 * d + 8.0 * B * Hh * S,
              attention_bwd(qkv, dctx, P, B, Hh, d, scale, dqkv, s_));
@@ -1222,10 +1247,11 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     }
     GemmDesc wq = gd(3 * d, d, T, opR(dqkv, 3 * d), opR(a, d), d);
     wq.epi.out_f32 = grad(p);
-    gemm(wq);
+    side_gemm(wq, {dqkv, a});
     LAUNCH("bias_grad", 0, colsum_bytes(T, 3 * d, 2), column_sum(dqkv, 1, T, 3 * d, 3 * d, grad(p + 1), 0, part, s_));
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
+    protect(out);
     GemmDesc xq = gd(T, d, 3 * d, opK(dqkv, 3 * d), opR(wb(p), d), d);
     xq.epi.res_bf16 = dr1;
     xq.epi.out_bf16 = static_cast<bf16_t*>(out);

@@ -4,6 +4,7 @@
 
 #include <cstdint>
 #include <cstdio>
+#include <initializer_list>
 #include <map>
 #include <stdexcept>
 #include <string>
@@ -125,8 +126,11 @@ class Stage {
   // chain that follows; join_side() makes the stage stream wait for all of
   // the side stream's work (before a buffer those GEMMs read is rewritten,
   // and at the end of every backward).
-  void side_gemm(const GemmDesc& d);
+  void side_gemm(const GemmDesc& d, std::initializer_list<const void*> reads);
   void join_side();
+  // The stage stream waits for the side-stream GEMMs that read `buf` before
+  // it is rewritten (no-op when none is pending).
+  void protect(const void* buf);
 
   // Launch wrapper: checks the launch status and, while profiling, brackets
   // the launch with events on the stage's stream.
@@ -201,6 +205,9 @@ class Stage {
   hipStream_t ls_ = nullptr;             // stream of the launch being issued: s_ or s2_
   hipEvent_t fork_ev_ = nullptr, join_ev_ = nullptr;
   bool side_pending_ = false;
+  std::vector<hipEvent_t> side_ev_;      // completion events of side GEMMs (a ring)
+  size_t side_next_ = 0;
+  std::map<const void*, hipEvent_t> side_reads_;   // buffer -> last side GEMM reading it
   int device_ = -1;                      // device current at create (the stream's device)
   bool g_pending_ = false;
   DeviceBlock defer_block_;              // split-K partials of gradients the update reduces
