@@ -364,7 +364,7 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="resnet_bottleneck", choices=sorted(DESCRIPTIONS))
-    ap.add_argument("--profile-steps", type=int, default=20)
+    ap.add_argument("--profile-steps", type=int, default=50)
     ap.add_argument("--cpu-steps", type=int, default=3,
                     help="oracle steps timed for cpu_baseline (the median step is reported)")
     ap.add_argument("--cpu-layers", type=int, default=0,
