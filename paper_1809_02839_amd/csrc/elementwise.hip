@@ -742,9 +742,8 @@ hipError_t layernorm_fwd(const bf16_t* r, const bf16_t* gamma, const bf16_t* bet
   return hipGetLastError();
 }
 
-hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd, const bf16_t* gamma,
-                         int R, int D, bf16_t* dr, float* dgamma, float* dbeta, float* dsum, float* partial_ws,
-                         hipStream_t s) {
+hipError_t layernorm_bwd_rows(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd,
+                              const bf16_t* gamma, int R, int D, bf16_t* dr, float* partial_ws, hipStream_t s) {
   if (D % 64 || D > 64 * 32) return hipErrorInvalidValue;
   const int nb = (R + LNB_ROWS - 1) / LNB_ROWS;
   const dim3 grid(nb), block(NT);
@@ -758,6 +757,13 @@ hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, c
     case 32: hipLaunchKernelGGL(layernorm_bwd_kernel<32>, grid, block, 0, s, dy, r, mean, rstd, gamma, R, D, dr, p); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t layernorm_bwd_params(const float* partial_ws, int R, int D, float* dgamma, float* dbeta, float* dsum,
+                                hipStream_t s) {
+  const int nb = (R + LNB_ROWS - 1) / LNB_ROWS;
+  const float* p = partial_ws;
   // partial columns [0, D) sum dr, [D, 2D) dgamma, [2D, 3D) dbeta
   if (dsum && dsum + D == dgamma && dgamma + D == dbeta) {
     hipLaunchKernelGGL(colsum_final_kernel, dim3((3 * D + 15) / 16), dim3(256), 0, s, p, nb, 3 * D, dsum, 0);
@@ -769,6 +775,14 @@ hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, c
       hipLaunchKernelGGL(colsum_strided_final_kernel, dim3((D + 15) / 16), dim3(256), 0, s, p + i * D, nb, D, 3 * D,
                          out[i]);
   return hipGetLastError();
+}
+
+hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd, const bf16_t* gamma,
+                         int R, int D, bf16_t* dr, float* dgamma, float* dbeta, float* dsum, float* partial_ws,
+                         hipStream_t s) {
+  const hipError_t e = layernorm_bwd_rows(dy, r, mean, rstd, gamma, R, D, dr, partial_ws, s);
+  if (e != hipSuccess) return e;
+  return layernorm_bwd_params(partial_ws, R, D, dgamma, dbeta, dsum, s);
 }
 
 hipError_t softmax_rows(const float* S, int R, int C, float* P, bf16_t* Pb, hipStream_t s) {

@@ -169,6 +169,13 @@ hipError_t layernorm_fwd(const bf16_t* r, const bf16_t* gamma, const bf16_t* bet
 hipError_t layernorm_bwd(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd,
                          const bf16_t* gamma, int R, int D, bf16_t* dr, float* dgamma, float* dbeta, float* dsum,
                          float* partial_ws, hipStream_t s);
+// The same in two launches: the rows (dr and the per-block partials in
+// partial_ws), then the reduction of the partials into dgamma, dbeta and dsum
+// (which may be on another stream once the first has completed).
+hipError_t layernorm_bwd_rows(const bf16_t* dy, const bf16_t* r, const float* mean, const float* rstd,
+                              const bf16_t* gamma, int R, int D, bf16_t* dr, float* partial_ws, hipStream_t s);
+hipError_t layernorm_bwd_params(const float* partial_ws, int R, int D, float* dgamma, float* dbeta, float* dsum,
+                                hipStream_t s);
 // Row softmax of float32 scores [R, C] -> P float32 and bf16(P).
 hipError_t softmax_rows(const float* S, int R, int C, float* P, bf16_t* Pb, hipStream_t s);
 // Softmax backward: dS = bf16(P * (dP - sum_j P dP)) per row.

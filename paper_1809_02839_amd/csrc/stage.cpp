@@ -98,7 +98,10 @@ void fail(const std::string& m) { throw StageError(SPECTRAIN_EINVAL, m); }
 double ce_bytes(double R, double C) { return R * C * (4.0 + 2.0) + R * 8.0; }   // scores, gradient, label, loss
 double colsum_bytes(double R, double C, double esz) { return R * C * esz + C * 4.0; }
 double ln_bytes(double R, double D) { return R * D * 4.0 + R * 8.0 + D * 4.0; }  // r in, y out (bf16), stats
-double lnb_bytes(double R, double D) { return R * D * 6.0 + R * 8.0 + D * 14.0; }  // dy, r in, dr out; 3 sums
+double lnb_rows_bytes(double R, double D) { return R * D * 6.0 + R * 8.0 + D * 2.0; }   // dy, r in, dr out, stats
+double lnb_params_bytes(double R, double D) {   // per-block partials of 3 column sums in, 3 sums out
+  return 12.0 * D * ((R + LNB_ROWS - 1) / LNB_ROWS) + 12.0 * D;
+}
 
 }  // namespace
 
@@ -209,8 +212,7 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
   const double bytes = gemm_algorithmic_bytes(d, esz_);
   GemmDesc dd = d;
   const bool side = ls_ == s2_;   // each stream has its own split-K partials
-  dd.workspace = ext_ws_ ? ext_ws_ + (side ? gemm_ws_bytes_ / 4 : 0)
-                         : ws<float>(static_cast<int>(ws_off_.size()) - (side ? 1 : 2));
+  dd.workspace = ext_ws_ ? ext_ws_ + (side ? gemm_ws_bytes_ / 4 : 0) : ws<float>(side ? ws_split2_ : ws_split_);
   dd.workspace_bytes = gemm_ws_bytes_;
   if (!dt_) {
     LAUNCH(gemm_f32_kernel_name(dd), flops, bytes, gemm_f32(dd, ls_));
@@ -254,24 +256,7 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
 }
 
 void Stage::side_gemm(const GemmDesc& d, std::initializer_list<const void*> reads) {
-  hip_check(hipEventRecord(fork_ev_, s_), "hipEventRecord");
-  hip_check(hipStreamWaitEvent(s2_, fork_ev_, 0), "hipStreamWaitEvent");
-  ls_ = s2_;
-  try {
-    gemm(d);
-  } catch (...) {
-    ls_ = s_;
-    throw;
-  }
-  ls_ = s_;
-  side_pending_ = true;
-  // completion event of this GEMM for the buffers it reads; a ring entry is
-  // recorded again only after many later side GEMMs, and a wait enqueued
-  // earlier already refers to the record it saw
-  hipEvent_t ev = side_ev_[side_next_];
-  side_next_ = (side_next_ + 1) % side_ev_.size();
-  hip_check(hipEventRecord(ev, s2_), "hipEventRecord");
-  for (const void* b : reads) side_reads_[b] = ev;
+  on_side(reads, [&]() { gemm(d); });
 }
 
 void Stage::protect(const void* buf) {
@@ -437,9 +422,14 @@ void Stage::plan_buffers() {
       break;
     }
   }
-  ws.push_back(static_cast<size_t>(std::max<long>(partial, 1) * 4));  // column-sum partials
+  ws_colsum_ = static_cast<int>(ws.size());
+  ws.push_back(static_cast<size_t>(std::max<long>(partial, 1) * 4));  // column-sum partials, stage stream
+  ws_colsum2_ = static_cast<int>(ws.size());
+  ws.push_back(static_cast<size_t>(std::max<long>(partial, 1) * 4));  // column-sum partials, side stream
+  ws_split_ = static_cast<int>(ws.size());
   ws.push_back(std::max<size_t>(gemm_ws_bytes_, 1));                   // split-K partials, stage stream
-  ws.push_back(std::max<size_t>(gemm_ws_bytes_, 1));                   // split-K partials, side stream: last id
+  ws_split2_ = static_cast<int>(ws.size());
+  ws.push_back(std::max<size_t>(gemm_ws_bytes_, 1));                   // split-K partials, side stream
   if (defer_cap_ > 0) {
     const size_t o = defer_block_.add(static_cast<size_t>(defer_cap_) * 4);
     defer_block_.allocate();
@@ -800,7 +790,7 @@ void Stage::bwd_fc(int slot, const void* dy, void* dx) {
     GemmDesc gw = gd(fout, fin, B, opR(dz, fout), opR(act(l), fin), fin);
     gw.epi.out_f32 = grad(2 * l);
     gemm(gw);
-    LAUNCH("bias_grad", 0, colsum_bytes(B, fout, esz_), column_sum(dz, dt_, B, fout, fout, grad(2 * l + 1), 0, ws<float>(4), s_));
+    LAUNCH("bias_grad", 0, colsum_bytes(B, fout, esz_), column_sum(dz, dt_, B, fout, fout, grad(2 * l + 1), 0, ws<float>(ws_colsum_), s_));
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
     GemmDesc gx = gd(B, fin, fout, opK(dz, fout), opR(wb(2 * l), fin), fin);
@@ -863,7 +853,7 @@ void Stage::pool_head_bwd(int slot, const void* yl, int HW, int C, int t, int id
   gw.epi.out_f32 = grad(t);
   gemm(gw);
   LAUNCH("bias_grad", 0, colsum_bytes(B, V, 2),
-         column_sum(dl, 1, B, V, V, grad(t + 1), 0, ws<float>(static_cast<int>(ws_off_.size()) - 3), s_));
+         column_sum(dl, 1, B, V, V, grad(t + 1), 0, ws<float>(ws_colsum_), s_));
   bf16_t* dpool = ws<bf16_t>(wsl + 2);
   GemmDesc gx = gd(B, C, V, opK(dl, V), opR(wb(t), C), C);
   gx.epi.out_bf16 = dpool;
@@ -1111,7 +1101,8 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
   const int T = B * S, dh = d / Hh;
   const float scale = 1.0f / std::sqrt(static_cast<float>(dh));
   const Slot& sl = slots_[slot];
-  float* part = ws<float>(12);
+  float* part = ws<float>(ws_colsum_);
+  float* part2 = ws<float>(ws_colsum2_);
   const void* gy = dy;
   int pp = 2;
   if (d_.head == SPECTRAIN_HEAD_CE) {   // vocabulary head: its gradients and dY of the last layer
@@ -1146,10 +1137,18 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     bf16_t* dctx = ws<bf16_t>(8);
     bf16_t* dqkv = ws<bf16_t>(9);
 
+    // layer-norm backward rows on the stage stream; its parameter gradients
+    // (and the FFN output bias gradient: column sums of dr2) reduced from the
+    // per-block partials on the side stream
     protect(dr2);
-    LAUNCH("layernorm_bwd", 0, lnb_bytes(T, d), layernorm_bwd(static_cast<const bf16_t*>(gy), r2, stash<float>(slot, q + 10), stash<float>(slot, q + 11),
-                            static_cast<const bf16_t*>(wb(p + 10)), T, d, dr2, grad(p + 10), grad(p + 11), grad(p + 9),
-                            part, s_));   // also the FFN output bias gradient: column sums of dr2
+    protect(part);
+    LAUNCH("layernorm_bwd", 0, lnb_rows_bytes(T, d),
+           layernorm_bwd_rows(static_cast<const bf16_t*>(gy), r2, stash<float>(slot, q + 10), stash<float>(slot, q + 11),
+                              static_cast<const bf16_t*>(wb(p + 10)), T, d, dr2, part, s_));
+    on_side({part}, [&]() {
+      LAUNCH("layernorm_bwd_params", 0, lnb_params_bytes(T, d),
+             layernorm_bwd_params(part, T, d, grad(p + 10), grad(p + 11), grad(p + 9), ls_));
+    });
     GemmDesc w2 = gd(d, F, T, opR(dr2, d), opR(f1, F), F);
     w2.epi.out_f32 = grad(p + 8);
     side_gemm(w2, {dr2});
@@ -1161,15 +1160,22 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     GemmDesc w1 = gd(F, d, T, opR(df1, F), opR(h, d), d);
     w1.epi.out_f32 = grad(p + 6);
     side_gemm(w1, {df1});
-    LAUNCH("bias_grad", 0, colsum_bytes(T, F, 2), column_sum(df1, 1, T, F, F, grad(p + 7), 0, part, s_));
+    on_side({df1}, [&]() {
+      LAUNCH("bias_grad", 0, colsum_bytes(T, F, 2), column_sum(df1, 1, T, F, F, grad(p + 7), 0, part2, ls_));
+    });
     GemmDesc x1 = gd(T, d, F, opK(df1, F), opR(wb(p + 6), d), d);
     x1.epi.res_bf16 = dr2;
     x1.epi.out_bf16 = dhh;
     gemm(x1);
     protect(dr1);
-    LAUNCH("layernorm_bwd", 0, lnb_bytes(T, d), layernorm_bwd(dhh, r1, stash<float>(slot, q + 5), stash<float>(slot, q + 6),
-                            static_cast<const bf16_t*>(wb(p + 4)), T, d, dr1, grad(p + 4), grad(p + 5), grad(p + 3),
-                            part, s_));   // also the attention output bias gradient: column sums of dr1
+    protect(part);
+    LAUNCH("layernorm_bwd", 0, lnb_rows_bytes(T, d),
+           layernorm_bwd_rows(dhh, r1, stash<float>(slot, q + 5), stash<float>(slot, q + 6),
+                              static_cast<const bf16_t*>(wb(p + 4)), T, d, dr1, part, s_));
+    on_side({part}, [&]() {   // also the attention output bias gradient: column sums of dr1
+      LAUNCH("layernorm_bwd_params", 0, lnb_params_bytes(T, d),
+             layernorm_bwd_params(part, T, d, grad(p + 4), grad(p + 5), grad(p + 3), ls_));
+    });
     GemmDesc wo = gd(d, d, T, opR(dr1, d), opR(ctx, d), d);
     wo.epi.out_f32 = grad(p + 2);
     side_gemm(wo, {dr1});
@@ -1248,7 +1254,10 @@ void Stage::bwd_tfm(int slot, const void* dy, void* dx) {
     GemmDesc wq = gd(3 * d, d, T, opR(dqkv, 3 * d), opR(a, d), d);
     wq.epi.out_f32 = grad(p);
     side_gemm(wq, {dqkv, a});
-    LAUNCH("bias_grad", 0, colsum_bytes(T, 3 * d, 2), column_sum(dqkv, 1, T, 3 * d, 3 * d, grad(p + 1), 0, part, s_));
+    on_side({dqkv}, [&]() {
+      LAUNCH("bias_grad", 0, colsum_bytes(T, 3 * d, 2),
+             column_sum(dqkv, 1, T, 3 * d, 3 * d, grad(p + 1), 0, part2, ls_));
+    });
     if (l == 0 && !dx) break;
     void* out = l == 0 ? dx : ws<void>(pp);
     protect(out);
@@ -1322,7 +1331,7 @@ void Stage::bwd_lstm(int slot, const void* dy, void* dx) {
   const bool ce = d_.head == SPECTRAIN_HEAD_CE;
   const long TB = static_cast<long>(T) * B;
   const Slot& sl = slots_[slot];
-  float* part = ws<float>(9);
+  float* part = ws<float>(ws_colsum_);
   const void* du = dy;
   int pp = 2;
   if (ce) {

@@ -127,6 +127,28 @@ class Stage {
   // the side stream's work (before a buffer those GEMMs read is rewritten,
   // and at the end of every backward).
   void side_gemm(const GemmDesc& d, std::initializer_list<const void*> reads);
+  // Any launches issued by `issue` on the side stream (they launch on ls_).
+  template <typename F>
+  void on_side(std::initializer_list<const void*> reads, F&& issue) {
+    hip_check(hipEventRecord(fork_ev_, s_), "hipEventRecord");
+    hip_check(hipStreamWaitEvent(s2_, fork_ev_, 0), "hipStreamWaitEvent");
+    ls_ = s2_;
+    try {
+      issue();
+    } catch (...) {
+      ls_ = s_;
+      throw;
+    }
+    ls_ = s_;
+    side_pending_ = true;
+    // completion event for the buffers read; a ring entry is recorded again
+    // only after many later side launches, and a wait enqueued earlier
+    // already refers to the record it saw
+    hipEvent_t ev = side_ev_[side_next_];
+    side_next_ = (side_next_ + 1) % side_ev_.size();
+    hip_check(hipEventRecord(ev, s2_), "hipEventRecord");
+    for (const void* b : reads) side_reads_[b] = ev;
+  }
   void join_side();
   // The stage stream waits for the side-stream GEMMs that read `buf` before
   // it is rewritten (no-op when none is pending).
@@ -199,6 +221,9 @@ class Stage {
   std::vector<size_t> stash_bytes_;      // size of each stash buffer (0: unused for this stage)
   DeviceBlock ws_block_;
   std::vector<size_t> ws_off_;
+  // workspace ids after the kind's own buffers: column-sum partials of the
+  // stage stream and of the side stream, split-K partials of each stream
+  int ws_colsum_ = -1, ws_colsum2_ = -1, ws_split_ = -1, ws_split2_ = -1;
   size_t gemm_ws_bytes_ = 0;
   float* ext_ws_ = nullptr;              // split-K partials of the current call, when not the workspace
   hipStream_t s2_ = nullptr;             // side stream (weight gradients), default priority
