@@ -253,7 +253,8 @@ class PipeLoop:
         total = {}
         for st in self.st:
             for k, v in st.profile_read().items():
-                t = total.setdefault(k, {"launches": 0, "ms_total": 0.0, "flops_total": 0.0, "bytes_total": 0.0})
+                t = total.setdefault(k, {"launches": 0, "ms_total": 0.0, "flops_total": 0.0, "bytes_total": 0.0,
+                                     "extra_bytes_total": 0.0})
                 for f in t:
                     t[f] += v[f]
         return total

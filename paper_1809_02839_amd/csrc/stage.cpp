@@ -208,14 +208,15 @@ double gemm_algorithmic_bytes(const GemmDesc& d, size_t esz) {
 
 void Stage::gemm(const GemmDesc& d, bool defer) {
   // launch families are the kernel instantiations, as a profiler names them
+  // (names and work are only worked out while profiling: they cost host time)
   const double flops = 2.0 * d.M * d.N * static_cast<double>(d.K) * d.batch;
-  const double bytes = gemm_algorithmic_bytes(d, esz_);
+  const double bytes = prof_on_ ? gemm_algorithmic_bytes(d, esz_) : 0.0;
   GemmDesc dd = d;
   const bool side = ls_ == s2_;   // each stream has its own split-K partials
   dd.workspace = ext_ws_ ? ext_ws_ + (side ? gemm_ws_bytes_ / 4 : 0) : ws<float>(side ? ws_split2_ : ws_split_);
   dd.workspace_bytes = gemm_ws_bytes_;
   if (!dt_) {
-    LAUNCH(gemm_f32_kernel_name(dd), flops, bytes, gemm_f32(dd, ls_));
+    LAUNCH(prof_on_ ? gemm_f32_kernel_name(dd) : "gemm_f32", flops, bytes, gemm_f32(dd, ls_));
     return;
   }
   if (defer) {
@@ -230,7 +231,8 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
       dd.workspace = defer_ + defer_used_;
       dd.workspace_bytes = static_cast<size_t>(splits * mn) * 4;
       // the partial planes replace the g write: splits - 1 planes more
-      LAUNCH_X(gemm_bf16_kernel_name(dd), flops, bytes, 4.0 * (splits - 1) * mn, gemm_bf16(dd, ls_, GEMM_MAIN));
+      LAUNCH_X(prof_on_ ? gemm_bf16_kernel_name(dd) : "gemm_bf16", flops, bytes, 4.0 * (splits - 1) * mn,
+               gemm_bf16(dd, ls_, GEMM_MAIN));
       UpdateSegment sg;
       sg.off = off;
       sg.n = mn;
@@ -244,14 +246,14 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
   const int splits = gemm_bf16_splits(dd);
   const double mn = static_cast<double>(d.M) * d.N * d.batch;
   // with a K split the GEMM writes float32 partial planes instead of the output
-  LAUNCH_X(gemm_bf16_kernel_name(dd), flops, bytes, splits > 1 ? 4.0 * splits * mn : 0.0,
+  LAUNCH_X(prof_on_ ? gemm_bf16_kernel_name(dd) : "gemm_bf16", flops, bytes, splits > 1 ? 4.0 * splits * mn : 0.0,
            gemm_bf16(dd, ls_, GEMM_MAIN));
   if (splits > 1) {
     // the reduction's own traffic: partials read once, output written once
     // (read too when accumulating), epilogue operands read once
     const double out = d.epi.out_f32 ? 4.0 : 2.0;
     const double rbytes = mn * (4.0 * splits + out * (d.epi.accumulate ? 2 : 1));
-    LAUNCH(gemm_bf16_reduce_name(dd), 0, rbytes, gemm_bf16(dd, ls_, GEMM_REDUCE));
+    LAUNCH(prof_on_ ? gemm_bf16_reduce_name(dd) : "splitk_reduce", 0, rbytes, gemm_bf16(dd, ls_, GEMM_REDUCE));
   }
 }
 
