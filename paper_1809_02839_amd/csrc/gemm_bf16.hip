@@ -377,10 +377,13 @@ __device__ __forceinline__ void epilogue4(const EpiDev& e, long idx, int col, fl
   }
 }
 
-// epilogue4 with the bf16 bias, residual and mask already loaded (bb, rb, mk:
-// four bf16 each; read only where the epilogue has that operand).
-__device__ __forceinline__ void epilogue4_pre(const EpiDev& e, long idx, int col, float4 a, uint2 bb, uint2 rb,
-                                              uint2 mk) {
+// The epilogue values of four consecutive columns with the bf16 bias,
+// residual and mask already loaded (bb, rb, mk: four bf16 each; read only
+// where the epilogue has that operand): stores the float32 output if there
+// is one and returns the four bf16 results (zero where the mask is not
+// positive).
+__device__ __forceinline__ uint2 epilogue4_values(const EpiDev& e, long idx, int col, float4 a, uint2 bb, uint2 rb,
+                                                  uint2 mk) {
   float v[4] = {a.x * e.alpha, a.y * e.alpha, a.z * e.alpha, a.w * e.alpha};
   auto unpack = [](uint2 u, float (&f)[4]) {
     f[0] = bf16_to_f32(static_cast<bf16_t>(u.x & 0xffff));
@@ -418,18 +421,23 @@ __device__ __forceinline__ void epilogue4_pre(const EpiDev& e, long idx, int col
     }
     *o = make_float4(v[0], v[1], v[2], v[3]);
   }
-  if (e.out_bf16) {
-    uint32_t h[4];
+  uint32_t h[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) h[q] = f32_to_bf16(v[q]);
-    if (e.mask) {
-      unpack(mk, t);
+  for (int q = 0; q < 4; ++q) h[q] = f32_to_bf16(v[q]);
+  if (e.mask) {
+    unpack(mk, t);
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (!(t[q] > 0.0f)) h[q] = 0;
-    }
-    *reinterpret_cast<uint2*>(e.out_bf16 + idx) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    for (int q = 0; q < 4; ++q)
+      if (!(t[q] > 0.0f)) h[q] = 0;
   }
+  return make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+}
+
+// epilogue4 with the bf16 operands already loaded (see epilogue4_values).
+__device__ __forceinline__ void epilogue4_pre(const EpiDev& e, long idx, int col, float4 a, uint2 bb, uint2 rb,
+                                              uint2 mk) {
+  const uint2 h = epilogue4_values(e, idx, col, a, bb, rb, mk);
+  if (e.out_bf16) *reinterpret_cast<uint2*>(e.out_bf16 + idx) = h;
 }
 
 // Stores a block's 128 x 128 accumulator tile: float32 partials of its K
@@ -667,9 +675,33 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
   if constexpr (KSL == 1) {
     if (args.splits == 1 && args.vec8) {
       // float32 tile [128][BNT] in LDS (row pitch BNT + 4 floats), then each
-      // thread takes 8 consecutive columns of a row: every load and store of
-      // the epilogue covers whole row segments
+      // thread takes 8 consecutive columns of NP rows: every load and store
+      // of the epilogue covers whole row segments. All of a thread's operand
+      // loads are issued before the tile is staged and before its first
+      // store: loads and stores share one counter of outstanding memory
+      // operations, so a load issued after a store would wait for the store
+      // to complete and every row would cost a memory round trip.
       constexpr int EP = BNT + 4;
+      constexpr int TPR = BNT / 8;          // threads per row
+      constexpr int RPP = NT / TPR;         // rows per pass
+      constexpr int NP = 128 / RPP;         // rows per thread
+      const int ecl = (tid % TPR) * 8, erl = tid / TPR;
+      const int ecol = col0 + ecl;
+      const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
+      const EpiDev& e = args.e;
+      const bool colok = ecol < args.N;
+      uint4 ebb = make_uint4(0, 0, 0, 0), erb[NP], emk[NP];
+      if (colok && !e.bias && e.bias_bf16) ebb = *reinterpret_cast<const uint4*>(e.bias_bf16 + ecol);
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        const int row = row0 + erl + p * RPP;
+        const long idx = coff + static_cast<long>(row) * e.ldc + ecol;
+        erb[p] = emk[p] = make_uint4(0, 0, 0, 0);
+        if (colok && row < args.M) {
+          if (e.res_bf16) erb[p] = *reinterpret_cast<const uint4*>(e.res_bf16 + idx);
+          if (e.mask) emk[p] = *reinterpret_cast<const uint4*>(e.mask + idx);
+        }
+      }
       float* tile = reinterpret_cast<float*>(&lds[0][0][0]);
       static_assert(sizeof(lds) >= 128 * (BNT + 4) * sizeof(float), "the float32 tile fits the operand buffers");
       __syncthreads();
@@ -685,25 +717,18 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
                 make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
           }
       __syncthreads();
-      constexpr int TPR = BNT / 8;          // threads per row
-      constexpr int RPP = NT / TPR;         // rows per pass
-      const int cl = (tid % TPR) * 8, rl = tid / TPR;
-      const int col = col0 + cl;
-      const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
-      const EpiDev& e = args.e;
-#pragma unroll 4
-      for (int rr = rl; rr < 128; rr += RPP) {
-        const int row = row0 + rr;
-        if (row >= args.M || col >= args.N) continue;
-        const long idx = coff + static_cast<long>(row) * e.ldc + col;
-        uint4 rb = make_uint4(0, 0, 0, 0), mk = make_uint4(0, 0, 0, 0), bb = make_uint4(0, 0, 0, 0);
-        if (e.res_bf16) rb = *reinterpret_cast<const uint4*>(e.res_bf16 + idx);
-        if (e.mask) mk = *reinterpret_cast<const uint4*>(e.mask + idx);
-        if (!e.bias && e.bias_bf16) bb = *reinterpret_cast<const uint4*>(e.bias_bf16 + col);
-        const float4 a0 = *reinterpret_cast<const float4*>(tile + rr * EP + cl);
-        const float4 a1 = *reinterpret_cast<const float4*>(tile + rr * EP + cl + 4);
-        epilogue4_pre(e, idx, col, a0, make_uint2(bb.x, bb.y), make_uint2(rb.x, rb.y), make_uint2(mk.x, mk.y));
-        epilogue4_pre(e, idx + 4, col + 4, a1, make_uint2(bb.z, bb.w), make_uint2(rb.z, rb.w), make_uint2(mk.z, mk.w));
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        const int rr = erl + p * RPP, row = row0 + rr;
+        if (row >= args.M || !colok) continue;
+        const long idx = coff + static_cast<long>(row) * e.ldc + ecol;
+        const float4 a0 = *reinterpret_cast<const float4*>(tile + rr * EP + ecl);
+        const float4 a1 = *reinterpret_cast<const float4*>(tile + rr * EP + ecl + 4);
+        const uint2 h0 = epilogue4_values(e, idx, ecol, a0, make_uint2(ebb.x, ebb.y), make_uint2(erb[p].x, erb[p].y),
+                                          make_uint2(emk[p].x, emk[p].y));
+        const uint2 h1 = epilogue4_values(e, idx + 4, ecol + 4, a1, make_uint2(ebb.z, ebb.w),
+                                          make_uint2(erb[p].z, erb[p].w), make_uint2(emk[p].z, emk[p].w));
+        if (e.out_bf16) *reinterpret_cast<uint4*>(e.out_bf16 + idx) = make_uint4(h0.x, h0.y, h1.x, h1.y);
       }
       return;
     }
