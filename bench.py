@@ -109,7 +109,7 @@ def log(*a):
 class StageLoop:
     """Steady-state driver of one stage through the C ABI with a device ring of inputs."""
 
-    def __init__(self, spec, torch, native, stream, ring=8):
+    def __init__(self, spec, torch, native, stream, ring=8, concurrent=True):
         import numpy as np
         import synth
         self.torch, self.spec, self.stream = torch, spec, stream
@@ -119,6 +119,13 @@ class StageLoop:
         k, N = spec.stage_index, spec.num_stages
         self.sf, self.sb = native.policy_versions(spec.policy, k, N)
         self.depth = N - k
+        # Each step is a forward, a backward and the update (the stage's
+        # one-forward-one-backward order). With two or more mini-batches in
+        # flight the forward of mini-batch m + depth - 1 and the backward of
+        # m, which read weights of the same version, go through the combined
+        # call that runs them concurrently; at the last stage (depth 1) the
+        # forward is the one its backward needs, so the calls stay separate.
+        self.concurrent = concurrent and self.depth >= 2
         self.ring = ring
         with torch.cuda.stream(stream):
             self.st.predict(self.sf, 0)
@@ -140,7 +147,7 @@ class StageLoop:
                 self.y = [torch.empty(spec.output_shape(), device=dev, dtype=dt) for _ in range(self.depth + 1)]
             self.dx = torch.empty(spec.input_shape(), device=dev, dtype=dt)
         self.next_b = 0
-        for m in range(self.depth):
+        for m in range(self.depth - 1 if self.concurrent else self.depth):
             self._forward(m)
         stream.synchronize()
         _ = np
@@ -162,11 +169,21 @@ class StageLoop:
     def steps(self, n, before_update=None):
         for _ in range(n):
             m = self.next_b
-            self.st.backward(m, None if self.dy is None else self.dy[m % self.ring], self.dx)
+            dy = None if self.dy is None else self.dy[m % self.ring]
+            if self.concurrent:
+                f = m + self.depth - 1
+                r = f % self.ring
+                if self.spec.head == "ce":
+                    self.st.forward_backward(f, self.x[r], None, m, dy, self.dx, labels=self.lab[r], loss=self.loss[r])
+                else:
+                    self.st.forward_backward(f, self.x[r], self.y[f % (self.depth + 1)], m, dy, self.dx)
+            else:
+                self.st.backward(m, dy, self.dx)
             if before_update is not None:
                 before_update()
             self.st.update(self.sf, self.sb)
-            self._forward(m + self.depth)
+            if not self.concurrent:
+                self._forward(m + self.depth)
             self.next_b += 1
 
 
@@ -385,6 +402,10 @@ def main():
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="steps of a second per-launch pass in which a 1 GiB read evicts the caches (MALL "
                          "included) before every update, for the update's cold-cache bandwidth (0: skip)")
+    ap.add_argument("--serial", action="store_true",
+                    help="issue each step's forward and backward as separate calls (by default a single stage "
+                         "with two or more mini-batches in flight runs them concurrently through "
+                         "spectrain_stage_forward_backward)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (a known-size reference "
                          "dispatch for scaling hardware byte counters)")
@@ -414,7 +435,8 @@ def main():
         log(f"[bench] calibration kernel (neg): {n * 4} bytes read, {n * 4} bytes written")
         del src, dst
     stream = torch.cuda.Stream()
-    loop = PipeLoop(specs, torch, native, stream) if pipeline else StageLoop(spec, torch, native, stream)
+    loop = (PipeLoop(specs, torch, native, stream) if pipeline
+            else StageLoop(spec, torch, native, stream, concurrent=not args.serial))
 
     loop.steps(args.warmup)
     torch.cuda.synchronize()
@@ -556,6 +578,7 @@ def main():
         "dtype": spec.dtype,
         "data": "synthetic",
         "hip_graph": bool(args.graph),
+        "concurrent_forward_backward": bool(getattr(loop, "concurrent", False)),
         "config": {"workload": f"{args.workload}: {DESCRIPTIONS[args.workload]}", "policy": args.policy,
                    "batch": spec.batch,
                    "stage_index": None if pipeline else spec.stage_index, "num_stages": spec.num_stages,

@@ -128,7 +128,11 @@ int32_t spectrain_version_difference(int32_t k, int32_t N, int32_t is_forward);
  * stage's device work runs on it. v starts at 0, so both predicted slots start
  * equal to W0 (Eq. 4 with v = 0). Device dims that the kernels need to be
  * multiples of 8 (bf16 channel/feature counts) are checked here (EINVAL).
- * Synchronises the stream before returning. */
+ * Every device buffer the stage uses is allocated here: the arenas, the
+ * stash ring, the workspace and a second workspace copy (for the forward of
+ * spectrain_stage_forward_backward), and two streams of the stage's own
+ * (default priority: weight gradients, and that forward). Synchronises the
+ * stream before returning. */
 int spectrain_stage_create(const spectrain_stage_desc* desc, const float* W0_host, size_t n_params,
                            void* hip_stream, spectrain_stage_t* out);
 
@@ -181,6 +185,28 @@ int spectrain_stage_backward(spectrain_stage_t st, int64_t mb_id, const void* dy
  * overlap on one GPU, on different streams, race. */
 #define SPECTRAIN_NOALLOC_SCRATCH_BYTES (128u << 20)
 int spectrain_stage_backward_noalloc(spectrain_stage_t st, int64_t mb_id, const void* dy_dev, void* dx_dev);
+
+/* The forward of mb_fwd followed by the backward of mb_bwd, with the effect
+ * of spectrain_stage_forward then spectrain_stage_backward (same arguments,
+ * state rules and results, bitwise), the two passes running concurrently on
+ * the GPU. In the one-forward-one-backward order of Section 3.1 a stage's
+ * forward is followed by a backward with no update between them, so both
+ * passes read weights of the same version (slot 0 and slot 1 as refreshed by
+ * the last update, or the mini-batch's weight stash) and neither writes what
+ * the other reads. The forward runs on a stream of the stage's own (default
+ * priority) against a second copy of the stage's workspace, both made by
+ * spectrain_stage_create, so the call allocates nothing and can be captured
+ * in a HIP graph; the backward runs as spectrain_stage_backward does, and
+ * work enqueued later on the stage's stream waits for both.
+ * ESTATE, with nothing enqueued, when mb_fwd == mb_bwd, mb_fwd is in flight,
+ * no stash slot is free (always so at the last stage, k = N - 1, whose
+ * forward is the one its backward needs), mb_bwd is not in flight or a
+ * gradient still waits for its update; EINVAL for a NULL x_dev, for a NULL
+ * y_dev or dy_dev without a CE head, or a CE head without labels_dev and
+ * loss_dev. */
+int spectrain_stage_forward_backward(spectrain_stage_t st, int64_t mb_fwd, const void* x_dev, void* y_dev,
+                                     const int32_t* labels_dev, float* loss_dev, int64_t mb_bwd, const void* dy_dev,
+                                     void* dx_dev);
 
 /* One fused pass over the arenas: Eq. 1, W <- W - eta v, then Eq. 4 for both
  * slots (slot 0 with s_next_fwd, slot 1 with s_next_bwd; a negative s leaves

@@ -92,6 +92,14 @@ int spectrain_stage_backward_noalloc(spectrain_stage_t st, int64_t mb_id, const 
   return guarded(st, [&](spx::Stage& x) { x.backward_noalloc(mb_id, dy_dev, dx_dev); });
 }
 
+int spectrain_stage_forward_backward(spectrain_stage_t st, int64_t mb_fwd, const void* x_dev, void* y_dev,
+                                     const int32_t* labels_dev, float* loss_dev, int64_t mb_bwd, const void* dy_dev,
+                                     void* dx_dev) {
+  return guarded(st, [&](spx::Stage& x) {
+    x.forward_backward(mb_fwd, x_dev, y_dev, labels_dev, loss_dev, mb_bwd, dy_dev, dx_dev);
+  });
+}
+
 int spectrain_stage_update(spectrain_stage_t st, int32_t s_next_fwd, int32_t s_next_bwd) {
   return guarded(st, [&](spx::Stage& x) { x.update(s_next_fwd, s_next_bwd); });
 }

@@ -441,6 +441,9 @@ void Stage::plan_buffers() {
   stash_bytes_ = st;
   for (size_t b : st) stash_off_.push_back(probe.add(std::max<size_t>(b, 1)));
   for (size_t b : ws) ws_off_.push_back(ws_block_.add(std::max<size_t>(b, 1)));
+  // a second copy for a forward that runs beside a backward (the combined
+  // call), allocated here so that the call itself allocates nothing
+  for (size_t b : ws) ws_block_f_.add(std::max<size_t>(b, 1));
   const int nslots = d_.num_stages - d_.stage_index;
   slots_.resize(nslots);
   slot_blocks_.resize(nslots);
@@ -449,6 +452,7 @@ void Stage::plan_buffers() {
     slot_blocks_[i].allocate();
   }
   ws_block_.allocate();
+  ws_block_f_.allocate();
 }
 
 // ---------------------------------------------------------------- create ----
@@ -533,6 +537,9 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
   hip_check(hipEventCreateWithFlags(&join_ev_, hipEventDisableTiming), "hipEventCreate");
   side_ev_.resize(32, nullptr);
   for (hipEvent_t& e : side_ev_) hip_check(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreate");
+  hip_check(hipStreamCreateWithFlags(&s3_, hipStreamNonBlocking), "hipStreamCreate");
+  hip_check(hipEventCreateWithFlags(&ffork_ev_, hipEventDisableTiming), "hipEventCreate");
+  hip_check(hipEventCreateWithFlags(&fjoin_ev_, hipEventDisableTiming), "hipEventCreate");
   // arenas: W, v, g (float32), two predicted slots (operand dtype), all padded
   size_t oW = arena_.add(n_arena_ * 4), ov = arena_.add(n_arena_ * 4), og = arena_.add(n_arena_ * 4);
   size_t of = arena_.add(n_arena_ * esz_), ob = arena_.add(n_arena_ * esz_);
@@ -564,12 +571,16 @@ Stage::Stage(const spectrain_stage_desc& d, const float* W0, size_t n_params, hi
 Stage::~Stage() {
   (void)hipStreamSynchronize(s_);
   if (s2_) (void)hipStreamSynchronize(s2_);
+  if (s3_) (void)hipStreamSynchronize(s3_);
   for (hipEvent_t e : prof_pool_) (void)hipEventDestroy(e);
   if (fork_ev_) (void)hipEventDestroy(fork_ev_);
   if (join_ev_) (void)hipEventDestroy(join_ev_);
   for (hipEvent_t e : side_ev_)
     if (e) (void)hipEventDestroy(e);
+  if (ffork_ev_) (void)hipEventDestroy(ffork_ev_);
+  if (fjoin_ev_) (void)hipEventDestroy(fjoin_ev_);
   if (s2_) (void)hipStreamDestroy(s2_);
+  if (s3_) (void)hipStreamDestroy(s3_);
 }
 
 void Stage::sync() { hip_check(hipStreamSynchronize(s_), "hipStreamSynchronize"); }
@@ -689,7 +700,7 @@ void Stage::forward(int64_t mb, const void* x, void* y, const int32_t* labels, f
   if (free_slot < 0) throw StageError(SPECTRAIN_ESTATE, "N - k mini-batches already in flight");
   if (d_.weight_policy == SPECTRAIN_POLICY_STASH)
     hip_check(hipMemcpyAsync(wstash_.at<char>(wstash_off_[free_slot]), what_[0], n_arena_ * esz_,
-                             hipMemcpyDeviceToDevice, s_),
+                             hipMemcpyDeviceToDevice, ls_),
               "stash weights");
   switch (d_.kind) {
     case SPECTRAIN_KIND_FC: fwd_fc(free_slot, x, y, labels, loss); break;
@@ -743,6 +754,52 @@ void Stage::backward_noalloc(int64_t mb, const void* dy, void* dx) {
   ext_ws_ = nullptr;
 }
 
+void Stage::forward_backward(int64_t mb_f, const void* x, void* y, const int32_t* labels, float* loss, int64_t mb_b,
+                             const void* dy, void* dx) {
+  // Every precondition of both passes is checked before anything is issued,
+  // so a refused call leaves the stage unchanged.
+  const bool ce = d_.head == SPECTRAIN_HEAD_CE;
+  if (mb_f == mb_b) throw StageError(SPECTRAIN_ESTATE, "the forward and the backward name the same mini-batch");
+  if (!x) fail("x_dev is NULL");
+  if (ce && (!labels || !loss)) fail("a CE head needs labels_dev and loss_dev");
+  if (!ce && !y) fail("y_dev is NULL");
+  if (!ce && !dy) fail("dy_dev is NULL");
+  bool b_in_flight = false, has_free = false;
+  for (const Slot& sl : slots_) {
+    if (sl.used && sl.mb == mb_f) throw StageError(SPECTRAIN_ESTATE, "mini-batch already in flight");
+    if (sl.used && sl.mb == mb_b) b_in_flight = true;
+    if (!sl.used) has_free = true;
+  }
+  if (!b_in_flight) throw StageError(SPECTRAIN_ESTATE, "backward of a mini-batch that is not in flight");
+  if (!has_free) throw StageError(SPECTRAIN_ESTATE, "N - k mini-batches already in flight");
+  if (g_pending_) throw StageError(SPECTRAIN_ESTATE, "the previous gradient has not been applied by an update");
+  // the forward starts after everything issued on the stage stream so far
+  // (the update that refreshed its weights)
+  hip_check(hipEventRecord(ffork_ev_, s_), "hipEventRecord");
+  hip_check(hipStreamWaitEvent(s3_, ffork_ev_, 0), "hipStreamWaitEvent");
+  ls_ = s3_;
+  wsb_ = &ws_block_f_;
+  try {
+    forward(mb_f, x, y, labels, loss);
+  } catch (...) {
+    ls_ = s_;
+    wsb_ = &ws_block_;
+    hip_check(hipEventRecord(fjoin_ev_, s3_), "hipEventRecord");
+    hip_check(hipStreamWaitEvent(s_, fjoin_ev_, 0), "hipStreamWaitEvent");
+    throw;
+  }
+  ls_ = s_;
+  wsb_ = &ws_block_;
+  hip_check(hipEventRecord(fjoin_ev_, s3_), "hipEventRecord");
+  try {
+    backward(mb_b, dy, dx);
+  } catch (...) {
+    hip_check(hipStreamWaitEvent(s_, fjoin_ev_, 0), "hipStreamWaitEvent");
+    throw;
+  }
+  hip_check(hipStreamWaitEvent(s_, fjoin_ev_, 0), "hipStreamWaitEvent");
+}
+
 // ==================================================================== FC ====
 // y_l = relu(a_l W_l^T + b_l); the last layer of a CE stage produces logits.
 void Stage::fwd_fc(int slot, const void* x, void* y, const int32_t* labels, float* loss) {
@@ -770,7 +827,7 @@ void Stage::fwd_fc(int slot, const void* x, void* y, const int32_t* labels, floa
   }
   if (ce)
     LAUNCH("softmax_ce", 0, ce_bytes(B, d_.dims[1]),
-           softmax_ce(ws<float>(0), labels, B, d_.dims[1], stash<void>(slot, L - 1), dt_, loss, ws<float>(3), s_));
+           softmax_ce(ws<float>(0), labels, B, d_.dims[1], stash<void>(slot, L - 1), dt_, loss, ws<float>(3), ls_));
 }
 
 void Stage::bwd_fc(int slot, const void* dy, void* dx) {
@@ -838,13 +895,13 @@ void Stage::pool_head_fwd(int slot, const void* yl, int HW, int C, int t, int id
   const int B = d_.batch, V = d_.dims[4];
   bf16_t* pooled = stash<bf16_t>(slot, id_pool);
   LAUNCH("avgpool", 0, 2.0 * B * C * (HW + 1),
-         avgpool_fwd(static_cast<const bf16_t*>(yl), B, HW, C, pooled, s_));
+         avgpool_fwd(static_cast<const bf16_t*>(yl), B, HW, C, pooled, ls_));
   GemmDesc g = gd(B, V, C, opK(pooled, C), opK(wf(t), C), V);
   g.epi.bias_bf16 = static_cast<const bf16_t*>(wf(t + 1));
   g.epi.out_f32 = ws<float>(wsl);
   gemm(g);
   LAUNCH("softmax_ce", 0, ce_bytes(B, V), softmax_ce(ws<float>(wsl), labels, B, V, stash<void>(slot, id_dl), 1, loss,
-                                        ws<float>(wsl + 1), s_));
+                                        ws<float>(wsl + 1), ls_));
 }
 
 void Stage::pool_head_bwd(int slot, const void* yl, int HW, int C, int t, int id_pool, int id_dl, int wsl, void* dz) {
@@ -1033,7 +1090,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     gemm(g);
     if (attention_fused_supported(S, dh, d)) {
       LAUNCH("attention", 4.0 * B * Hh * S * S * dh, 2.0 * T * 4 * d + 8.0 * B * Hh * S,
-             attention_fwd(qkv, B, Hh, d, scale, P, ctx, s_));
+             attention_fwd(qkv, B, Hh, d, scale, P, ctx, ls_));
     } else {
     // scores[b, h] = Q K^T * scale
     Operand qa = opK(qkv, 3 * d), kb = opK(qkv + d, 3 * d);
@@ -1047,7 +1104,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     sc.epi.alpha = scale;
     sc.epi.out_f32 = ws<float>(0);
     gemm(sc);
-    LAUNCH("softmax", 0, 10.0 * B * Hh * S * S, softmax_rows(ws<float>(0), B * Hh * S, S, P, Pb, s_));
+    LAUNCH("softmax", 0, 10.0 * B * Hh * S * S, softmax_rows(ws<float>(0), B * Hh * S, S, P, Pb, ls_));
     // ctx[b, :, h] = P V
     Operand pa = opK(Pb, S), vb = opR(qkv + 2 * d, 3 * d);
     pa.bs1 = static_cast<long>(Hh) * S * S;
@@ -1068,7 +1125,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     go.epi.out_bf16 = r1;
     gemm(go);
     LAUNCH("layernorm", 0, ln_bytes(T, d), layernorm_fwd(r1, static_cast<const bf16_t*>(wf(p + 4)), static_cast<const bf16_t*>(wf(p + 5)), T, d,
-                            LN_EPS, h, stash<float>(slot, q + 5), stash<float>(slot, q + 6), s_));
+                            LN_EPS, h, stash<float>(slot, q + 5), stash<float>(slot, q + 6), ls_));
     GemmDesc g1 = gd(T, F, d, opK(h, d), opK(wf(p + 6), d), F);
     g1.epi.bias_bf16 = static_cast<const bf16_t*>(wf(p + 7));
     g1.epi.relu = 1;
@@ -1081,7 +1138,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     gemm(g2);
     LAUNCH("layernorm", 0, ln_bytes(T, d), layernorm_fwd(r2, static_cast<const bf16_t*>(wf(p + 10)), static_cast<const bf16_t*>(wf(p + 11)), T, d,
                             LN_EPS, static_cast<bf16_t*>(out), stash<float>(slot, q + 10), stash<float>(slot, q + 11),
-                            s_));
+                            ls_));
     a = out;
   }
   if (ce) {   // logits of every token (float32), mean token cross-entropy, dlogits (bf16) for the backward
@@ -1091,7 +1148,7 @@ void Stage::fwd_tfm(int slot, const void* x, void* y, const int32_t* labels, flo
     gv.epi.out_f32 = ws<float>(10);
     gemm(gv);
     LAUNCH("softmax_ce", 0, ce_bytes(T, V), softmax_ce(ws<float>(10), labels, T, V, stash<void>(slot, 13 * L), 1, loss,
-                                          ws<float>(11), s_));
+                                          ws<float>(11), ls_));
   }
 }
 
@@ -1301,7 +1358,7 @@ void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, fl
       const long o = static_cast<long>(t) * B;
       LAUNCH("lstm_step", t > 0 ? 8.0 * B * H * H : 0.0, (t > 0 ? 8.0 * H * H : 0.0) + 34.0 * B * H,
              lstm_step_fwd(zx + o * 4 * H, t > 0 ? hs + (o - B) * H : nullptr, static_cast<const bf16_t*>(wf(p + 1)),
-                           t > 0 ? c + (o - B) * H : nullptr, B, H, gates + o * 4 * H, c + o * H, hs + o * H, s_));
+                           t > 0 ? c + (o - B) * H : nullptr, B, H, gates + o * 4 * H, c + o * H, hs + o * H, ls_));
     }
     for (int t = 0; t < T && !fused; ++t) {
       float* zt = zx + static_cast<long>(t) * B * 4 * H;
@@ -1313,9 +1370,9 @@ void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, fl
       }
       LAUNCH("lstm_cell", 0, 0, lstm_cell_fwd(zt, t > 0 ? c + static_cast<long>(t - 1) * B * H : nullptr, B, H,
                               gates + static_cast<long>(t) * B * 4 * H, c + static_cast<long>(t) * B * H,
-                              hs + static_cast<long>(t) * B * H, s_));
+                              hs + static_cast<long>(t) * B * H, ls_));
     }
-    LAUNCH("residual", 0, 6.0 * TB * H, add_bf16(static_cast<const bf16_t*>(u), hs, static_cast<bf16_t*>(out), TB * H, s_));
+    LAUNCH("residual", 0, 6.0 * TB * H, add_bf16(static_cast<const bf16_t*>(u), hs, static_cast<bf16_t*>(out), TB * H, ls_));
     u = out;
   }
   if (ce) {
@@ -1324,7 +1381,7 @@ void Stage::fwd_lstm(int slot, const void* x, void* y, const int32_t* labels, fl
     gv.epi.out_f32 = ws<float>(1);
     gemm(gv);
     LAUNCH("softmax_ce", 0, ce_bytes(TB, V), softmax_ce(ws<float>(1), labels, static_cast<int>(TB), V, stash<void>(slot, 4 * L), 1, loss, ws<float>(7),
-                         s_));
+                         ls_));
   }
 }
 

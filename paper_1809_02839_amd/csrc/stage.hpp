@@ -88,6 +88,14 @@ class Stage {
   // The same backward with every split-K partial plane in the device's
   // scratch array instead of the stage's workspace; allocates nothing.
   void backward_noalloc(int64_t mb, const void* dy, void* dx);
+  // The forward of mb_f and the backward of mb_b with the effect of forward()
+  // then backward(): no update lies between the two in the stage's order, so
+  // both read the weights of the same version, and they share no buffer. The
+  // forward runs on a stream of its own with its own workspace copy, beside
+  // the backward; the stage stream waits for both before the call's later
+  // work.
+  void forward_backward(int64_t mb_f, const void* x, void* y, const int32_t* labels, float* loss, int64_t mb_b,
+                        const void* dy, void* dx);
   void update(int s_f, int s_b);
   void get_state(float* W, float* v);
   void set_state(const float* W, const float* v);
@@ -116,7 +124,7 @@ class Stage {
   template <typename T>
   T* stash(int slot, int buf) const { return slot_blocks_[slot].at<T>(stash_off_[buf]); }
   template <typename T>
-  T* ws(int buf) const { return ws_block_.at<T>(ws_off_[buf]); }
+  T* ws(int buf) const { return wsb_->at<T>(ws_off_[buf]); }
   // defer: the GEMM is the only writer of a gradient tensor (plain float32
   // store into g); when it splits K, its partials stay in the deferred buffer
   // and the update sums them instead of a separate reduction pass.
@@ -221,13 +229,17 @@ class Stage {
   std::vector<size_t> stash_bytes_;      // size of each stash buffer (0: unused for this stage)
   DeviceBlock ws_block_;
   std::vector<size_t> ws_off_;
+  DeviceBlock ws_block_f_;               // workspace copy of a forward that runs beside a backward
+  const DeviceBlock* wsb_ = &ws_block_;  // workspace of the pass being issued
   // workspace ids after the kind's own buffers: column-sum partials of the
   // stage stream and of the side stream, split-K partials of each stream
   int ws_colsum_ = -1, ws_colsum2_ = -1, ws_split_ = -1, ws_split2_ = -1;
   size_t gemm_ws_bytes_ = 0;
   float* ext_ws_ = nullptr;              // split-K partials of the current call, when not the workspace
   hipStream_t s2_ = nullptr;             // side stream (weight gradients), default priority
-  hipStream_t ls_ = nullptr;             // stream of the launch being issued: s_ or s2_
+  hipStream_t ls_ = nullptr;             // stream of the launch being issued: s_, s2_ or s3_
+  hipStream_t s3_ = nullptr;             // forward beside a backward, default priority
+  hipEvent_t ffork_ev_ = nullptr, fjoin_ev_ = nullptr;
   hipEvent_t fork_ev_ = nullptr, join_ev_ = nullptr;
   bool side_pending_ = false;
   std::vector<hipEvent_t> side_ev_;      // completion events of side GEMMs (a ring)

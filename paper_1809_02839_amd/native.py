@@ -25,7 +25,7 @@ KIND_BY_NAME = {"fc": KIND_FC, "conv3x3": KIND_CONV3X3, "bottleneck": KIND_BOTTL
 
 EXPORTED = ("spectrain_version_difference", "spectrain_stage_create", "spectrain_stage_num_params",
             "spectrain_stage_predict", "spectrain_stage_forward", "spectrain_stage_backward",
-            "spectrain_stage_backward_noalloc",
+            "spectrain_stage_backward_noalloc", "spectrain_stage_forward_backward",
             "spectrain_stage_update", "spectrain_stage_get_state", "spectrain_stage_set_state",
             "spectrain_stage_get_predicted", "spectrain_stage_profile", "spectrain_stage_profile_read",
             "spectrain_stage_read_stash", "spectrain_stage_destroy", "spectrain_last_error")
@@ -70,6 +70,7 @@ def lib():
             "spectrain_stage_forward": (ctypes.c_int, [vp, i64, vp, vp, vp, vp]),
             "spectrain_stage_backward": (ctypes.c_int, [vp, i64, vp, vp]),
             "spectrain_stage_backward_noalloc": (ctypes.c_int, [vp, i64, vp, vp]),
+            "spectrain_stage_forward_backward": (ctypes.c_int, [vp, i64, vp, vp, vp, vp, i64, vp, vp]),
             "spectrain_stage_update": (ctypes.c_int, [vp, i32, i32]),
             "spectrain_stage_get_state": (ctypes.c_int, [vp, fp, fp]),
             "spectrain_stage_set_state": (ctypes.c_int, [vp, fp, fp]),
@@ -187,6 +188,14 @@ class Stage:
     def backward_noalloc(self, mb: int, dy=None, dx=None):
         a = self._act
         _check(lib().spectrain_stage_backward_noalloc(self.h, mb, _dptr(dy, a, "dy"), _dptr(dx, a, "dx")))
+
+    def forward_backward(self, mb_fwd: int, x, y, mb_bwd: int, dy=None, dx=None, labels=None, loss=None):
+        """forward(mb_fwd) then backward(mb_bwd), the two passes running concurrently."""
+        a = self._act
+        _check(lib().spectrain_stage_forward_backward(self.h, mb_fwd, _dptr(x, a, "x"), _dptr(y, a, "y"),
+                                                      _dptr(labels, "torch.int32", "labels"),
+                                                      _dptr(loss, "torch.float32", "loss"), mb_bwd,
+                                                      _dptr(dy, a, "dy"), _dptr(dx, a, "dx")))
 
     def update(self, s_next_fwd: int, s_next_bwd: int):
         _check(lib().spectrain_stage_update(self.h, s_next_fwd, s_next_bwd))
