@@ -56,6 +56,7 @@ struct GemmDesc {
   int batch = 1, zdiv = 1;
   float* workspace = nullptr;      // split-K partials (bf16 GEMM); NULL disables splitting
   size_t workspace_bytes = 0;
+  bool concurrent = false;         // launched beside another pass's launches (selects the tile rule)
   Operand A, B;
   Epilogue epi;
 };
@@ -67,7 +68,7 @@ enum { GEMM_MAIN = 1, GEMM_REDUCE = 2, GEMM_ALL = 3 };
 hipError_t gemm_bf16(const GemmDesc& d, hipStream_t s, int phases = GEMM_ALL);
 int gemm_bf16_splits(const GemmDesc& d);   // K splits the launch will use (1 = none)
 // The same count from the shape alone, for a workspace of workspace_bytes.
-int gemm_bf16_split_rule(int M, int N, int K, int batch, size_t workspace_bytes);
+int gemm_bf16_split_rule(int M, int N, int K, int batch, size_t workspace_bytes, bool concurrent);
 hipError_t gemm_f32(const GemmDesc& d, hipStream_t s);
 // Names of the kernels a launch runs, as a profiler lists the instantiations
 // (e.g. "gemm_bf16_kernel<0, 3, false, 128, 1>"); the returned buffer is

@@ -215,6 +215,7 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
   const bool side = ls_ == s2_;   // each stream has its own split-K partials
   dd.workspace = ext_ws_ ? ext_ws_ + (side ? gemm_ws_bytes_ / 4 : 0) : ws<float>(side ? ws_split2_ : ws_split_);
   dd.workspace_bytes = gemm_ws_bytes_;
+  dd.concurrent = concurrent_;
   if (!dt_) {
     LAUNCH(prof_on_ ? gemm_f32_kernel_name(dd) : "gemm_f32", flops, bytes, gemm_f32(dd, ls_));
     return;
@@ -225,7 +226,7 @@ void Stage::gemm(const GemmDesc& d, bool defer) {
     const long off = e.out_f32 ? static_cast<long>(e.out_f32 - g_) : -1;
     const bool plain = d.batch == 1 && e.out_f32 && !e.out_bf16 && !e.bias && !e.bias_bf16 && !e.res_f32 &&
                        !e.res_bf16 && !e.mask && e.alpha == 1.0f && !e.relu && !e.accumulate && e.ldc == d.N;
-    const int splits = gemm_bf16_split_rule(d.M, d.N, d.K, d.batch, gemm_ws_bytes_);
+    const int splits = gemm_bf16_split_rule(d.M, d.N, d.K, d.batch, gemm_ws_bytes_, concurrent_);
     if (plain && splits > 1 && off >= 0 && off + mn <= n_arena_ && off % 8 == 0 && mn % 8 == 0 &&
         defer_used_ + splits * mn <= defer_cap_ && defer_segs_.size() < static_cast<size_t>(UPDATE_MAX_SEGMENTS)) {
       dd.workspace = defer_ + defer_used_;
@@ -355,8 +356,9 @@ void Stage::plan_buffers() {
       partial = partial_floats(B, V);
       for (int l = 0; l < L && dt_; ++l) {   // filter-gradient partials, reduced by the update
         const int C = l == 0 ? dm[0] : dm[1];
-        defer_cap_ += static_cast<long>(gemm_bf16_split_rule(dm[1], 9 * C, static_cast<int>(P), 1, gemm_ws_bytes_)) *
-                      dm[1] * 9 * C;
+        const int sp = std::max(gemm_bf16_split_rule(dm[1], 9 * C, static_cast<int>(P), 1, gemm_ws_bytes_, false),
+                                 gemm_bf16_split_rule(dm[1], 9 * C, static_cast<int>(P), 1, gemm_ws_bytes_, true));
+        defer_cap_ += static_cast<long>(sp) * dm[1] * 9 * C;
       }
       break;
     }
@@ -779,11 +781,13 @@ void Stage::forward_backward(int64_t mb_f, const void* x, void* y, const int32_t
   hip_check(hipStreamWaitEvent(s3_, ffork_ev_, 0), "hipStreamWaitEvent");
   ls_ = s3_;
   wsb_ = &ws_block_f_;
+  concurrent_ = true;
   try {
     forward(mb_f, x, y, labels, loss);
   } catch (...) {
     ls_ = s_;
     wsb_ = &ws_block_;
+    concurrent_ = false;
     hip_check(hipEventRecord(fjoin_ev_, s3_), "hipEventRecord");
     hip_check(hipStreamWaitEvent(s_, fjoin_ev_, 0), "hipStreamWaitEvent");
     throw;
@@ -794,9 +798,11 @@ void Stage::forward_backward(int64_t mb_f, const void* x, void* y, const int32_t
   try {
     backward(mb_b, dy, dx);
   } catch (...) {
+    concurrent_ = false;
     hip_check(hipStreamWaitEvent(s_, fjoin_ev_, 0), "hipStreamWaitEvent");
     throw;
   }
+  concurrent_ = false;
   hip_check(hipStreamWaitEvent(s_, fjoin_ev_, 0), "hipStreamWaitEvent");
 }
 

@@ -231,6 +231,7 @@ class Stage {
   std::vector<size_t> ws_off_;
   DeviceBlock ws_block_f_;               // workspace copy of a forward that runs beside a backward
   const DeviceBlock* wsb_ = &ws_block_;  // workspace of the pass being issued
+  bool concurrent_ = false;              // issuing the passes of forward_backward (GEMM tile rule)
   // workspace ids after the kind's own buffers: column-sum partials of the
   // stage stream and of the side stream, split-K partials of each stream
   int ws_colsum_ = -1, ws_colsum2_ = -1, ws_split_ = -1, ws_split2_ = -1;
