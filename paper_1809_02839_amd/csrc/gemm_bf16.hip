@@ -17,6 +17,15 @@
 // buffer loads whose resource spans exactly the operand tensor: an offset
 // outside it (zero padding of convolutions, ragged tile edges) reads zero.
 //
+// Direct loads (128-wide 4-wave blocks): the buffer loads carry the LDS
+// flag, so each lane's 16 bytes go straight into a two-stage LDS ring at the
+// position fixed by its lane number, with no register stage and no LDS store
+// instruction (LDS stores contend with the MFMA operand reads; direct loads
+// measured beside LDS reads do not). The lanes' source addresses are
+// permuted instead of the destinations: K-mode tiles become rows of 64 k
+// without padding whose 16-byte chunks are XOR-swizzled by row pairs, R-mode
+// tiles keep the layout above.
+//
 // Epilogue: an unsplit 4-wave launch whose output rows allow 16-byte
 // accesses stages its float32 tile in LDS and then gives each thread eight
 // consecutive columns of a row, so the residual and mask loads and the output
@@ -60,6 +69,16 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 // MFMA operand (8 consecutive k of one row) from a K-mode tile [row][PITCH].
 __device__ __forceinline__ bf16x8_t frag_k(const bf16_t* s, int row, int k) {
   return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u16x8_t*>(s + row * PITCH + k));
+}
+
+// The same operand from a K-mode tile filled by direct loads: rows of 64 k
+// without padding, the eight 16-byte chunks of row r permuted by an XOR with
+// (r / 2) % 8. Sixteen lanes reading one chunk of sixteen consecutive rows
+// then hit every bank once (rows 2j and 2j + 1 share a slot but lie in
+// different halves of the 64 banks).
+__device__ __forceinline__ bf16x8_t frag_kd(const bf16_t* s, int row, int k) {
+  return __builtin_bit_cast(
+      bf16x8_t, *reinterpret_cast<const u16x8_t*>(s + row * BK + ((((k >> 3) ^ ((row >> 1) & 7))) << 3)));
 }
 
 // The same operand from an R-mode tile [k][RPITCH] with two transposing LDS
@@ -114,6 +133,7 @@ struct KArgs {
   int vec8;              // ... and the eight-column one (N, ldc multiples of 8, 16-byte aligned tensors)
   int bn;                // block tile width in N (host side: selects the kernel)
   int ksl;               // waves per output sub-tile (host side: selects the kernel)
+  int dma;               // operand tiles loaded directly into LDS (host side: selects the kernel)
   EpiDev e;
 };
 
@@ -130,22 +150,40 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, int byte_off) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Direct load into LDS: the 16 bytes of lane l land at LDS byte address
+// lds_base + 16 l (lds_base wave-uniform, passed in M0); an offset outside
+// the resource writes zeros. Issued through inline assembly so that the
+// compiler, which cannot tell the stages of the LDS ring apart, does not wait
+// for every outstanding direct load before each LDS read: the K loop waits
+// for exactly the stage it reads (dma_wait) and then synchronises the block.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t lds_base, int byte_off) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds_base), "v"(byte_off), "s"(r)
+               : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void dma_wait() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // ---- K-mode: 8 consecutive k of one row ----------------------------------
 // Thread t of NTH loads vectors v = t + NTH i (i < 8 ROWS / NTH): tile row
 // v / 8, k chunk t % 8.
 // TAPK (convolutions whose channel count is a multiple of BK): every K step
 // lies inside one filter tap, so the tap and its pixel shift are uniform for
 // the whole block and each vector costs one add and a bounds check.
-template <int MODE, bool TAPK, int ROWS, int NTH>
+template <int MODE, bool TAPK, int ROWS, int NTH, bool DMA = false>
 struct KLoader {
   static constexpr int V = 8 * ROWS / NTH;   // 16-byte vectors per thread
+  static_assert(!DMA || NTH % 128 == 0, "the direct-load chunk permutation assumes 16 | NTH / 8");
   int row_ok[4];
   int base[4];       // byte offset of the row (PLAIN) or of the pixel's channel 0 (CONV)
   int ph[4], pw[4];  // CONV: pixel coordinates
   int kq8;           // this thread's k offset inside a K step
 
   __device__ void init(const OperandDev& o, int row0, int tid, int /*k0*/) {
-    kq8 = (tid & 7) * 8;
+    // DMA: vector t + NTH i lands in LDS slot t % 8 of its row, which holds
+    // k chunk slot ^ ((row / 2) % 8) (see frag_kd); row / 2 % 8 = t / 16 % 8
+    kq8 = DMA ? (((tid & 7) ^ ((tid >> 4) & 7)) * 8) : (tid & 7) * 8;
 #pragma unroll
     for (int i = 0; i < V; ++i) {
       const int r = row0 + ((tid + NTH * i) >> 3);
@@ -164,12 +202,15 @@ struct KLoader {
     }
   }
 
-  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, uint4 (&reg)[4]) {
+  // Byte offset (OOB for zero padding) of each of the thread's V vectors of
+  // the K step starting at k0, handed to f(i, offset).
+  template <class F>
+  __device__ __forceinline__ void visit(const OperandDev& o, int k0, F&& f) {
     const int k = k0 + kq8;
     const bool kok = k < o.K;
     if (MODE == OP_K_PLAIN) {
 #pragma unroll
-      for (int i = 0; i < V; ++i) reg[i] = bload(rs, (row_ok[i] & kok) ? base[i] + k * 2 : OOB);
+      for (int i = 0; i < V; ++i) f(i, (row_ok[i] & kok) ? base[i] + k * 2 : OOB);
     } else if (TAPK) {
       const int tap = static_cast<int>(o.fdC.div(k0));     // uniform
       const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
@@ -181,7 +222,7 @@ struct KLoader {
         const int hh = ph[i] + dh, ww = pw[i] + dw;
         const bool ok = row_ok[i] & (static_cast<unsigned>(hh) < static_cast<unsigned>(o.H)) &
                         (static_cast<unsigned>(ww) < static_cast<unsigned>(o.W));
-        reg[i] = bload(rs, ok ? base[i] + shift : OOB);
+        f(i, ok ? base[i] + shift : OOB);
       }
     } else {
       const uint32_t tap = o.fdC.div(kok ? k : 0);
@@ -196,9 +237,19 @@ struct KLoader {
         const int hh = ph[i] + dh, ww = pw[i] + dw;
         const bool ok = row_ok[i] & kok & (static_cast<unsigned>(hh) < static_cast<unsigned>(o.H)) &
                         (static_cast<unsigned>(ww) < static_cast<unsigned>(o.W));
-        reg[i] = bload(rs, ok ? base[i] + shift : OOB);
+        f(i, ok ? base[i] + shift : OOB);
       }
     }
+  }
+
+  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, uint4 (&reg)[4]) {
+    visit(o, k0, [&](int i, int off) { reg[i] = bload(rs, off); });
+  }
+
+  // DMA: vector i of wave w's lanes lands at tile byte 16 (64 w + NTH i) + 16 lane
+  __device__ __forceinline__ void dma(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, uint32_t tile,
+                                      int wave) {
+    visit(o, k0, [&](int i, int off) { dma16(rs, tile + 16u * (64 * wave + NTH * i), off); });
   }
 
   __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[4], int tid) const {
@@ -217,9 +268,10 @@ struct KLoader {
 // 8 (t % G) .. + 7) at k = k0 + t / G + (NTH / G) i (i < BK G / NTH): G lanes
 // cover one k row of the tile. Loads must be issued for consecutive K steps
 // (the filter-gradient gather advances its pixel coordinates by BK per call).
-template <int MODE, bool TAPK, int ROWS, int NTH>
+template <int MODE, bool TAPK, int ROWS, int NTH, bool DMA = false>
 struct RLoader {
   static constexpr int G = ROWS / 8, KS = NTH / G, V = BK / KS;
+  static_assert(!DMA || (G == 16 && NTH % 64 == 0), "direct loads fill 256-byte k rows of 128-row tiles");
   int rows_ok;
   int colb;      // byte offset of the row group (PLAIN, FILTER_T) or of its channel + tap shift (WGRAD)
   int tkh, tkw;  // WGRAD: filter tap of the row group
@@ -228,7 +280,10 @@ struct RLoader {
 
   __device__ void init(const OperandDev& o, int row0, int tid, int k0) {
     kk0 = tid / G;
-    const int r = row0 + (tid % G) * 8;
+    // DMA: vector t + NTH i lands in unit slot t % 16 of its k row, which
+    // holds row group slot ^ 4 (k % 4) (rcol); k % 4 = t / 16 % 4
+    const int grp = DMA ? ((tid & 15) ^ (((tid >> 4) & 3) << 2)) : tid % G;
+    const int r = row0 + grp * 8;
     rows_ok = r < o.rows;  // rows are a multiple of 8
     const uint32_t rr = rows_ok ? r : 0;
     tkh = tkw = 0;
@@ -250,7 +305,11 @@ struct RLoader {
     }
   }
 
-  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, uint4 (&reg)[4]) {
+  // Byte offsets of the thread's V vectors of the K step starting at k0
+  // (called once per K step, in order: the filter-gradient gather advances
+  // its pixel coordinates by BK per call).
+  template <class F>
+  __device__ __forceinline__ void visit(const OperandDev& o, int k0, F&& f) {
     int t0 = 0, c0 = 0;
     if (MODE == OP_R_FILTER_T && TAPK) {
       t0 = static_cast<int>(o.fdC2.div(k0));  // uniform
@@ -261,12 +320,12 @@ struct RLoader {
       const int k = k0 + kk0 + KS * i;
       const bool kok = rows_ok & (k < o.K);
       if (MODE == OP_R_PLAIN) {
-        reg[i] = bload(rs, kok ? static_cast<int>(k * o.ld * 2) + colb : OOB);
+        f(i, kok ? static_cast<int>(k * o.ld * 2) + colb : OOB);
       } else if (MODE == OP_R_CONV_WGRAD) {
         const int hh = h[i] + tkh - 1, ww = w[i] + tkw - 1;
         const bool ok = kok & (static_cast<unsigned>(hh) < static_cast<unsigned>(o.H)) &
                         (static_cast<unsigned>(ww) < static_cast<unsigned>(o.W));
-        reg[i] = bload(rs, ok ? k * o.C * 2 + colb : OOB);
+        f(i, ok ? k * o.C * 2 + colb : OOB);
         // advance this k by one K step (BK pixels) inside its image
         w[i] += o.step_w;
         const int cw = w[i] >= o.W;
@@ -282,9 +341,18 @@ struct RLoader {
           t = static_cast<int>(o.fdC2.div(k < o.K ? k : 0));
           c2 = k - t * o.C2;
         }
-        reg[i] = bload(rs, kok ? (c2 * 9 + t) * o.C * 2 + colb : OOB);
+        f(i, kok ? (c2 * 9 + t) * o.C * 2 + colb : OOB);
       }
     }
+  }
+
+  __device__ __forceinline__ void load(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, uint4 (&reg)[4]) {
+    visit(o, k0, [&](int i, int off) { reg[i] = bload(rs, off); });
+  }
+
+  __device__ __forceinline__ void dma(const OperandDev& o, __amdgpu_buffer_rsrc_t rs, int k0, uint32_t tile,
+                                      int wave) {
+    visit(o, k0, [&](int i, int off) { dma16(rs, tile + 16u * (64 * wave + NTH * i), off); });
   }
 
   __device__ __forceinline__ void store(bf16_t* lds, const uint4 (&reg)[4], int tid) const {
@@ -296,10 +364,10 @@ struct RLoader {
   }
 };
 
-template <int MODE, bool TAPK, int ROWS, int NTH>
+template <int MODE, bool TAPK, int ROWS, int NTH, bool DMA = false>
 struct LoaderFor {
-  using type = typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE, TAPK, ROWS, NTH>,
-                                         RLoader<MODE, TAPK, ROWS, NTH>>::type;
+  using type = typename std::conditional<(MODE <= OP_K_CONV_DGRAD), KLoader<MODE, TAPK, ROWS, NTH, DMA>,
+                                         RLoader<MODE, TAPK, ROWS, NTH, DMA>>::type;
 };
 
 // value = acc * alpha + bias + residuals, ReLU, then float32 and/or bf16 stores
@@ -527,12 +595,17 @@ __device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2]
 // second half of every K step; their accumulators are added through LDS at
 // the end (first half + second half), so one block per CU keeps two waves
 // on every SIMD without the narrow tile's extra operand traffic.
-template <int MA, int MB, bool TAPK, int BNT, int KSL>
+// DMA (128-wide 4-wave blocks): the operand tiles go from global memory
+// straight into a two-stage LDS ring (buffer loads with the LDS flag), with
+// no register stage and no LDS store instruction; a stage is read after its
+// own loads are counted complete and the block has synchronised.
+template <int MA, int MB, bool TAPK, int BNT, int KSL, bool DMA = false>
 __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
   constexpr int NJ = BNT / 64;   // 32-column MFMA tiles per wave
   constexpr int NTH = NT * KSL;
   constexpr int KW = BK / KSL;   // k of each K step that one wave multiplies
   static_assert(KSL == 1 || BNT == 128, "K-sliced waves use the 128-wide tile");
+  static_assert(!DMA || (KSL == 1 && BNT == 128), "direct loads serve the 128-wide 4-wave tile");
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TILE_ELEMS];  // [buffer][A|B]
 
   const int tid = threadIdx.x;
@@ -570,8 +643,8 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
   const int kend = min(args.K, kbeg + args.k_per_split);
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
-  typename LoaderFor<MA, TAPK, BM, NTH>::type la;
-  typename LoaderFor<MB, TAPK, BNT, NTH>::type lb;
+  typename LoaderFor<MA, TAPK, BM, NTH, DMA>::type la;
+  typename LoaderFor<MB, TAPK, BNT, NTH, DMA>::type lb;
   la.init(A, row0, tid, kbeg);
   lb.init(B, col0, tid, kbeg);
 
@@ -597,12 +670,15 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
       const int kl = kk + (lane >> 5) * 8;
 #pragma unroll
       for (int i = 0; i < 2; ++i)
-        fa[i] = (MA <= OP_K_CONV_DGRAD) ? frag_k(sa, wm * 64 + i * 32 + (lane & 31), kl)
-                                        : frag_r(sa, wm * 64 + i * 32, kk, lane);
+        fa[i] = (MA <= OP_K_CONV_DGRAD)
+                    ? (DMA ? frag_kd(sa, wm * 64 + i * 32 + (lane & 31), kl) : frag_k(sa, wm * 64 + i * 32 + (lane & 31), kl))
+                    : frag_r(sa, wm * 64 + i * 32, kk, lane);
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
-        fb[j] = (MB <= OP_K_CONV_DGRAD) ? frag_k(sb, wn * (32 * NJ) + j * 32 + (lane & 31), kl)
-                                        : frag_r(sb, wn * (32 * NJ) + j * 32, kk, lane);
+        fb[j] = (MB <= OP_K_CONV_DGRAD)
+                    ? (DMA ? frag_kd(sb, wn * (32 * NJ) + j * 32 + (lane & 31), kl)
+                           : frag_k(sb, wn * (32 * NJ) + j * 32 + (lane & 31), kl))
+                    : frag_r(sb, wn * (32 * NJ) + j * 32, kk, lane);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -613,7 +689,38 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
     if constexpr (MA == OP_K_CONV_DGRAD && MB == OP_R_FILTER_T) __builtin_amdgcn_s_setprio(0);
   };
 
-  if (nk > 0) {
+  if constexpr (DMA) {
+    if (nk > 0) {
+      // stage b (b = 0, 1) at elements [2 b BK 128, ...): A tile then B tile,
+      // 128 x 64 each; the prefetch of the two steps past the end reads zeros
+      // or data that is never multiplied, and is drained before the LDS is
+      // reused by the epilogue
+      constexpr int TE = BM * BK, SE = 2 * TE;
+      static_assert(sizeof(lds) >= 2 * SE * sizeof(bf16_t), "two stages fit the operand buffers");
+      constexpr int VS = decltype(la)::V + decltype(lb)::V;   // direct loads per thread per stage
+      bf16_t* const l0 = &lds[0][0][0];
+      const uint32_t lbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) bf16_t*)l0));
+      const int wv = __builtin_amdgcn_readfirstlane(wave);
+      auto issue = [&](int buf, int k0) {
+        const uint32_t t = lbase + static_cast<uint32_t>(buf * SE * 2);
+        la.dma(A, ra, k0, t, wv);
+        lb.dma(B, rb, k0, t + TE * 2, wv);
+      };
+      issue(0, kbeg);
+      issue(1, kbeg + BK);
+      dma_wait<VS>();
+      __syncthreads();
+      for (int kt = 0; kt < nk; ++kt) {
+        const bf16_t* sa = l0 + (kt & 1) * SE;
+        compute(sa, sa + TE);
+        __syncthreads();
+        issue(kt & 1, kbeg + (kt + 2) * BK);
+        dma_wait<VS>();
+        __syncthreads();
+      }
+      dma_wait<0>();
+    }
+  } else if (nk > 0) {
     uint4 ra0[4], rb0[4], ra1[4], rb1[4];
     // Prefetch loads are issued unconditionally (a step past the end reads
     // zeros or data that is never stored), so the compiler can count the
@@ -844,6 +951,8 @@ hipError_t launch(const KArgs& a, hipStream_t s) {
     if constexpr (MB != OP_K_PLAIN || (MA != OP_K_CONV_FWD && MA != OP_K_CONV_DGRAD))
       return hipErrorInvalidValue;   // 8-wave blocks serve convolution gathers against a row-major filter
     hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 2>), grid, dim3(2 * NT), 0, s, a);
+  } else if (a.dma) {
+    hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 1, true>), grid, dim3(NT), 0, s, a);
   } else {
     hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 1>), grid, dim3(NT), 0, s, a);
   }
@@ -930,6 +1039,7 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   const Shape sh = shape_of(d.M, d.N, d.K, d.batch, d.workspace ? d.workspace_bytes : 0, gather, d.concurrent);
   a.bn = sh.bn;
   a.ksl = sh.ksl;
+  a.dma = sh.bn == 128 && sh.ksl == 1;
   a.tiles_n = (d.N + a.bn - 1) / a.bn;
   a.tiles_total = a.tiles_n * ((d.M + BM - 1) / BM);
   const int splits = sh.splits;
@@ -1009,8 +1119,8 @@ const char* gemm_bf16_kernel_name(const GemmDesc& d) {
   if (ma == OP_K_CONV_DGRAD && mb == OP_R_FILTER_T) tapk = d.A.g.C % BK == 0 && d.B.g.C2 % BK == 0;
   // the kernel's template arguments as a profiler prints the instantiation
   static thread_local char buf[64];
-  std::snprintf(buf, sizeof(buf), "gemm_bf16_kernel<%d, %d, %s, %d, %d>", ma, mb, tapk ? "true" : "false",
-                a.bn == 64 ? 64 : 128, a.bn == 64 ? 1 : a.ksl);
+  std::snprintf(buf, sizeof(buf), "gemm_bf16_kernel<%d, %d, %s, %d, %d, %s>", ma, mb, tapk ? "true" : "false",
+                a.bn == 64 ? 64 : 128, a.bn == 64 ? 1 : a.ksl, a.dma ? "true" : "false");
   return buf;
 }
 
