@@ -484,14 +484,20 @@ def main():
         log(f"[bench] per-step median {ms_median:.3f} ms, min {per[0]:.3f}, max {per[-1]:.3f} "
             f"over {args.median_steps} steps")
 
-    # per-kernel pass (events around every launch, separate from the timed region)
+    # per-kernel pass (events around every launch, separate from the timed
+    # region). A single stage issues every launch on its stage stream, one at
+    # a time, with the kernels and launch shapes of the timed steps: each
+    # event-to-event duration is then the launch's own (under concurrency it
+    # would include the time the launch shares the GPU with the other streams,
+    # and a profiler's kernel trace, which also reduces that sharing, would
+    # not see the same durations).
     if pipeline:
         loop.profile(True)
         loop.steps(args.profile_steps)
         prof = loop.profile_read()
         loop.profile(False)
     else:
-        loop.st.profile(True)
+        loop.st.profile(True, serial=True)
         loop.steps(args.profile_steps)
         prof = loop.st.profile_read()
         loop.st.profile(False)
@@ -508,11 +514,16 @@ def main():
         def flush():
             with torch.cuda.stream(stream):
                 sink.append(evict.sum())
-        target = loop if pipeline else loop.st
-        target.profile(True)
+        if pipeline:
+            loop.profile(True)
+        else:
+            loop.st.profile(True, serial=True)
         loop.steps(args.cold_steps, before_update=flush)
         cold = loop.profile_read() if pipeline else loop.st.profile_read()
-        target.profile(False)
+        if pipeline:
+            loop.profile(False)
+        else:
+            loop.st.profile(False)
         torch.cuda.synchronize()
         del evict, sink
         u = cold.get("fused_update")

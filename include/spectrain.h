@@ -229,9 +229,14 @@ int spectrain_stage_set_state(spectrain_stage_t st, const float* W_host, const f
 int spectrain_stage_get_predicted(spectrain_stage_t st, int32_t slot, float* What_host);
 
 /* Per-kernel launch statistics of a stage, collected between
- * spectrain_stage_profile(st, 1) and a read. Durations come from HIP events
- * recorded around every launch on the stage's stream (which serialises the
- * launches: use a separate pass, not the timed one). flops and bytes are the
+ * spectrain_stage_profile(st, 1 or 2) and a read. Durations come from HIP
+ * events recorded around every launch on the stream it runs on (use a
+ * separate pass, not the timed one). With enable == 2 every launch of the
+ * stage, including the weight gradients and the forward of
+ * spectrain_stage_forward_backward, is issued on the stage's stream, one at
+ * a time, with the kernels and launch shapes of the concurrent call: each
+ * duration is then the launch's own, not shared with launches of the other
+ * streams. flops and bytes are the
  * algorithmic work of the launches: 2*M*N*K per GEMM (3x3 convolutions count
  * all 9 taps); for a GEMM each operand tensor read once (a convolution's
  * feature map once, not once per tap), each output written once and each
@@ -252,8 +257,9 @@ typedef struct {
   double extra_bytes_total;   /* bytes beyond the algorithmic ones (split-K partial planes) */
 } spectrain_kernel_stat;
 
-/* enable != 0: clear the statistics and time every following launch;
- * enable == 0: stop timing (statistics are kept for reading). */
+/* enable 1 or 2: clear the statistics and time every following launch (2:
+ * with every launch issued on the stage's stream, see above); enable == 0:
+ * stop timing (statistics are kept for reading). EINVAL for other values. */
 int spectrain_stage_profile(spectrain_stage_t st, int32_t enable);
 
 /* Copy up to capacity kernel families into out (in first-launch order) and

@@ -123,7 +123,10 @@ int spectrain_stage_read_stash(spectrain_stage_t st, int64_t mb_id, int32_t inde
 }
 
 int spectrain_stage_profile(spectrain_stage_t st, int32_t enable) {
-  return guarded(st, [&](spx::Stage& x) { x.profile(enable != 0); }, false);
+  return guarded(st, [&](spx::Stage& x) {
+    if (enable < 0 || enable > 2) throw spx::StageError(SPECTRAIN_EINVAL, "profile mode must be 0, 1 or 2");
+    x.profile(enable != 0, enable == 2);
+  }, false);
 }
 
 int spectrain_stage_profile_read(spectrain_stage_t st, spectrain_kernel_stat* out, int32_t capacity, int32_t* count) {

@@ -304,13 +304,14 @@ void Stage::prof_collect() {
   prof_used_ = 0;
 }
 
-void Stage::profile(bool enable) {
+void Stage::profile(bool enable, bool serial) {
   if (enable) {
     prof_collect();
     prof_stats_.clear();
     prof_index_.clear();
   }
   prof_on_ = enable;
+  serial_ = enable && serial;
 }
 
 int Stage::profile_read(spectrain_kernel_stat* out, int capacity) {
@@ -779,7 +780,7 @@ void Stage::forward_backward(int64_t mb_f, const void* x, void* y, const int32_t
   // (the update that refreshed its weights)
   hip_check(hipEventRecord(ffork_ev_, s_), "hipEventRecord");
   hip_check(hipStreamWaitEvent(s3_, ffork_ev_, 0), "hipStreamWaitEvent");
-  ls_ = s3_;
+  ls_ = serial_ ? s_ : s3_;
   wsb_ = &ws_block_f_;
   concurrent_ = true;
   try {

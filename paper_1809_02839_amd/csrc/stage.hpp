@@ -103,7 +103,9 @@ class Stage {
   size_t read_stash(int64_t mb, int index, void* host, size_t capacity);
   bool nonfinite() const { return *reinterpret_cast<volatile int*>(flag_.host()) != 0; }
   void sync();
-  void profile(bool enable);
+  // serial: every launch on the stage stream (forward_backward's forward and
+  // the weight gradients included), for each launch's own duration
+  void profile(bool enable, bool serial = false);
   int profile_read(spectrain_kernel_stat* out, int capacity);
 
  private:
@@ -138,6 +140,10 @@ class Stage {
   // Any launches issued by `issue` on the side stream (they launch on ls_).
   template <typename F>
   void on_side(std::initializer_list<const void*> reads, F&& issue) {
+    if (serial_) {   // profiling one launch at a time: the side launches stay on the stage stream
+      issue();
+      return;
+    }
     hip_check(hipEventRecord(fork_ev_, s_), "hipEventRecord");
     hip_check(hipStreamWaitEvent(s2_, fork_ev_, 0), "hipStreamWaitEvent");
     ls_ = s2_;
@@ -259,6 +265,7 @@ class Stage {
     double flops, bytes, extra;
   };
   bool prof_on_ = false;
+  bool serial_ = false;                  // profile mode 2: every launch on the stage stream
   std::vector<hipEvent_t> prof_pool_;
   size_t prof_used_ = 0;
   std::vector<ProfRec> prof_recs_;

@@ -227,8 +227,9 @@ class Stage:
                                                     ctypes.byref(n)))
         return out
 
-    def profile(self, enable: bool):
-        _check(lib().spectrain_stage_profile(self.h, 1 if enable else 0))
+    def profile(self, enable: bool, serial: bool = False):
+        """Time every launch (serial: each on the stage stream, one at a time)."""
+        _check(lib().spectrain_stage_profile(self.h, (2 if serial else 1) if enable else 0))
 
     def profile_read(self):
         """{family: dict(launches, ms_total, flops_total, bytes_total, extra_bytes_total)} in first-launch order."""

@@ -177,3 +177,38 @@ def test_last_stage_has_no_free_slot():
         torch.cuda.synchronize()
     finally:
         drv.st.destroy()
+
+
+def test_serial_profile_mode_is_bitwise_and_times_every_launch():
+    """Profile mode 2 issues every launch of the combined call on the stage
+    stream, one at a time (the durations are the launches' own): results stay
+    bitwise equal, every kernel family of both passes is timed, and modes
+    other than 0, 1, 2 are refused."""
+    from paper_1809_02839_amd import native
+    spec = CASES["resnet_bottleneck_small"]
+    d = spec.num_stages - spec.stage_index
+    ref, alt = _Driver(spec, True), _Driver(spec, True)
+    try:
+        assert native.lib().spectrain_stage_profile(alt.st.h, 3) == native.EINVAL
+        alt.st.profile(True, serial=True)
+        for drv in (ref, alt):
+            for m in range(d - 1):
+                drv.forward(m)
+            for m in range(3):
+                drv.step(m + d - 1, m)
+        prof = alt.st.profile_read()
+        alt.st.profile(False)
+        for key in ref.out:
+            a, b = ref.out[key], alt.out[key]
+            if key[0] == "state":
+                assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), key
+            else:
+                assert torch.equal(a, b), key
+        names = " ".join(prof)
+        # forward (conv3x3 gather), data gradients, weight gradients, the update
+        for fam in ("gemm_bf16_kernel<1, 0,", "gemm_bf16_kernel<0, 3,", "gemm_bf16_kernel<3, 3,", "fused_update"):
+            assert fam in names, (fam, sorted(prof))
+        assert all(v["launches"] > 0 and v["ms_total"] > 0 for v in prof.values())
+    finally:
+        ref.st.destroy()
+        alt.st.destroy()
