@@ -156,6 +156,8 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, int byte_off) {
 // compiler, which cannot tell the stages of the LDS ring apart, does not wait
 // for every outstanding direct load before each LDS read: the K loop waits
 // for exactly the stage it reads (dma_wait) and then synchronises the block.
+// The statement declares M0 clobbered; nothing else in these kernels keeps a
+// value in M0 (a host test checks the assembly for it).
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t lds_base, int byte_off) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds_base), "v"(byte_off), "s"(r)
                : "memory", "m0");
