@@ -1,6 +1,8 @@
-// float32 GEMM for float32 stages (the small fully-connected workload):
-// 64 x 64 block tile, K step 16, 256 threads each computing a 4 x 4 patch
-// with FMAs. Any M, N, K and leading dimension; plain operand modes only.
+// float32 GEMM for float32 stages (the small fully-connected workload) on
+// the matrix cores: 64 x 64 block tile, K step 16 staged in LDS as [k][row],
+// 4 waves each owning a 32 x 32 sub-tile of v_mfma_f32_32x32x2_f32 (eight
+// per K step; float32 operands, float32 accumulation). Any M, N, K and
+// leading dimension; plain operand modes only.
 // These stages are a few MFLOP per layer, so latency rather than matrix-core
 // throughput bounds them: when the tiles are few and K is long, K is split
 // over blocks (each block's K loop stays short) and a second pass sums the
@@ -67,46 +69,42 @@ __device__ __forceinline__ void epilogue_f32(const F32Args& a, int row, int col,
   else a.out[idx] = v;
 }
 
+// Wave w owns rows 32 (w / 2) .. and columns 32 (w % 2) .. of the block
+// tile. Each MFMA takes two k: lane l supplies k = l / 32 of row l % 32 of
+// each operand (B first, so the output's register layout is indexed by B's
+// columns): lane l then holds output row l % 32 of columns
+// 8 (r / 4) + 4 (l / 32) + r % 4 in register r.
 template <int MA, int MB>
 __global__ __launch_bounds__(NT) void gemm_f32_kernel(F32Args a) {
   __shared__ float As[TK][TB + 4];
   __shared__ float Bs[TK][TB + 4];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row0 = blockIdx.y * TB, col0 = blockIdx.x * TB;
-  const int tx = tid & 15, ty = tid >> 4;
-  float acc[4][4] = {};
+  const int wm = wave >> 1, wn = wave & 1;
+  f32x16_t acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
   const int kbeg = blockIdx.z * a.k_per_split, kend = min(a.K, kbeg + a.k_per_split);
+  const int ra = wm * 32 + (lane & 31), rb = wn * 32 + (lane & 31), kh = lane >> 5;
   for (int k0 = kbeg; k0 < kend; k0 += TK) {
     load_tile<MA>(a.A, a.lda, a.M, kend, row0, k0, tid, As);
     load_tile<MB>(a.B, a.ldb, a.N, kend, col0, k0, tid, Bs);
     __syncthreads();
 #pragma unroll
-    for (int k = 0; k < TK; ++k) {
-      float av[4], bv[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = As[k][ty * 4 + i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) bv[j] = Bs[k][tx * 4 + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
-    }
+    for (int k = 0; k < TK; k += 2)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(Bs[k + kh][rb], As[k + kh][ra], acc, 0, 0, 0);
     __syncthreads();
   }
+  const int row = row0 + ra;
+  if (row >= a.M) return;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = row0 + ty * 4 + i;
-    if (row >= a.M) continue;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = col0 + tx * 4 + j;
-      if (col >= a.N) continue;
-      if (a.splits > 1)
-        a.partial[(static_cast<long>(blockIdx.z) * a.M + row) * a.N + col] = acc[i][j];
-      else
-        epilogue_f32(a, row, col, acc[i][j]);
-    }
+  for (int r = 0; r < 16; ++r) {
+    const int col = col0 + wn * 32 + 8 * (r >> 2) + 4 * kh + (r & 3);
+    if (col >= a.N) continue;
+    if (a.splits > 1)
+      a.partial[(static_cast<long>(blockIdx.z) * a.M + row) * a.N + col] = acc[r];
+    else
+      epilogue_f32(a, row, col, acc[r]);
   }
 }
 
