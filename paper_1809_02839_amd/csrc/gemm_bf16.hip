@@ -396,7 +396,11 @@ __device__ __forceinline__ void epilogue(const EpiDev& e, long idx, int col, flo
 // stores; needs idx and col multiples of 4 and 16-byte aligned float32 (8-byte
 // aligned bf16) tensors, which the host checks.
 __device__ __forceinline__ void epilogue4(const EpiDev& e, long idx, int col, float4 a) {
-  float v[4] = {a.x * e.alpha, a.y * e.alpha, a.z * e.alpha, a.w * e.alpha};
+  float v[4] = {a.x, a.y, a.z, a.w};
+  if (e.alpha != 1.0f) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] *= e.alpha;
+  }
   auto unpack = [](uint2 u, float (&f)[4]) {
     f[0] = bf16_to_f32(static_cast<bf16_t>(u.x & 0xffff));
     f[1] = bf16_to_f32(static_cast<bf16_t>(u.x >> 16));
@@ -434,16 +438,12 @@ __device__ __forceinline__ void epilogue4(const EpiDev& e, long idx, int col, fl
     *o = make_float4(v[0], v[1], v[2], v[3]);
   }
   if (e.out_bf16) {
-    uint32_t h[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) h[q] = f32_to_bf16(v[q]);
     if (e.mask) {
       unpack(*reinterpret_cast<const uint2*>(e.mask + idx), t);
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (!(t[q] > 0.0f)) h[q] = 0;
+      for (int q = 0; q < 4; ++q) v[q] = t[q] > 0.0f ? v[q] : 0.0f;
     }
-    *reinterpret_cast<uint2*>(e.out_bf16 + idx) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    *reinterpret_cast<uint2*>(e.out_bf16 + idx) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
   }
 }
 
@@ -454,7 +454,11 @@ __device__ __forceinline__ void epilogue4(const EpiDev& e, long idx, int col, fl
 // positive).
 __device__ __forceinline__ uint2 epilogue4_values(const EpiDev& e, long idx, int col, float4 a, uint2 bb, uint2 rb,
                                                   uint2 mk) {
-  float v[4] = {a.x * e.alpha, a.y * e.alpha, a.z * e.alpha, a.w * e.alpha};
+  float v[4] = {a.x, a.y, a.z, a.w};
+  if (e.alpha != 1.0f) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] *= e.alpha;
+  }
   auto unpack = [](uint2 u, float (&f)[4]) {
     f[0] = bf16_to_f32(static_cast<bf16_t>(u.x & 0xffff));
     f[1] = bf16_to_f32(static_cast<bf16_t>(u.x >> 16));
@@ -491,16 +495,12 @@ __device__ __forceinline__ uint2 epilogue4_values(const EpiDev& e, long idx, int
     }
     *o = make_float4(v[0], v[1], v[2], v[3]);
   }
-  uint32_t h[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) h[q] = f32_to_bf16(v[q]);
   if (e.mask) {
     unpack(mk, t);
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (!(t[q] > 0.0f)) h[q] = 0;
+    for (int q = 0; q < 4; ++q) v[q] = t[q] > 0.0f ? v[q] : 0.0f;
   }
-  return make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+  return make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
 }
 
 // epilogue4 with the bf16 operands already loaded (see epilogue4_values).
@@ -590,6 +590,85 @@ __device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2]
   }
 }
 
+// The bf16 operands of the staged epilogue (below) for one thread: the bias
+// of its 8 columns and the residual and mask of its NP row segments (8
+// columns each, rows erl + RPP p of the tile).
+template <int BNT>
+struct EpiOperands {
+  static constexpr int TPR = BNT / 8;   // threads per row
+  static constexpr int RPP = NT / TPR;  // rows per pass
+  static constexpr int NP = 128 / RPP;  // rows per thread
+  uint4 bb, rb[NP], mk[NP];
+
+  __device__ __forceinline__ void load(const KArgs& args, int row0, int col0, int tid, long coff) {
+    const EpiDev& e = args.e;
+    const int ecol = col0 + (tid % TPR) * 8, erl = tid / TPR;
+    const bool colok = ecol < args.N;
+    bb = make_uint4(0, 0, 0, 0);
+    if (colok && !e.bias && e.bias_bf16) bb = *reinterpret_cast<const uint4*>(e.bias_bf16 + ecol);
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int row = row0 + erl + p * RPP;
+      const long idx = coff + static_cast<long>(row) * e.ldc + ecol;
+      rb[p] = mk[p] = make_uint4(0, 0, 0, 0);
+      if (colok && row < args.M) {
+        if (e.res_bf16) rb[p] = *reinterpret_cast<const uint4*>(e.res_bf16 + idx);
+        if (e.mask) mk[p] = *reinterpret_cast<const uint4*>(e.mask + idx);
+      }
+    }
+  }
+};
+
+// The staged epilogue's rows for one combination of bf16 operands known at
+// compile time (bias, residual, ReLU, mask; alpha 1, no float32 output) on a
+// tile inside the output: straight-line code whose NP rows the compiler can
+// interleave. The operations and their order are those of epilogue4_values,
+// so both paths give the same bits.
+template <int BNT, bool BIAS, bool RES, bool RELU, bool MASK>
+__device__ __forceinline__ void staged_rows(const EpiDev& e, const float* tile, const EpiOperands<BNT>& eop,
+                                            bf16_t* out, int ecl, int erl) {
+  constexpr int EP = BNT + 4, RPP = EpiOperands<BNT>::RPP, NP = EpiOperands<BNT>::NP;
+  auto unpack8 = [](uint4 u, float (&f)[8]) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      f[2 * q] = __uint_as_float(w[q] << 16);
+      f[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+    }
+  };
+  float bias[8];
+  if constexpr (BIAS) unpack8(eop.bb, bias);
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int rr = erl + p * RPP;
+    const float4 a0 = *reinterpret_cast<const float4*>(tile + rr * EP + ecl);
+    const float4 a1 = *reinterpret_cast<const float4*>(tile + rr * EP + ecl + 4);
+    float v[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+    if constexpr (BIAS) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += bias[q];
+    }
+    if constexpr (RES) {
+      float r[8];
+      unpack8(eop.rb[p], r);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += r[q];
+    }
+    if constexpr (RELU) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = fmaxf(v[q], 0.0f);
+    }
+    if constexpr (MASK) {
+      float m[8];
+      unpack8(eop.mk[p], m);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = m[q] > 0.0f ? v[q] : 0.0f;
+    }
+    *reinterpret_cast<uint4*>(out + static_cast<long>(rr) * e.ldc) =
+        make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+  }
+}
+
 // BNT: block tile width in N (128, or 64 for launches whose 128-wide tiles
 // cannot give every CU two blocks); each wave owns 64 x (BNT / 2).
 // KSL: waves per output sub-tile. With KSL = 2 (8 waves, 128-wide tiles
@@ -649,6 +728,19 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
   typename LoaderFor<MB, TAPK, BNT, NTH, DMA>::type lb;
   la.init(A, row0, tid, kbeg);
   lb.init(B, col0, tid, kbeg);
+
+  // The staged epilogue's operands do not depend on the product: the
+  // direct-load kernels, which hold no operand tiles in registers, issue
+  // their loads before the first K step so that they arrive while the block
+  // multiplies (the register-staged loop has no registers to spare for them
+  // and loads them in the epilogue). Issued before the first direct loads,
+  // they are older than every stage the K loop waits for.
+  const bool staged_epi = KSL == 1 && args.splits == 1 && args.vec8;
+  const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
+  EpiOperands<BNT> eop;
+  if constexpr (DMA) {
+    if (staged_epi) eop.load(args, row0, col0, tid, coff);
+  }
 
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = (wave >> 1) & 1, wn = wave & 1, kslice = wave >> 2;
@@ -782,7 +874,7 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
         for (int r = 0; r < 16; ++r) acc[i][j][r] += mine[((i * NJ + j) * 16 + r) * 64];
   }
   if constexpr (KSL == 1) {
-    if (args.splits == 1 && args.vec8) {
+    if (staged_epi) {
       // float32 tile [128][BNT] in LDS (row pitch BNT + 4 floats), then each
       // thread takes 8 consecutive columns of NP rows: every load and store
       // of the epilogue covers whole row segments. All of a thread's operand
@@ -791,26 +883,15 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
       // operations, so a load issued after a store would wait for the store
       // to complete and every row would cost a memory round trip.
       constexpr int EP = BNT + 4;
-      constexpr int TPR = BNT / 8;          // threads per row
-      constexpr int RPP = NT / TPR;         // rows per pass
-      constexpr int NP = 128 / RPP;         // rows per thread
+      constexpr int TPR = EpiOperands<BNT>::TPR, RPP = EpiOperands<BNT>::RPP, NP = EpiOperands<BNT>::NP;
       const int ecl = (tid % TPR) * 8, erl = tid / TPR;
       const int ecol = col0 + ecl;
-      const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
       const EpiDev& e = args.e;
       const bool colok = ecol < args.N;
-      uint4 ebb = make_uint4(0, 0, 0, 0), erb[NP], emk[NP];
-      if (colok && !e.bias && e.bias_bf16) ebb = *reinterpret_cast<const uint4*>(e.bias_bf16 + ecol);
-#pragma unroll
-      for (int p = 0; p < NP; ++p) {
-        const int row = row0 + erl + p * RPP;
-        const long idx = coff + static_cast<long>(row) * e.ldc + ecol;
-        erb[p] = emk[p] = make_uint4(0, 0, 0, 0);
-        if (colok && row < args.M) {
-          if (e.res_bf16) erb[p] = *reinterpret_cast<const uint4*>(e.res_bf16 + idx);
-          if (e.mask) emk[p] = *reinterpret_cast<const uint4*>(e.mask + idx);
-        }
-      }
+      if constexpr (!DMA) eop.load(args, row0, col0, tid, coff);
+      const uint4 ebb = eop.bb;
+      const uint4 (&erb)[NP] = eop.rb;
+      const uint4 (&emk)[NP] = eop.mk;
       float* tile = reinterpret_cast<float*>(&lds[0][0][0]);
       static_assert(sizeof(lds) >= 128 * (BNT + 4) * sizeof(float), "the float32 tile fits the operand buffers");
       __syncthreads();
@@ -826,6 +907,26 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
                 make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
           }
       __syncthreads();
+      // whole tiles with only bf16 operands: the specialised rows
+      if (e.out_bf16 && !e.out_f32 && !e.bias && !e.res_f32 && e.alpha == 1.0f && row0 + 128 <= args.M &&
+          col0 + BNT <= args.N) {
+        bf16_t* const out = e.out_bf16 + coff + static_cast<long>(row0) * e.ldc + ecol;   // row rr at + rr ldc
+        const int kind = (e.bias_bf16 ? 1 : 0) | (e.res_bf16 ? 2 : 0) | (e.relu ? 4 : 0) | (e.mask ? 8 : 0);
+        bool done = true;
+        switch (kind) {
+          case 0: staged_rows<BNT, false, false, false, false>(e, tile, eop, out, ecl, erl); break;
+          case 1: staged_rows<BNT, true, false, false, false>(e, tile, eop, out, ecl, erl); break;
+          case 2: staged_rows<BNT, false, true, false, false>(e, tile, eop, out, ecl, erl); break;
+          case 3: staged_rows<BNT, true, true, false, false>(e, tile, eop, out, ecl, erl); break;
+          case 4: staged_rows<BNT, false, false, true, false>(e, tile, eop, out, ecl, erl); break;
+          case 5: staged_rows<BNT, true, false, true, false>(e, tile, eop, out, ecl, erl); break;
+          case 6: staged_rows<BNT, false, true, true, false>(e, tile, eop, out, ecl, erl); break;
+          case 8: staged_rows<BNT, false, false, false, true>(e, tile, eop, out, ecl, erl); break;
+          case 10: staged_rows<BNT, false, true, false, true>(e, tile, eop, out, ecl, erl); break;
+          default: done = false;
+        }
+        if (done) return;
+      }
 #pragma unroll
       for (int p = 0; p < NP; ++p) {
         const int rr = erl + p * RPP, row = row0 + rr;
