@@ -593,10 +593,10 @@ __device__ __forceinline__ void write_tile(const KArgs& args, f32x16_t (&acc)[2]
 // The bf16 operands of the staged epilogue (below) for one thread: the bias
 // of its 8 columns and the residual and mask of its NP row segments (8
 // columns each, rows erl + RPP p of the tile).
-template <int BNT>
+template <int BNT, int NTH>
 struct EpiOperands {
   static constexpr int TPR = BNT / 8;   // threads per row
-  static constexpr int RPP = NT / TPR;  // rows per pass
+  static constexpr int RPP = NTH / TPR; // rows per pass
   static constexpr int NP = 128 / RPP;  // rows per thread
   uint4 bb, rb[NP], mk[NP];
 
@@ -624,10 +624,10 @@ struct EpiOperands {
 // tile inside the output: straight-line code whose NP rows the compiler can
 // interleave. The operations and their order are those of epilogue4_values,
 // so both paths give the same bits.
-template <int BNT, bool BIAS, bool RES, bool RELU, bool MASK>
-__device__ __forceinline__ void staged_rows(const EpiDev& e, const float* tile, const EpiOperands<BNT>& eop,
+template <int BNT, int NTH, bool BIAS, bool RES, bool RELU, bool MASK>
+__device__ __forceinline__ void staged_rows(const EpiDev& e, const float* tile, const EpiOperands<BNT, NTH>& eop,
                                             bf16_t* out, int ecl, int erl) {
-  constexpr int EP = BNT + 4, RPP = EpiOperands<BNT>::RPP, NP = EpiOperands<BNT>::NP;
+  constexpr int EP = BNT + 4, RPP = EpiOperands<BNT, NTH>::RPP, NP = EpiOperands<BNT, NTH>::NP;
   auto unpack8 = [](uint4 u, float (&f)[8]) {
     const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
@@ -676,17 +676,22 @@ __device__ __forceinline__ void staged_rows(const EpiDev& e, const float* tile, 
 // second half of every K step; their accumulators are added through LDS at
 // the end (first half + second half), so one block per CU keeps two waves
 // on every SIMD without the narrow tile's extra operand traffic.
-// DMA (128-wide 4-wave blocks): the operand tiles go from global memory
-// straight into a two-stage LDS ring (buffer loads with the LDS flag), with
-// no register stage and no LDS store instruction; a stage is read after its
-// own loads are counted complete and the block has synchronised.
+// DMA (128-wide tiles, 4- or 8-wave blocks): the operand tiles go from
+// global memory straight into a two-stage LDS ring (buffer loads with the
+// LDS flag), with no register stage and no LDS store instruction; a stage is
+// read after its own loads are counted complete and the block has
+// synchronised. A wave that issues its share of a stage's direct loads
+// waits for the memory pipeline to accept them, about as long as its MFMAs
+// of a K step take; on 8-wave blocks the two waves of a SIMD issue half as
+// many loads each and one multiplies while the other waits.
 template <int MA, int MB, bool TAPK, int BNT, int KSL, bool DMA = false>
 __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
   constexpr int NJ = BNT / 64;   // 32-column MFMA tiles per wave
   constexpr int NTH = NT * KSL;
   constexpr int KW = BK / KSL;   // k of each K step that one wave multiplies
   static_assert(KSL == 1 || BNT == 128, "K-sliced waves use the 128-wide tile");
-  static_assert(!DMA || (KSL == 1 && BNT == 128), "direct loads serve the 128-wide 4-wave tile");
+  static_assert(!DMA || BNT == 128, "direct loads serve the 128-wide tile");
+  static_assert(KSL == 1 || DMA, "8-wave blocks load their operands directly");
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TILE_ELEMS];  // [buffer][A|B]
 
   const int tid = threadIdx.x;
@@ -730,15 +735,16 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
   lb.init(B, col0, tid, kbeg);
 
   // The staged epilogue's operands do not depend on the product: the
-  // direct-load kernels, which hold no operand tiles in registers, issue
-  // their loads before the first K step so that they arrive while the block
-  // multiplies (the register-staged loop has no registers to spare for them
-  // and loads them in the epilogue). Issued before the first direct loads,
-  // they are older than every stage the K loop waits for.
-  const bool staged_epi = KSL == 1 && args.splits == 1 && args.vec8;
+  // direct-load 4-wave kernels, which hold no operand tiles in registers,
+  // issue their loads before the first K step so that they arrive while the
+  // block multiplies (the register-staged loop, and the 8-wave blocks with
+  // half the registers per wave, have none to spare for them and load them
+  // in the epilogue). Issued before the first direct loads, they are older
+  // than every stage the K loop waits for.
+  const bool staged_epi = args.splits == 1 && args.vec8;
   const long coff = z1 * args.c_bs1 + z2 * args.c_bs2;
-  EpiOperands<BNT> eop;
-  if constexpr (DMA) {
+  EpiOperands<BNT, NTH> eop;
+  if constexpr (DMA && KSL == 1) {
     if (staged_epi) eop.load(args, row0, col0, tid, coff);
   }
 
@@ -865,15 +871,22 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
           for (int r = 0; r < 16; ++r) mine[((i * NJ + j) * 16 + r) * 64] = acc[i][j][r];
     }
     __syncthreads();
-    if (kslice == 1) return;
+    if (kslice == 0) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] += mine[((i * NJ + j) * 16 + r) * 64];
+          for (int r = 0; r < 16; ++r) acc[i][j][r] += mine[((i * NJ + j) * 16 + r) * 64];
+    }
+    if (!staged_epi) {
+      if (kslice == 1) return;
+      write_tile<NJ>(args, acc, row0, col0, wm, wn, lane, split, z, z1, z2);
+      return;
+    }
+    __syncthreads();   // the sums are read before the staged tile overwrites them
   }
-  if constexpr (KSL == 1) {
+  {
     if (staged_epi) {
       // float32 tile [128][BNT] in LDS (row pitch BNT + 4 floats), then each
       // thread takes 8 consecutive columns of NP rows: every load and store
@@ -883,29 +896,32 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
       // operations, so a load issued after a store would wait for the store
       // to complete and every row would cost a memory round trip.
       constexpr int EP = BNT + 4;
-      constexpr int TPR = EpiOperands<BNT>::TPR, RPP = EpiOperands<BNT>::RPP, NP = EpiOperands<BNT>::NP;
+      using EO = EpiOperands<BNT, NTH>;
+      constexpr int TPR = EO::TPR, RPP = EO::RPP, NP = EO::NP;
       const int ecl = (tid % TPR) * 8, erl = tid / TPR;
       const int ecol = col0 + ecl;
       const EpiDev& e = args.e;
       const bool colok = ecol < args.N;
-      if constexpr (!DMA) eop.load(args, row0, col0, tid, coff);
+      if constexpr (!(DMA && KSL == 1)) eop.load(args, row0, col0, tid, coff);
       const uint4 ebb = eop.bb;
       const uint4 (&erb)[NP] = eop.rb;
       const uint4 (&emk)[NP] = eop.mk;
       float* tile = reinterpret_cast<float*>(&lds[0][0][0]);
       static_assert(sizeof(lds) >= 128 * (BNT + 4) * sizeof(float), "the float32 tile fits the operand buffers");
-      __syncthreads();
+      if constexpr (KSL == 1) __syncthreads();   // every wave has read its last operand tile
+      if (kslice == 0) {                         // 8-wave blocks: the first-half waves hold the sums
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < NJ; ++j)
+          for (int j = 0; j < NJ; ++j)
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int r = wm * 64 + i * 32 + (lane & 31);
-            const int c = wn * (32 * NJ) + j * 32 + 8 * g + 4 * (lane >> 5);
-            *reinterpret_cast<float4*>(tile + r * EP + c) =
-                make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
-          }
+            for (int g = 0; g < 4; ++g) {
+              const int r = wm * 64 + i * 32 + (lane & 31);
+              const int c = wn * (32 * NJ) + j * 32 + 8 * g + 4 * (lane >> 5);
+              *reinterpret_cast<float4*>(tile + r * EP + c) =
+                  make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+            }
+      }
       __syncthreads();
       // whole tiles with only bf16 operands: the specialised rows
       if (e.out_bf16 && !e.out_f32 && !e.bias && !e.res_f32 && e.alpha == 1.0f && row0 + 128 <= args.M &&
@@ -914,15 +930,15 @@ __global__ __launch_bounds__(NT * KSL, 2) void gemm_bf16_kernel(KArgs args) {
         const int kind = (e.bias_bf16 ? 1 : 0) | (e.res_bf16 ? 2 : 0) | (e.relu ? 4 : 0) | (e.mask ? 8 : 0);
         bool done = true;
         switch (kind) {
-          case 0: staged_rows<BNT, false, false, false, false>(e, tile, eop, out, ecl, erl); break;
-          case 1: staged_rows<BNT, true, false, false, false>(e, tile, eop, out, ecl, erl); break;
-          case 2: staged_rows<BNT, false, true, false, false>(e, tile, eop, out, ecl, erl); break;
-          case 3: staged_rows<BNT, true, true, false, false>(e, tile, eop, out, ecl, erl); break;
-          case 4: staged_rows<BNT, false, false, true, false>(e, tile, eop, out, ecl, erl); break;
-          case 5: staged_rows<BNT, true, false, true, false>(e, tile, eop, out, ecl, erl); break;
-          case 6: staged_rows<BNT, false, true, true, false>(e, tile, eop, out, ecl, erl); break;
-          case 8: staged_rows<BNT, false, false, false, true>(e, tile, eop, out, ecl, erl); break;
-          case 10: staged_rows<BNT, false, true, false, true>(e, tile, eop, out, ecl, erl); break;
+          case 0: staged_rows<BNT, NTH, false, false, false, false>(e, tile, eop, out, ecl, erl); break;
+          case 1: staged_rows<BNT, NTH, true, false, false, false>(e, tile, eop, out, ecl, erl); break;
+          case 2: staged_rows<BNT, NTH, false, true, false, false>(e, tile, eop, out, ecl, erl); break;
+          case 3: staged_rows<BNT, NTH, true, true, false, false>(e, tile, eop, out, ecl, erl); break;
+          case 4: staged_rows<BNT, NTH, false, false, true, false>(e, tile, eop, out, ecl, erl); break;
+          case 5: staged_rows<BNT, NTH, true, false, true, false>(e, tile, eop, out, ecl, erl); break;
+          case 6: staged_rows<BNT, NTH, false, true, true, false>(e, tile, eop, out, ecl, erl); break;
+          case 8: staged_rows<BNT, NTH, false, false, false, true>(e, tile, eop, out, ecl, erl); break;
+          case 10: staged_rows<BNT, NTH, false, true, false, true>(e, tile, eop, out, ecl, erl); break;
           default: done = false;
         }
         if (done) return;
@@ -1051,13 +1067,9 @@ hipError_t launch(const KArgs& a, hipStream_t s) {
   if (a.bn == 64) {
     hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 64, 1>), grid, dim3(NT), 0, s, a);
   } else if (a.ksl == 2) {
-    if constexpr (MB != OP_K_PLAIN || (MA != OP_K_CONV_FWD && MA != OP_K_CONV_DGRAD))
-      return hipErrorInvalidValue;   // 8-wave blocks serve convolution gathers against a row-major filter
-    hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 2>), grid, dim3(2 * NT), 0, s, a);
-  } else if (a.dma) {
-    hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 1, true>), grid, dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 2, true>), grid, dim3(2 * NT), 0, s, a);
   } else {
-    hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 1>), grid, dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MA, MB, TAPK, 128, 1, true>), grid, dim3(NT), 0, s, a);
   }
   return hipGetLastError();
 }
@@ -1079,7 +1091,11 @@ constexpr long kTargetBlocks = 2 * kCUs;   // two resident 4-wave blocks per CU
 //    whose 128-wide tiles give between 7/8 of the CUs and every CU one block
 //    runs them on 8-wave blocks instead (ksl = 2; its gathered A operand is
 //    then loaded once per 128 x 128 outputs). Other operand pairs, and
-//    launches filling fewer CUs, were measured slower on 8-wave blocks.
+//    launches filling fewer CUs, were measured slower on 8-wave blocks (with
+//    direct loads too: every launch of at most one 128-wide block per CU on
+//    8-wave blocks made the 1x1 and filter-gradient launches no faster or
+//    slower alone, and the concurrent bottleneck step 20 % slower, its
+//    8-wave blocks leaving no room on their CUs for the other pass).
 //  * A split gives each slice at least 12 K steps (shorter slices cost more
 //    in the reduction than they gain), at most MAX_SPLITS slices and no more
 //    partials than the workspace holds.
@@ -1142,7 +1158,7 @@ bool plan(const GemmDesc& d, KArgs& a, hipError_t& err) {
   const Shape sh = shape_of(d.M, d.N, d.K, d.batch, d.workspace ? d.workspace_bytes : 0, gather, d.concurrent);
   a.bn = sh.bn;
   a.ksl = sh.ksl;
-  a.dma = sh.bn == 128 && sh.ksl == 1;
+  a.dma = sh.bn == 128;
   a.tiles_n = (d.N + a.bn - 1) / a.bn;
   a.tiles_total = a.tiles_n * ((d.M + BM - 1) / BM);
   const int splits = sh.splits;

@@ -145,3 +145,34 @@ def test_narrow_tile_ragged_edges_stepwise():
     print(f"[stepwise] {wl.name}", flush=True)
     worst = run_stepwise(wl, wl.steps, torch)
     print(f"[stepwise] {wl.name}: {worst.report()}", flush=True)
+
+
+def test_bf16_rounding_through_predict():
+    """The bf16 copies are rounded to nearest, ties to even, on every float32
+    input class: ties going down and up, neighbours of ties, overflow of the
+    largest float to infinity, subnormals (ties included) and signed zeros,
+    plus random bit patterns. With v = 0 the prediction of Eq. 4 is W itself,
+    so the predicted slot holds exactly the rounded W; the expected bits come
+    from the integer definition (u + 0x7fff + bit 16 of u) >> 16."""
+    from paper_1809_02839_amd import native
+    spec = synth.StageSpec("fc", "bf16", "none", 0, 2, 4, 1, (256, 256, 256), 0.01, 0.9)
+    st = native.Stage(native.desc_from_spec(spec), synth.initial_params(spec), torch.cuda.current_stream())
+    try:
+        n = st.n_params
+        special = np.array([0x3f808000, 0x3f818000, 0x3f808001, 0x3f807fff, 0xbf818000, 0x7f7fffff, 0xff7fffff,
+                            0x00000001, 0x00008000, 0x00018000, 0x807fffff, 0x80000000, 0x00000000, 0x7f7f8000,
+                            0x477fe000, 0x477ff000], dtype=np.uint32)
+        rng = np.random.default_rng(7)
+        u = rng.integers(0, 2**32, size=n, dtype=np.uint64).astype(np.uint32)
+        u = np.where((u & 0x7f800000) == 0x7f800000, u ^ 0x40000000, u).astype(np.uint32)   # finite inputs only
+        u[:len(special)] = special
+        W = u.view(np.float32)
+        st.set_state(W, np.zeros(n, np.float32))
+        st.predict(1, 0)
+        got = st.get_predicted(0).view(np.uint32) >> 16
+        want = ((u.astype(np.uint64) + 0x7fff + ((u >> 16) & 1)) >> 16).astype(np.uint32)
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, [(hex(u[i]), hex(got[i]), hex(want[i])) for i in bad[:8]]
+        assert want[5] == 0x7f80 and want[7] == 0 and want[9] == 0x0002 and want[11] == 0x8000
+    finally:
+        st.destroy()
