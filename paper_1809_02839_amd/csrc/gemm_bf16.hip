@@ -12,12 +12,14 @@
 // 16-byte MFMA operand read; the 144-byte row pitch puts eight consecutive
 // rows on disjoint banks); R-mode tiles (rows contiguous in memory) are staged
 // as [k][row] as loaded, with the 16-byte units of each 256-byte k row
-// permuted by an XOR with 4 (k mod 4), and transposed by the LDS reads. Global loads run two K steps ahead of
-// the MFMAs (two register stages, two LDS buffers). All global reads are
+// permuted by an XOR with 4 (k mod 4), and transposed by the LDS reads. In
+// the register-staged kernel (the 128 x 64 tiles) global loads run two K
+// steps ahead of the MFMAs (two register stages, two LDS buffers). All
+// global reads are
 // buffer loads whose resource spans exactly the operand tensor: an offset
 // outside it (zero padding of convolutions, ragged tile edges) reads zero.
 //
-// Direct loads (128-wide 4-wave blocks): the buffer loads carry the LDS
+// Direct loads (every 128-wide block, 4 or 8 waves): the buffer loads carry the LDS
 // flag, so each lane's 16 bytes go straight into a two-stage LDS ring at the
 // position fixed by its lane number, with no register stage and no LDS store
 // instruction (LDS stores contend with the MFMA operand reads; direct loads
@@ -26,13 +28,17 @@
 // without padding whose 16-byte chunks are XOR-swizzled by row pairs, R-mode
 // tiles keep the layout above.
 //
-// Epilogue: an unsplit 4-wave launch whose output rows allow 16-byte
-// accesses stages its float32 tile in LDS and then gives each thread eight
+// Epilogue: an unsplit launch whose output rows allow 16-byte accesses
+// stages its float32 tile in LDS and then gives each thread eight
 // consecutive columns of a row, so the residual and mask loads and the output
 // stores of a wave cover whole row segments (an output line is never written
 // piecemeal, which had tripled the HBM write traffic of the bottleneck's
-// 1x1 data gradient); other launches write from the MFMA layout, with every
-// epilogue load of a lane issued before its first store.
+// 1x1 data gradient). Whole tiles whose epilogue has only bf16 operands run
+// straight-line rows compiled for that operand set (the generic rows test
+// every feature per group and issue about one instruction per ten cycles);
+// bf16 rounding uses the conversion instruction. Other launches write from
+// the MFMA layout, with every epilogue load of a lane issued before its
+// first store.
 //
 // Split-K: a 128 x 128 launch may divide K into `splits` ranges; each writes
 // float32 partial tiles to a workspace and an elementwise pass sums the
